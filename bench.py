@@ -1,0 +1,236 @@
+#!/usr/bin/env python3
+"""Benchmark of the HSA forward pass on one MI355X.
+
+A step is one pass of the whole path over one chunk of synthetic input with
+everything resident in HBM: hsa_state_update over every page of the layer
+(cold build of the linear state and page index) followed by hsa_forward
+(query summary, page selection, sparse branch, linear branch, gated merge).
+Default workload: one layer, 12 heads x d128, 4680 queries, 21 history pages
+of 1560 tokens plus the 3 current pages, k_h = 4 (``--config c2``). The
+streaming 30-layer workload is ``--config c5``.
+
+Prints one JSON line. ``value`` is milliseconds per chunk (lower is better);
+the line also carries effective TFLOP/s, per-phase times, the roofline of the
+dominant kernel (the attention kernel inside hsa_forward) and the fp64 oracle
+timed on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def attn_flops(wl, k_eff, n_q):
+    d, P = wl.head_dim, wl.page_size
+    return sum(4.0 * n_q * (k + wl.n_cur) * P * d for k in k_eff) * wl.batch
+
+
+def linear_flops(wl, n_q):
+    return 2.0 * n_q * wl.head_dim ** 2 * wl.heads * wl.batch
+
+
+def state_flops_bytes(wl, n_pages):
+    keys = n_pages * wl.page_size * wl.heads * wl.batch
+    esize = 2 if wl.dtype == "bf16" else 4
+    return 2.0 * keys * wl.head_dim ** 2, keys * 2 * wl.head_dim * esize
+
+
+def time_loop(fn, iters, torch):
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(iters):
+        fn()
+    e.record()
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / iters
+
+
+def cpu_baseline(wl, dev, k_h, heads):
+    """The fp64 oracle on this host's cores over a bounded sample of heads."""
+    import numpy as np
+    from oracle import hsa_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count()
+    host = dict(q=dev["q"].float().cpu().numpy(), k_pool=dev["k_pool"].float().cpu().numpy(),
+                v_pool=dev["v_pool"].float().cpu().numpy(),
+                page_table=dev["page_table"].cpu().numpy())
+    t0 = time.perf_counter()
+    O.hsa_forward(host["q"], host["k_pool"], host["v_pool"], host["page_table"], wl.n_cand,
+                  wl.n_cur, list(k_h), heads=heads)
+    dt = time.perf_counter() - t0
+    scale = wl.heads / len(heads)
+    return {"value": round(dt * scale * 1e3, 1), "unit": "ms/chunk", "cores": int(cores),
+            "kind": "oracle",
+            "sample": f"{len(heads)} of {wl.heads} heads of one {wl.name} chunk (all queries, "
+                      f"cold state), {dt:.1f} s, scaled x{scale:g} to the chunk"}
+
+
+def bench_single(args, wl):
+    import torch
+    from paper_2609_34606_amd import HsaLayer, hsa_page_select
+    from synth_inputs import make_case_torch
+
+    dev = make_case_torch(wl, "cuda:0")
+    torch.cuda.synchronize()
+    q, k_h = dev["q"], [int(x) for x in dev["k_h"]]
+    k_max = max(1, max(k_h))
+    n_q, n_pages = wl.n_q, wl.n_pages
+    layer = HsaLayer(wl.batch, wl.heads, wl.head_dim, wl.page_size, q.dtype, q.device,
+                     k_pool=dev["k_pool"], v_pool=dev["v_pool"], page_table=dev["page_table"])
+    out = torch.empty_like(q)
+    sel = torch.empty((wl.batch, wl.heads, k_max), dtype=torch.int32, device=q.device)
+
+    def step():
+        layer.fold(0, n_pages)
+        layer.forward(q, wl.n_cand, wl.n_cur, k_h, k_max=k_max, out=out)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ms = time_loop(step, args.steps, torch)
+    log(f"step {ms:.4f} ms")
+    # phases, each timed over the same number of launches
+    ms_state = time_loop(lambda: layer.fold(0, n_pages), args.steps, torch)
+    ms_warm = time_loop(lambda: layer.fold(wl.n_cand, wl.n_cur), args.steps, torch)
+    ws = layer.workspace("sel", 1 << 24)
+    ms_sel = time_loop(lambda: hsa_page_select(layer.cfg, q, n_q, layer.page_kmean, layer.max_pages,
+                                               wl.n_cand, k_h, k_max, sel, ws=ws), args.steps, torch)
+    ms_fwd = time_loop(lambda: layer.forward(q, wl.n_cand, wl.n_cur, k_h, k_max=k_max, out=out),
+                       args.steps, torch)
+    ms_attn = max(ms_fwd - ms_sel, 1e-6)
+    k_eff = [min(k, wl.n_cand) for k in k_h]
+    fa = attn_flops(wl, k_eff, n_q)
+    fl = linear_flops(wl, n_q)
+    fs, bs = state_flops_bytes(wl, n_pages)
+    total = fa + fl + fs
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
+    achieved = fa / (ms_attn * 1e-3) / 1e12
+    res = {
+        "metric": "HSA ms/chunk + effective TFLOP/s (MFMA util %) at 12 heads x d128, 4680 queries",
+        "value": round(ms, 4), "unit": "ms/chunk", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": False,
+        "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
+        "effective_tflops": round(total / (ms * 1e-3) / 1e12, 2),
+        "mfma_util_attention": round(achieved / peak, 4),
+        "config": {"workload": wl.name, "batch": wl.batch, "heads": wl.heads,
+                   "head_dim": wl.head_dim, "n_q": n_q, "page_size": wl.page_size,
+                   "history_pages": wl.n_cand, "current_pages": wl.n_cur, "k_h": k_h,
+                   "state": "cold (all pages folded every step)", "parallelism": "single GPU"},
+        "phases_ms": {"state_update_cold": round(ms_state, 4),
+                      "state_update_warm_current_pages": round(ms_warm, 4),
+                      "page_select": round(ms_sel, 4), "forward": round(ms_fwd, 4),
+                      "attention_kernel_est": round(ms_attn, 4)},
+        "state_update_hbm_gbs": round(bs / (ms_state * 1e-3) / 1e9, 1),
+        "state_update_hbm_frac": round(bs / (ms_state * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None,
+                     "kernel": "attn_bf16_kernel<128> (hsa_forward minus hsa_page_select)",
+                     "flops_per_launch": fa},
+    }
+    if not args.no_cpu_baseline:
+        heads = list(range(wl.heads)) if wl.heads * wl.n_pages <= 12 * 24 else [0, 1]
+        log("timing the oracle on the host ...")
+        res["cpu_baseline"] = cpu_baseline(wl, dev, k_h, heads)
+    return res
+
+
+def bench_streaming(args, wl):
+    """30 independent layers x 60 chunks; per chunk each layer folds its 3 new
+    pages into the state and runs HSA over the grown history."""
+    import torch
+    from paper_2609_34606_amd import HsaLayer
+    from synth_inputs import make_case_torch
+    from synth_inputs.configs import streaming_chunk
+
+    L, T = wl.layers if not args.layers else args.layers, wl.chunks if not args.chunks else args.chunks
+    npg = wl.n_cur * T
+    layers, qs = [], []
+    for l in range(L):
+        layer = HsaLayer(wl.batch, wl.heads, wl.head_dim, wl.page_size, torch.bfloat16, "cuda:0",
+                         num_slots=wl.batch * npg, max_pages=npg)
+        layers.append(layer)
+    # all pages and queries are generated up front (untimed)
+    for t in range(1, T + 1):
+        wt = streaming_chunk(wl, t).replace(n_cand=0)
+        for l in range(L):
+            d = make_case_torch(wt, "cuda:0", layer=l, chunk=t, k_pool=layers[l].k_pool,
+                                v_pool=layers[l].v_pool, slot_base=wl.n_cur * (t - 1))
+            layers[l].page_table[:, wl.n_cur * (t - 1):wl.n_cur * t] = d["page_table"]
+            qs.append(d["q"])
+    torch.cuda.synchronize()
+    k_h = list(wl.budgets())
+    outs = [torch.empty_like(qs[0]) for _ in range(L)]
+    per_chunk = []
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    flops = 0.0
+    for t in range(1, T + 1):
+        n_cand = wl.n_cur * (t - 1)
+        s.record()
+        for l in range(L):
+            layers[l].fold(n_cand, wl.n_cur)
+            layers[l].forward(qs[(t - 1) * L + l], n_cand, wl.n_cur, k_h, k_max=max(k_h),
+                              out=outs[l])
+        e.record()
+        torch.cuda.synchronize()
+        per_chunk.append(s.elapsed_time(e))
+        k_eff = [min(k, n_cand) for k in k_h]
+        flops += L * (attn_flops(wl, k_eff, wl.n_q) + linear_flops(wl, wl.n_q) +
+                      state_flops_bytes(wl, wl.n_cur)[0])
+    import numpy as np
+    pc = np.array(per_chunk)
+    ms = float(pc.mean())
+    return {
+        "metric": "HSA ms/chunk + effective TFLOP/s (MFMA util %) at 12 heads x d128, 4680 queries",
+        "value": round(ms, 3), "unit": "ms/chunk (30 layers)", "n_gpus": 1, "steps": T,
+        "warmup": 0, "ms_per_step": round(ms, 3), "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "effective_tflops": round(flops / (pc.sum() * 1e-3) / 1e12, 2),
+        "ms_per_chunk_t_ge_4": round(float(pc[3:].mean()), 3) if T > 3 else None,
+        "config": {"workload": wl.name, "layers": L, "chunks": T, "heads": wl.heads,
+                   "head_dim": wl.head_dim, "n_q": wl.n_q, "page_size": wl.page_size,
+                   "pages_per_chunk": wl.n_cur, "k_h": k_h, "parallelism": "single GPU"},
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="c2", help="c1..c5")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layers", type=int, default=0, help="c5 only: override the layer count")
+    ap.add_argument("--chunks", type=int, default=0, help="c5 only: override the chunk count")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the HSA path here is a single-GPU build "
+              "(sharding over heads or pages is described in the design notes, not implemented); "
+              "run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    from synth_inputs import WORKLOADS
+    wl = WORKLOADS[args.config]
+    res = bench_streaming(args, wl) if wl.layers > 1 else bench_single(args, wl)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,201 @@
+/*
+ * hsa.h -- C ABI of the Hybrid Sparse Attention (HSA) forward pass for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * Method: WorldAttention (arxiv 2609.34606). HSA runs two branches over a
+ * paged KV cache and merges them per head:
+ *   - a linear global branch over the whole history, kept here as a running
+ *     kernelised state (feature map elu(x)+1);
+ *   - a page selector: each head scores every history page by the scaled dot
+ *     product of the chunk's mean query and the page's mean key and keeps its
+ *     top-k_h pages (Sec. 3.2, "Stage 2: page-level retrieval");
+ *   - exact softmax attention over the selected pages plus the current
+ *     chunk's own pages (Sec. 3.3 "Sparse branch"; App. A.1 eq. attention);
+ *   - a sigmoid-gated sum of the two branches (Sec. 3.3 "Gated fusion").
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Pointers named "device" point to GPU memory the caller allocated; the
+ * library never allocates, frees or retains them. "host" pointers are read
+ * during the call only. Every call is asynchronous on `stream` (a hipStream_t
+ * passed as void*; NULL is the null stream) and makes no host synchronisation,
+ * except that with environment variable HSA_CHECK=1 the page table is copied
+ * back and validated first (synchronising the stream).
+ *
+ * Errors: calls return an hsa_status_t. Arguments are validated on the host
+ * before any launch; on an error nothing is launched and no output is
+ * written. Kernels clamp physical slots into [0, num_slots) so that a corrupt
+ * page table cannot fault the GPU (results are then meaningless; HSA_CHECK=1
+ * reports HSA_ERR_OUT_OF_RANGE instead). A launch failure is HSA_ERR_DEVICE.
+ *
+ * Shapes: B batch, H heads (1..64), d head dim (64 or 128), P page size
+ * (a multiple of 8, >= 8), n_q queries in the chunk. Element type of q, k, v
+ * and o is cfg->dtype (bf16 or fp32); statistics are fp32/fp64 as stated.
+ *
+ * Layouts (row-major, innermost last):
+ *   q, o         [B, n_q, H, d]
+ *   pool.k       [num_slots, H, P, d]   key pages
+ *   pool.v       [num_slots, H, d, P]   value pages, stored d-major
+ *   page_table   [B, max_pages] int32   logical page -> physical slot;
+ *                logical pages are in age order (0 = oldest)
+ *   kv_state     [B, H, d, d] fp32      kv_state[b][h][j][i] = sum_t phi(k_t)[i] v_t[j]
+ *   k_state      [B, H, d] fp32         k_state[b][h][i]     = sum_t phi(k_t)[i]
+ *   page_kmean   [B, H, max_pages, d] fp64  mean key of each page
+ *   g_lin, g_sp  [B, n_q, H] fp32       gate logits (nullable: logit 0)
+ *   sel          [B, H, k_max] int32    selected logical pages, -1 padded
+ */
+#ifndef HSA_H_
+#define HSA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HSA_MAX_HEADS 64
+#define HSA_MAX_LIST 1024 /* k_max + n_cur_pages per head */
+#define HSA_MAX_CAND 8192 /* history pages a selection can score */
+
+typedef enum hsa_status {
+  HSA_OK = 0,
+  HSA_ERR_INVALID_ARG = 1, /* NULL pointer, negative size, empty key set */
+  HSA_ERR_UNSUPPORTED = 2, /* valid but not implemented: d, P, H, sizes  */
+  HSA_ERR_OUT_OF_RANGE = 3, /* page outside the pool / page table         */
+  HSA_ERR_WORKSPACE = 4,   /* workspace NULL or smaller than required    */
+  HSA_ERR_DEVICE = 5       /* a HIP call failed                          */
+} hsa_status_t;
+
+typedef enum hsa_dtype { HSA_DTYPE_BF16 = 0, HSA_DTYPE_F32 = 1 } hsa_dtype_t;
+
+typedef struct hsa_config {
+  int32_t batch;     /* B >= 1 */
+  int32_t num_heads; /* H in [1, HSA_MAX_HEADS] */
+  int32_t head_dim;  /* d in {64, 128} */
+  int32_t page_size; /* P >= 8, P % 8 == 0 */
+  int32_t dtype;     /* hsa_dtype_t of q, k, v, o */
+  float sm_scale;    /* softmax scale; 0 means 1/sqrt(d) (App. A.1 eq. attention) */
+} hsa_config_t;
+
+typedef struct hsa_kv_pool {
+  const void* k;              /* device [num_slots, H, P, d] */
+  const void* v;              /* device [num_slots, H, d, P] */
+  const int32_t* page_table;  /* device [B, max_pages] */
+  int32_t num_slots;
+  int32_t max_pages;
+} hsa_kv_pool_t;
+
+/* Human-readable name of a status code (static storage). */
+const char* hsa_status_string(hsa_status_t status);
+
+/* Device workspace, in bytes, each call needs for the given sizes. The
+ * workspace pointer must be 256-byte aligned. Returns 0 on invalid input. */
+size_t hsa_state_update_workspace_size(const hsa_config_t* cfg, int32_t n_pages);
+size_t hsa_page_select_workspace_size(const hsa_config_t* cfg, int32_t n_q);
+size_t hsa_sparse_attn_workspace_size(const hsa_config_t* cfg, int32_t n_q,
+                                      int32_t k_max, int32_t n_cur_pages);
+size_t hsa_forward_workspace_size(const hsa_config_t* cfg, int32_t n_q,
+                                  int32_t k_max, int32_t n_cur_pages);
+
+/*
+ * hsa_state_update -- fold logical pages [first_page, first_page+n_pages) of
+ * every batch entry into the linear-branch state and write their page index.
+ *
+ * Linear state (kernelised running form of the linear branch, Sec. 3.3 with
+ * feature map phi = elu + 1): for every key k_t, value v_t of those pages,
+ *   kv_state[b][h][j][i] += phi(k_t)[i] * v_t[j],   k_state[b][h][i] += phi(k_t)[i].
+ * Page index (Sec. 3.2 Stage 2, "average key" of a page; Sec. 3.2 "L1"
+ * holds page indices built from the keys):
+ *   page_kmean[b][h][p][:] = (1/P) sum_{t<P} K[slot(p)][h][t][:], in fp64.
+ * A cold build is (first_page = 0, n_pages = all pages) on zeroed states; a
+ * streaming step folds only the newly written pages. The result does not
+ * depend on the launch configuration (fixed-order reductions, no atomics).
+ *
+ * kv_state, k_state: device fp32, read-modify-write. page_kmean: device fp64,
+ * rows outside the range untouched. ws: device workspace of
+ * hsa_state_update_workspace_size(cfg, n_pages) bytes. n_pages == 0 is a
+ * no-op. Errors: INVALID_ARG (NULL, bad range), OUT_OF_RANGE (range beyond
+ * max_pages), UNSUPPORTED (d, P), WORKSPACE.
+ */
+hsa_status_t hsa_state_update(const hsa_config_t* cfg, const hsa_kv_pool_t* pool,
+                              int32_t first_page, int32_t n_pages, float* kv_state,
+                              float* k_state, double* page_kmean, void* ws,
+                              size_t ws_bytes, void* stream);
+
+/*
+ * hsa_page_select -- Stage-2 page-level retrieval (Sec. 3.2): per batch entry
+ * and head h, with qbar the mean of the n_q queries of head h and kbar_p the
+ * page's mean key,
+ *   alpha_p = qbar . kbar_p / sqrt(d)   for every candidate page p < n_cand,
+ * and sel[b][h][0..k_eff) = the k_eff = min(k_h[h], n_cand) candidates in
+ * decreasing alpha, equal scores ordered by increasing logical page index;
+ * sel[b][h][k_eff..k_max) = -1. All arithmetic is fp64.
+ *
+ * q: device [B, n_q, H, d] (cfg->dtype). page_kmean: device fp64
+ * [B, H, max_pages, d] (rows [0, n_cand) are read). k_h: host int32 [H],
+ * each in [0, k_max]. sel: device int32 [B, H, k_max]. sel_score: device fp64
+ * [B, H, k_max] or NULL (alpha of each selected page, 0 in padding).
+ * n_cand in [0, min(max_pages, HSA_MAX_CAND)]. ws: device workspace of
+ * hsa_page_select_workspace_size(cfg, n_q) bytes.
+ */
+hsa_status_t hsa_page_select(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                             const double* page_kmean, int32_t max_pages,
+                             int32_t n_cand, const int32_t* k_h, int32_t k_max,
+                             int32_t* sel, double* sel_score, void* ws,
+                             size_t ws_bytes, void* stream);
+
+/*
+ * hsa_sparse_attn -- sparse branch alone (Sec. 3.3; App. A.1 eq. attention
+ * with a zero mask on the active keys): per batch entry and head, the active
+ * keys are the pages sel[b][h][0..) (up to the first entry outside
+ * [0, max_pages)) followed by logical pages [cur_first_page,
+ * cur_first_page + n_cur_pages), with all their P tokens (Sec. 3.2 "Active
+ * KV construction", here a virtual concatenation through the page table).
+ *   o_sp[b][i][h] = sum_j softmax_j(scale * q_i . k_j) v_j   (fp32)
+ *   lse[b][h][i]  = log sum_j exp(scale * q_i . k_j)          (nullable)
+ * k_h: host int32 [H], upper bounds on the valid entries of each sel row
+ * (used for scheduling only; may be NULL meaning k_max). A head whose active
+ * set is empty is an error only if n_cur_pages == 0 and k_max == 0
+ * (INVALID_ARG); otherwise an empty row of sel with n_cur_pages == 0 yields
+ * o_sp = 0 and lse = -inf for that head.
+ * ws: hsa_sparse_attn_workspace_size(cfg, n_q, k_max, n_cur_pages) bytes.
+ */
+hsa_status_t hsa_sparse_attn(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                             const hsa_kv_pool_t* pool, const int32_t* sel,
+                             int32_t k_max, const int32_t* k_h,
+                             int32_t cur_first_page, int32_t n_cur_pages,
+                             float* o_sp, float* lse, void* ws, size_t ws_bytes,
+                             void* stream);
+
+/*
+ * hsa_forward -- the whole HSA forward pass for one chunk:
+ *   1. page selection over candidates [0, n_cand) as hsa_page_select;
+ *   2. sparse branch over the selected pages plus the current pages
+ *      [n_cand, n_cand + n_cur_pages) as hsa_sparse_attn;
+ *   3. linear branch from the running state:
+ *        O_lin[i] = (sum_a phi(q_i)[a] kv_state[j][a]) / (phi(q_i) . k_state);
+ *   4. gated fusion (Sec. 3.3): o = sigmoid(g_lin) O_lin + sigmoid(g_sp) O_sp,
+ *      gates broadcast over d; a NULL gate array means logit 0 (weight 1/2).
+ * The state and page index must already cover the pages (hsa_state_update
+ * over [0, n_cand + n_cur_pages) or its streaming equivalent).
+ *
+ * o: device [B, n_q, H, d] in cfg->dtype. sel_out: device int32
+ * [B, H, k_max] or NULL. k_h: host int32 [H] in [0, k_max]. Errors as
+ * above; n_cand + n_cur_pages must be <= max_pages and each head must have at
+ * least one active page (n_cur_pages >= 1 or k_h[h] >= 1 with n_cand >= 1).
+ * ws: hsa_forward_workspace_size(cfg, n_q, k_max, n_cur_pages) bytes.
+ */
+hsa_status_t hsa_forward(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                         const hsa_kv_pool_t* pool, int32_t n_cand,
+                         int32_t n_cur_pages, const int32_t* k_h, int32_t k_max,
+                         const float* kv_state, const float* k_state,
+                         const double* page_kmean, const float* g_lin,
+                         const float* g_sp, void* o, int32_t* sel_out, void* ws,
+                         size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HSA_H_ */

@@ -1,0 +1,27 @@
+"""MI355X (gfx950) implementation of the HSA forward pass of WorldAttention.
+
+The computation lives in libhsa.so (C ABI in include/hsa.h, HIP kernels in
+csrc/). ``hsa`` is its ctypes binding; ``layer`` holds device buffers of one
+attention layer and calls the binding.
+"""
+from .hsa import (  # noqa: F401
+    HSA_DTYPE_BF16,
+    HSA_DTYPE_F32,
+    HsaConfig,
+    HsaError,
+    HsaKvPool,
+    LibraryNotBuilt,
+    config,
+    hsa_forward,
+    hsa_forward_workspace_size,
+    hsa_page_select,
+    hsa_page_select_workspace_size,
+    hsa_sparse_attn,
+    hsa_sparse_attn_workspace_size,
+    hsa_state_update,
+    hsa_state_update_workspace_size,
+    hsa_status_string,
+    kv_pool,
+    lib,
+)
+from .layer import HsaLayer  # noqa: F401

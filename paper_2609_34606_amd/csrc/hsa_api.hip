@@ -1,0 +1,373 @@
+// C ABI of the HSA library: argument validation, launch planning and
+// workspace layout. Every computation happens in the kernels; this file only
+// checks arguments, sizes the grids and hands pointers over.
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "hsa_kernels.h"
+
+using namespace hsa;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int kStateTargetGroups = 512;  // ~2 workgroups per CU on 256 CUs
+constexpr int kStateMinPartKeys = 256;
+constexpr int kQsumRows = 32;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool check_env() {
+  const char* e = getenv("HSA_CHECK");
+  return e && e[0] == '1';
+}
+
+hsa_status_t check_cfg(const hsa_config_t* c) {
+  if (!c) return HSA_ERR_INVALID_ARG;
+  if (c->batch < 1 || c->num_heads < 1 || c->head_dim < 1 || c->page_size < 1)
+    return HSA_ERR_INVALID_ARG;
+  if (c->dtype != HSA_DTYPE_BF16 && c->dtype != HSA_DTYPE_F32) return HSA_ERR_UNSUPPORTED;
+  if (c->num_heads > HSA_MAX_HEADS) return HSA_ERR_UNSUPPORTED;
+  if (c->head_dim != 64 && c->head_dim != 128) return HSA_ERR_UNSUPPORTED;
+  if (c->page_size < 8 || c->page_size % 8 != 0) return HSA_ERR_UNSUPPORTED;
+  if (!(c->sm_scale >= 0.f) || isinf(c->sm_scale)) return HSA_ERR_INVALID_ARG;
+  return HSA_OK;
+}
+
+hsa_status_t check_pool(const hsa_kv_pool_t* p) {
+  if (!p || !p->k || !p->v || !p->page_table) return HSA_ERR_INVALID_ARG;
+  if (p->num_slots < 1 || p->max_pages < 1) return HSA_ERR_INVALID_ARG;
+  return HSA_OK;
+}
+
+// With HSA_CHECK=1: every page table entry in [first, first+n) must name a
+// slot of the pool.
+hsa_status_t validate_pages(const hsa_config_t* c, const hsa_kv_pool_t* p, int first, int n,
+                            hipStream_t s) {
+  if (!check_env() || n <= 0) return HSA_OK;
+  std::vector<int32_t> pt((size_t)c->batch * p->max_pages);
+  if (hipStreamSynchronize(s) != hipSuccess) return HSA_ERR_DEVICE;
+  if (hipMemcpy(pt.data(), p->page_table, pt.size() * 4, hipMemcpyDeviceToHost) != hipSuccess)
+    return HSA_ERR_DEVICE;
+  for (int b = 0; b < c->batch; ++b)
+    for (int i = first; i < first + n; ++i) {
+      const int32_t slot = pt[(size_t)b * p->max_pages + i];
+      if (slot < 0 || slot >= p->num_slots) return HSA_ERR_OUT_OF_RANGE;
+    }
+  return HSA_OK;
+}
+
+// With HSA_CHECK=1: every selected page (entries up to the first one outside
+// [0, max_pages), as the kernels read them) must map to a slot of the pool.
+hsa_status_t validate_selection(const hsa_config_t* c, const hsa_kv_pool_t* p,
+                                const int32_t* sel, int k_max, hipStream_t s) {
+  if (!check_env() || k_max <= 0) return HSA_OK;
+  const size_t rows = (size_t)c->batch * c->num_heads;
+  std::vector<int32_t> sl(rows * k_max), pt((size_t)c->batch * p->max_pages);
+  if (hipStreamSynchronize(s) != hipSuccess) return HSA_ERR_DEVICE;
+  if (hipMemcpy(sl.data(), sel, sl.size() * 4, hipMemcpyDeviceToHost) != hipSuccess ||
+      hipMemcpy(pt.data(), p->page_table, pt.size() * 4, hipMemcpyDeviceToHost) != hipSuccess)
+    return HSA_ERR_DEVICE;
+  for (size_t r = 0; r < rows; ++r) {
+    const size_t b = r / c->num_heads;
+    for (int i = 0; i < k_max; ++i) {
+      const int32_t e = sl[r * k_max + i];
+      if (e < 0 || e >= p->max_pages) break;
+      const int32_t slot = pt[b * p->max_pages + e];
+      if (slot < 0 || slot >= p->num_slots) return HSA_ERR_OUT_OF_RANGE;
+    }
+  }
+  return HSA_OK;
+}
+
+float softmax_scale(const hsa_config_t* c) {
+  return c->sm_scale > 0.f ? c->sm_scale : 1.f / sqrtf((float)c->head_dim);
+}
+
+struct StatePlan {
+  int parts, part_len, upw, n_groups;
+};
+
+StatePlan plan_state(const hsa_config_t* c, int n_pages) {
+  StatePlan pl{1, c->page_size, 1, n_pages};
+  const long units = (long)c->batch * c->num_heads * n_pages;
+  if (units >= kStateTargetGroups) {
+    pl.upw = (int)(units / kStateTargetGroups);
+    pl.n_groups = (n_pages + pl.upw - 1) / pl.upw;
+  } else if (units > 0) {
+    int parts = (int)((kStateTargetGroups + units - 1) / units);
+    parts = std::min(parts, std::max(1, c->page_size / kStateMinPartKeys));
+    int len = (c->page_size + parts - 1) / parts;
+    len = (len + 7) / 8 * 8;
+    pl.part_len = len;
+    pl.parts = (c->page_size + len - 1) / len;
+    pl.n_groups = n_pages * pl.parts;
+  }
+  return pl;
+}
+
+struct StateWs {
+  size_t s_off, z_off, k_off, total;
+};
+
+StateWs state_ws(const hsa_config_t* c, int n_pages, const StatePlan& pl) {
+  const size_t bh = (size_t)c->batch * c->num_heads, d = c->head_dim;
+  StateWs w;
+  w.s_off = 0;
+  w.z_off = align_up(bh * pl.n_groups * d * d * 4);
+  w.k_off = w.z_off + align_up(bh * pl.n_groups * d * 4);
+  w.total = w.k_off + align_up(bh * (size_t)n_pages * pl.parts * d * 8);
+  return w;
+}
+
+int qsum_splits(int n_q) { return (n_q + kQsumRows - 1) / kQsumRows; }
+
+size_t select_ws_bytes(const hsa_config_t* c, int n_q) {
+  return align_up((size_t)c->batch * qsum_splits(n_q) * c->num_heads * c->head_dim * 8);
+}
+
+hsa_status_t from_hip(hipError_t e) { return e == hipSuccess ? HSA_OK : HSA_ERR_DEVICE; }
+
+hsa_status_t check_ws(void* ws, size_t have, size_t need) {
+  if (need == 0) return HSA_OK;
+  if (!ws || have < need) return HSA_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign) return HSA_ERR_WORKSPACE;
+  return HSA_OK;
+}
+
+hsa_status_t check_budgets(const hsa_config_t* c, const int32_t* k_h, int k_max) {
+  if (k_max < 0) return HSA_ERR_INVALID_ARG;
+  if (!k_h) return HSA_OK;
+  for (int h = 0; h < c->num_heads; ++h)
+    if (k_h[h] < 0 || k_h[h] > k_max) return HSA_ERR_INVALID_ARG;
+  return HSA_OK;
+}
+
+hsa_status_t run_select(const hsa_config_t* c, const void* q, int n_q, const double* kmean,
+                        int max_pages, int n_cand, const int32_t* k_h, int k_max, int32_t* sel,
+                        double* sel_score, void* ws, hipStream_t s) {
+  QsumParams qp{};
+  qp.q = q;
+  qp.n_q = n_q;
+  qp.HD = c->num_heads * c->head_dim;
+  qp.rows_per_split = kQsumRows;
+  qp.n_split = qsum_splits(n_q);
+  qp.ws_qs = static_cast<double*>(ws);
+  SelectParams sp{};
+  sp.ws_qs = qp.ws_qs;
+  sp.page_kmean = kmean;
+  sp.H = c->num_heads;
+  sp.n_q = n_q;
+  sp.n_split = qp.n_split;
+  sp.max_pages = max_pages;
+  sp.n_cand = n_cand;
+  sp.k_max = k_max;
+  for (int h = 0; h < c->num_heads; ++h) sp.k_h[h] = k_h[h];
+  sp.sel = sel;
+  sp.sel_score = sel_score;
+  return from_hip(launch_page_select(c->dtype, c->head_dim, c->batch, qp, sp, s));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* hsa_status_string(hsa_status_t s) {
+  switch (s) {
+    case HSA_OK: return "HSA_OK";
+    case HSA_ERR_INVALID_ARG: return "HSA_ERR_INVALID_ARG";
+    case HSA_ERR_UNSUPPORTED: return "HSA_ERR_UNSUPPORTED";
+    case HSA_ERR_OUT_OF_RANGE: return "HSA_ERR_OUT_OF_RANGE";
+    case HSA_ERR_WORKSPACE: return "HSA_ERR_WORKSPACE";
+    case HSA_ERR_DEVICE: return "HSA_ERR_DEVICE";
+  }
+  return "HSA_ERR_UNKNOWN";
+}
+
+size_t hsa_state_update_workspace_size(const hsa_config_t* cfg, int32_t n_pages) {
+  if (check_cfg(cfg) != HSA_OK || n_pages < 0) return 0;
+  if (n_pages == 0) return 0;
+  return state_ws(cfg, n_pages, plan_state(cfg, n_pages)).total;
+}
+
+size_t hsa_page_select_workspace_size(const hsa_config_t* cfg, int32_t n_q) {
+  if (check_cfg(cfg) != HSA_OK || n_q < 1) return 0;
+  return select_ws_bytes(cfg, n_q);
+}
+
+size_t hsa_sparse_attn_workspace_size(const hsa_config_t* cfg, int32_t n_q, int32_t k_max,
+                                      int32_t n_cur_pages) {
+  if (check_cfg(cfg) != HSA_OK || n_q < 1 || k_max < 0 || n_cur_pages < 0) return 0;
+  return 0;
+}
+
+size_t hsa_forward_workspace_size(const hsa_config_t* cfg, int32_t n_q, int32_t k_max,
+                                  int32_t n_cur_pages) {
+  if (check_cfg(cfg) != HSA_OK || n_q < 1 || k_max < 0 || n_cur_pages < 0) return 0;
+  return select_ws_bytes(cfg, n_q) +
+         align_up((size_t)cfg->batch * cfg->num_heads * std::max(k_max, 1) * 4);
+}
+
+hsa_status_t hsa_state_update(const hsa_config_t* cfg, const hsa_kv_pool_t* pool,
+                              int32_t first_page, int32_t n_pages, float* kv_state,
+                              float* k_state, double* page_kmean, void* ws, size_t ws_bytes,
+                              void* stream) {
+  hsa_status_t st = check_cfg(cfg);
+  if (st != HSA_OK) return st;
+  if ((st = check_pool(pool)) != HSA_OK) return st;
+  if (!kv_state || !k_state || !page_kmean) return HSA_ERR_INVALID_ARG;
+  if (first_page < 0 || n_pages < 0) return HSA_ERR_INVALID_ARG;
+  if ((long)first_page + n_pages > pool->max_pages) return HSA_ERR_OUT_OF_RANGE;
+  if (n_pages == 0) return HSA_OK;
+  const StatePlan pl = plan_state(cfg, n_pages);
+  const StateWs w = state_ws(cfg, n_pages, pl);
+  if ((st = check_ws(ws, ws_bytes, w.total)) != HSA_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = validate_pages(cfg, pool, first_page, n_pages, s)) != HSA_OK) return st;
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  StateParams p{};
+  p.k = pool->k;
+  p.v = pool->v;
+  p.page_table = pool->page_table;
+  p.H = cfg->num_heads;
+  p.P = cfg->page_size;
+  p.num_slots = pool->num_slots;
+  p.max_pages = pool->max_pages;
+  p.first_page = first_page;
+  p.n_pages = n_pages;
+  p.parts = pl.parts;
+  p.part_len = pl.part_len;
+  p.upw = pl.upw;
+  p.n_groups = pl.n_groups;
+  p.ws_S = reinterpret_cast<float*>(base + w.s_off);
+  p.ws_z = reinterpret_cast<float*>(base + w.z_off);
+  p.ws_k = reinterpret_cast<double*>(base + w.k_off);
+  StateReduceParams r{};
+  r.kv_state = kv_state;
+  r.k_state = k_state;
+  r.page_kmean = page_kmean;
+  r.ws_S = p.ws_S;
+  r.ws_z = p.ws_z;
+  r.ws_k = p.ws_k;
+  r.H = cfg->num_heads;
+  r.P = cfg->page_size;
+  r.max_pages = pool->max_pages;
+  r.first_page = first_page;
+  r.n_pages = n_pages;
+  r.parts = pl.parts;
+  r.n_groups = pl.n_groups;
+  return from_hip(launch_state_update(cfg->dtype, cfg->head_dim, cfg->batch, p, r, s));
+}
+
+hsa_status_t hsa_page_select(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                             const double* page_kmean, int32_t max_pages, int32_t n_cand,
+                             const int32_t* k_h, int32_t k_max, int32_t* sel, double* sel_score,
+                             void* ws, size_t ws_bytes, void* stream) {
+  hsa_status_t st = check_cfg(cfg);
+  if (st != HSA_OK) return st;
+  if (!q || !page_kmean || !k_h || !sel) return HSA_ERR_INVALID_ARG;
+  if (n_q < 1 || n_cand < 0 || max_pages < 1 || k_max < 1) return HSA_ERR_INVALID_ARG;
+  if (n_cand > max_pages) return HSA_ERR_OUT_OF_RANGE;
+  if (n_cand > HSA_MAX_CAND) return HSA_ERR_UNSUPPORTED;
+  if ((st = check_budgets(cfg, k_h, k_max)) != HSA_OK) return st;
+  if ((st = check_ws(ws, ws_bytes, select_ws_bytes(cfg, n_q))) != HSA_OK) return st;
+  return run_select(cfg, q, n_q, page_kmean, max_pages, n_cand, k_h, k_max, sel, sel_score, ws,
+                    static_cast<hipStream_t>(stream));
+}
+
+hsa_status_t hsa_sparse_attn(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                             const hsa_kv_pool_t* pool, const int32_t* sel, int32_t k_max,
+                             const int32_t* k_h, int32_t cur_first_page, int32_t n_cur_pages,
+                             float* o_sp, float* lse, void* ws, size_t ws_bytes, void* stream) {
+  hsa_status_t st = check_cfg(cfg);
+  if (st != HSA_OK) return st;
+  if ((st = check_pool(pool)) != HSA_OK) return st;
+  if (!q || !o_sp || n_q < 1 || k_max < 0 || n_cur_pages < 0 || cur_first_page < 0)
+    return HSA_ERR_INVALID_ARG;
+  if (k_max > 0 && !sel) return HSA_ERR_INVALID_ARG;
+  if (k_max == 0 && n_cur_pages == 0) return HSA_ERR_INVALID_ARG;
+  if ((long)cur_first_page + n_cur_pages > pool->max_pages) return HSA_ERR_OUT_OF_RANGE;
+  if ((long)k_max + n_cur_pages > HSA_MAX_LIST) return HSA_ERR_UNSUPPORTED;
+  if ((st = check_budgets(cfg, k_h, k_max)) != HSA_OK) return st;
+  (void)ws;
+  (void)ws_bytes;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = validate_pages(cfg, pool, cur_first_page, n_cur_pages, s)) != HSA_OK) return st;
+  if ((st = validate_selection(cfg, pool, sel, k_max, s)) != HSA_OK) return st;
+  AttnParams p{};
+  p.q = q;
+  p.k = pool->k;
+  p.v = pool->v;
+  p.page_table = pool->page_table;
+  p.sel = sel;  // not read when k_max == 0
+  p.H = cfg->num_heads;
+  p.P = cfg->page_size;
+  p.n_q = n_q;
+  p.num_slots = pool->num_slots;
+  p.max_pages = pool->max_pages;
+  p.k_max = k_max;
+  p.cur_first = cur_first_page;
+  p.n_cur = n_cur_pages;
+  p.sm_scale = softmax_scale(cfg);
+  p.scale_log2 = p.sm_scale * 1.4426950408889634f;
+  p.mode = ATTN_SPARSE;
+  p.o_sp = o_sp;
+  p.lse = lse;
+  return from_hip(launch_attention(cfg->dtype, cfg->head_dim, cfg->batch, p, s));
+}
+
+hsa_status_t hsa_forward(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                         const hsa_kv_pool_t* pool, int32_t n_cand, int32_t n_cur_pages,
+                         const int32_t* k_h, int32_t k_max, const float* kv_state,
+                         const float* k_state, const double* page_kmean, const float* g_lin,
+                         const float* g_sp, void* o, int32_t* sel_out, void* ws, size_t ws_bytes,
+                         void* stream) {
+  hsa_status_t st = check_cfg(cfg);
+  if (st != HSA_OK) return st;
+  if ((st = check_pool(pool)) != HSA_OK) return st;
+  if (!q || !k_h || !kv_state || !k_state || !page_kmean || !o) return HSA_ERR_INVALID_ARG;
+  if (n_q < 1 || n_cand < 0 || n_cur_pages < 0 || k_max < 1) return HSA_ERR_INVALID_ARG;
+  if ((long)n_cand + n_cur_pages > pool->max_pages) return HSA_ERR_OUT_OF_RANGE;
+  if (n_cand > HSA_MAX_CAND) return HSA_ERR_UNSUPPORTED;
+  if ((long)k_max + n_cur_pages > HSA_MAX_LIST) return HSA_ERR_UNSUPPORTED;
+  if ((st = check_budgets(cfg, k_h, k_max)) != HSA_OK) return st;
+  for (int h = 0; h < cfg->num_heads; ++h)
+    if (n_cur_pages == 0 && std::min(k_h[h], n_cand) == 0) return HSA_ERR_INVALID_ARG;
+  const size_t need = hsa_forward_workspace_size(cfg, n_q, k_max, n_cur_pages);
+  if ((st = check_ws(ws, ws_bytes, need)) != HSA_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = validate_pages(cfg, pool, 0, n_cand + n_cur_pages, s)) != HSA_OK) return st;
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  int32_t* sel = sel_out ? sel_out : reinterpret_cast<int32_t*>(base + select_ws_bytes(cfg, n_q));
+  st = run_select(cfg, q, n_q, page_kmean, pool->max_pages, n_cand, k_h, k_max, sel, nullptr, ws, s);
+  if (st != HSA_OK) return st;
+  AttnParams p{};
+  p.q = q;
+  p.k = pool->k;
+  p.v = pool->v;
+  p.page_table = pool->page_table;
+  p.sel = sel;
+  p.H = cfg->num_heads;
+  p.P = cfg->page_size;
+  p.n_q = n_q;
+  p.num_slots = pool->num_slots;
+  p.max_pages = pool->max_pages;
+  p.k_max = k_max;
+  p.cur_first = n_cand;
+  p.n_cur = n_cur_pages;
+  p.sm_scale = softmax_scale(cfg);
+  p.scale_log2 = p.sm_scale * 1.4426950408889634f;
+  p.mode = ATTN_FINAL;
+  p.kv_state = kv_state;
+  p.k_state = k_state;
+  p.g_lin = g_lin;
+  p.g_sp = g_sp;
+  p.o = o;
+  return from_hip(launch_attention(cfg->dtype, cfg->head_dim, cfg->batch, p, s));
+}
+
+}  // extern "C"

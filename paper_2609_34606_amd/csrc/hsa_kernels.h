@@ -1,0 +1,93 @@
+// Kernel parameter blocks and launch entry points of the HSA library.
+// Host-side only; the C ABI (hsa_api.hip) validates arguments, carves the
+// workspace and calls these.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/hsa.h"
+
+namespace hsa {
+
+// ------------------------------------------------------------ state update
+struct StateParams {
+  const void* k;            // [num_slots, H, P, d]
+  const void* v;            // [num_slots, H, d, P]
+  const int32_t* page_table;
+  int32_t H, P, num_slots, max_pages;
+  int32_t first_page, n_pages;
+  int32_t parts;            // parts per page
+  int32_t part_len;         // keys per part (multiple of 8)
+  int32_t upw;              // units (page x part) per workgroup
+  int32_t n_groups;         // workgroups per (b, h)
+  float* ws_S;              // [B*H*n_groups, d, d] partial state, [j][i]
+  float* ws_z;              // [B*H*n_groups, d]
+  double* ws_k;             // [B*H*n_pages*parts, d] partial key sums
+};
+
+struct StateReduceParams {
+  float* kv_state;          // [B, H, d, d]
+  float* k_state;           // [B, H, d]
+  double* page_kmean;       // [B, H, max_pages, d]
+  const float* ws_S;
+  const float* ws_z;
+  const double* ws_k;
+  int32_t H, P, max_pages, first_page, n_pages, parts, n_groups;
+};
+
+hipError_t launch_state_update(int dtype, int d, int B, const StateParams& p,
+                               const StateReduceParams& r, hipStream_t s);
+
+// ------------------------------------------------------------ page select
+struct QsumParams {
+  const void* q;            // [B, n_q, H, d]
+  int32_t n_q, HD;          // HD = H * d
+  int32_t rows_per_split, n_split;
+  double* ws_qs;            // [B, n_split, H*d]
+};
+
+struct SelectParams {
+  const double* ws_qs;      // [B, n_split, H*d]
+  const double* page_kmean; // [B, H, max_pages, d]
+  int32_t H, n_q, n_split, max_pages, n_cand, k_max;
+  int32_t k_h[HSA_MAX_HEADS];
+  int32_t* sel;             // [B, H, k_max]
+  double* sel_score;        // nullable
+};
+
+hipError_t launch_page_select(int dtype, int d, int B, const QsumParams& qp,
+                              const SelectParams& sp, hipStream_t s);
+
+// ------------------------------------------------------------ attention
+enum AttnMode : int32_t {
+  ATTN_FINAL = 0,   // fused linear branch + gated merge, write o (dtype)
+  ATTN_SPARSE = 1,  // write o_sp (fp32) and lse
+};
+
+struct AttnParams {
+  const void* q;            // [B, n_q, H, d]
+  const void* k;            // pool keys
+  const void* v;            // pool values (d-major pages)
+  const int32_t* page_table;
+  const int32_t* sel;       // [B, H, k_max]
+  int32_t H, P, n_q, num_slots, max_pages, k_max;
+  int32_t cur_first, n_cur;
+  float sm_scale;           // softmax scale
+  float scale_log2;         // sm_scale * log2(e)
+  int32_t mode;
+  // final mode
+  const float* kv_state;    // [B, H, d, d]
+  const float* k_state;     // [B, H, d]
+  const float* g_lin;       // [B, n_q, H] nullable
+  const float* g_sp;
+  void* o;                  // [B, n_q, H, d] dtype
+  // sparse mode
+  float* o_sp;              // [B, n_q, H, d]
+  float* lse;               // [B, H, n_q] nullable
+};
+
+hipError_t launch_attention(int dtype, int d, int B, const AttnParams& p,
+                            hipStream_t s);
+
+}  // namespace hsa

@@ -1,0 +1,154 @@
+// Stage-2 page-level retrieval (Sec. 3.2): score every history page of a
+// head by qbar . kbar / sqrt(d) and keep the head's top-k_h pages.
+//
+// Two launches. The first reduces the query chunk to per-split fp64 column
+// sums (the chunk is 14 MB at 4680 x 12 x 128 bf16, so it is read by many
+// workgroups). The second runs one workgroup per (batch, head): it finishes
+// the mean query in a fixed order, scores the candidates in fp64 and takes
+// the top k_h by repeated block-wide arg-max, comparing (score, -index)
+// lexicographically so equal scores keep the older page.
+#include <float.h>
+
+#include "hsa_device.h"
+#include "hsa_kernels.h"
+
+namespace hsa {
+namespace {
+
+template <typename T>
+__device__ __forceinline__ void load8(const T* p, float (&x)[8]);
+
+template <>
+__device__ __forceinline__ void load8<uint16_t>(const uint16_t* p, float (&x)[8]) {
+  const u32x4 v = ld_global16(p);
+  x[0] = bf16_lo(v.x); x[1] = bf16_hi(v.x); x[2] = bf16_lo(v.y); x[3] = bf16_hi(v.y);
+  x[4] = bf16_lo(v.z); x[5] = bf16_hi(v.z); x[6] = bf16_lo(v.w); x[7] = bf16_hi(v.w);
+}
+
+template <>
+__device__ __forceinline__ void load8<float>(const float* p, float (&x)[8]) {
+  const f32x4 a = *reinterpret_cast<const f32x4*>(p);
+  const f32x4 b = *reinterpret_cast<const f32x4*>(p + 4);
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+  x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+
+// Column sums of a block of query rows, fp64: ws_qs[b][split][c].
+template <typename T>
+__global__ __launch_bounds__(256) void qsum_kernel(QsumParams p) {
+  const int b = blockIdx.y, split = blockIdx.x;
+  const int r0 = split * p.rows_per_split;
+  const int r1 = min(p.n_q, r0 + p.rows_per_split);
+  const T* q = static_cast<const T*>(p.q) + (size_t)b * p.n_q * p.HD;
+  const int nvec = p.HD / 8;
+  for (int vc = threadIdx.x; vc < nvec; vc += blockDim.x) {
+    double s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int r = r0; r < r1; ++r) {
+      float x[8];
+      load8<T>(q + (size_t)r * p.HD + vc * 8, x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s[e] += (double)x[e];
+    }
+    double* out = p.ws_qs + ((size_t)b * p.n_split + split) * p.HD + vc * 8;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) out[e] = s[e];
+  }
+}
+
+struct Best {
+  double s;
+  int i;
+};
+
+// (score desc, index asc) order: true if a ranks before b.
+__device__ __forceinline__ bool before(const Best& a, const Best& b) {
+  return a.s > b.s || (a.s == b.s && a.i < b.i);
+}
+
+__device__ __forceinline__ Best shfl_xor_best(Best v, int m) {
+  Best o;
+  o.s = __shfl_xor(v.s, m);
+  o.i = __shfl_xor(v.i, m);
+  return o;
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void select_kernel(SelectParams p) {
+  __shared__ double qbar[D];
+  __shared__ double score[HSA_MAX_CAND];
+  __shared__ uint8_t taken[HSA_MAX_CAND];
+  __shared__ Best wbest[4];
+  const int bh = blockIdx.x, b = bh / p.H, h = bh % p.H;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+  // mean query of head h, summing the splits in order
+  if (tid < D) {
+    double s = 0.0;
+    for (int k = 0; k < p.n_split; ++k)
+      s += p.ws_qs[((size_t)b * p.n_split + k) * (p.H * D) + h * D + tid];
+    qbar[tid] = s / (double)p.n_q;
+  }
+  __syncthreads();
+  const double* km = p.page_kmean + (size_t)bh * p.max_pages * D;
+  for (int c = tid; c < p.n_cand; c += 256) {
+    const double* kr = km + (size_t)c * D;
+    double s = 0.0;
+    for (int d = 0; d < D; ++d) s = fma(qbar[d], kr[d], s);
+    score[c] = s / sqrt((double)D);
+    taken[c] = 0;
+  }
+  __syncthreads();
+
+  const int k_eff = min(p.k_h[h], p.n_cand);
+  int32_t* sel = p.sel + (size_t)bh * p.k_max;
+  double* sc = p.sel_score ? p.sel_score + (size_t)bh * p.k_max : nullptr;
+  for (int r = 0; r < k_eff; ++r) {
+    Best best{-DBL_MAX, INT32_MAX};
+    bool have = false;
+    for (int c = tid; c < p.n_cand; c += 256) {
+      if (taken[c]) continue;
+      const Best cand{score[c], c};
+      if (!have || before(cand, best)) { best = cand; have = true; }
+    }
+    if (!have) best = Best{-DBL_MAX, INT32_MAX};
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+      const Best o = shfl_xor_best(best, m);
+      if (before(o, best)) best = o;
+    }
+    if (lane == 0) wbest[wave] = best;
+    __syncthreads();
+    if (tid == 0) {
+      Best bb = wbest[0];
+      for (int w = 1; w < 4; ++w)
+        if (wbest[w].i < p.n_cand && (bb.i >= p.n_cand || before(wbest[w], bb))) bb = wbest[w];
+      // a NaN score can leave no comparable candidate: pad instead of indexing
+      const bool ok = bb.i >= 0 && bb.i < p.n_cand;
+      if (ok) taken[bb.i] = 1;
+      sel[r] = ok ? bb.i : -1;
+      if (sc) sc[r] = ok ? bb.s : 0.0;
+    }
+    __syncthreads();
+  }
+  for (int r = k_eff + tid; r < p.k_max; r += 256) {
+    sel[r] = -1;
+    if (sc) sc[r] = 0.0;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_page_select(int dtype, int d, int B, const QsumParams& qp,
+                              const SelectParams& sp, hipStream_t s) {
+  const dim3 g1(qp.n_split, B);
+  if (dtype == HSA_DTYPE_BF16) qsum_kernel<uint16_t><<<g1, 256, 0, s>>>(qp);
+  else qsum_kernel<float><<<g1, 256, 0, s>>>(qp);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const dim3 g2(B * sp.H);
+  if (d == 128) select_kernel<128><<<g2, 256, 0, s>>>(sp);
+  else select_kernel<64><<<g2, 256, 0, s>>>(sp);
+  return hipGetLastError();
+}
+
+}  // namespace hsa

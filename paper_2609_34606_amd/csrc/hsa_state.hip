@@ -1,0 +1,297 @@
+// Linear-branch state and page index: one streaming pass over the new pages.
+//
+// For the pages being folded in, every (batch, head) accumulates
+//   kv_state[j][i] += sum_t phi(k_t)[i] v_t[j],  k_state[i] += sum_t phi(k_t)[i]
+// (kernelised linear branch, feature map elu+1) and the mean key of each page
+// (Sec. 3.2, Stage-2 page index) in fp64.
+//
+// The pass is HBM-bound (512 bytes read per key and head against 2*d*d
+// flops, well below the MFMA ridge), so the kernel is built around keeping
+// loads in flight: value pages (stored d-major) go straight from HBM into LDS
+// with global_load_lds, key rows come through registers because they must be
+// transposed (the contraction runs over keys, so both MFMA operands need
+// keys contiguous) and mapped through phi on the way. The contraction is
+// bf16 MFMA with fp32 accumulation; partial states per workgroup are reduced
+// in a fixed order by a second kernel (deterministic, no atomics).
+#include "hsa_device.h"
+#include "hsa_kernels.h"
+
+namespace hsa {
+namespace {
+
+constexpr int kTileKeys = 64;          // keys per LDS tile
+constexpr int kRowBytes = kTileKeys * 2;  // one LDS row: 64 bf16 keys
+
+// LDS rows of 8 x 16-byte chunks; XOR swizzle so that 16 consecutive rows
+// read at the same logical chunk hit distinct bank groups.
+__device__ __forceinline__ int swz8(int row) { return ((row >> 1) ^ (row >> 4)) & 7; }
+
+template <int D>
+struct StateSmem {
+  uint8_t vt[2][D * kRowBytes];   // V^T tile: [d_v][64 keys] bf16
+  uint8_t fk[2][D * kRowBytes];   // phi(K)^T tile: [d_k][64 keys] bf16
+  double red[8 * 128];            // cross-thread reductions (8 KB)
+};
+
+template <int D>
+__global__ __launch_bounds__(256, 2) void state_bf16_kernel(StateParams p) {
+  constexpr int DQ = D / 4;                // 4-wide d groups per key row
+  constexpr int KG = 256 / DQ;             // key groups
+  constexpr int KPT = kTileKeys / KG;      // keys per thread per tile (8 or 4)
+  constexpr int NV = D / 32;               // V^T 1-KB load instructions per wave
+  constexpr int NT = D / 32;               // 32-wide output blocks per dim
+  constexpr int TPW = NT * NT / 4;         // output tiles per wave
+  static_assert(KPT == 8 || KPT == 4, "layout");
+  __shared__ __attribute__((aligned(16))) StateSmem<D> sm;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int bh = blockIdx.x / p.n_groups, grp = blockIdx.x % p.n_groups;
+  const int b = bh / p.H, h = bh % p.H;
+  const int n_units = p.n_pages * p.parts;
+  const int u_begin = grp * p.upw;
+  const int u_end = min(n_units, u_begin + p.upw);
+
+  const uint16_t* __restrict__ kb = static_cast<const uint16_t*>(p.k);
+  const uint16_t* __restrict__ vb = static_cast<const uint16_t*>(p.v);
+
+  const int dq = tid % DQ, kg = tid / DQ;  // K-load role: 4 dims x KPT keys
+
+  f32x16 acc[TPW];
+#pragma unroll
+  for (int t = 0; t < TPW; ++t) acc[t] = f32x16{0};
+  float zacc[4] = {0.f, 0.f, 0.f, 0.f};
+
+  for (int u = u_begin; u < u_end; ++u) {
+    const int page = p.first_page + u / p.parts;
+    const int part = u % p.parts;
+    const int k_beg = part * p.part_len;
+    const int k_end = min(p.P, k_beg + p.part_len);
+    const int slot = clampi(p.page_table[(size_t)b * p.max_pages + page], 0, p.num_slots - 1);
+    const size_t head_base = ((size_t)slot * p.H + h);
+    const uint16_t* kpage = kb + head_base * p.P * D;   // [P][D]
+    const uint16_t* vpage = vb + head_base * D * p.P;   // [D][P]
+    const int ntiles = (k_end - k_beg + kTileKeys - 1) / kTileKeys;
+
+    double kacc[4] = {0.0, 0.0, 0.0, 0.0};
+    u32x2 kr[KPT];
+
+    auto issue = [&](int tile, int buf) {
+      const int k0 = k_beg + tile * kTileKeys;
+      // V^T: NV instructions of 8 rows x 128 bytes per wave
+#pragma unroll
+      for (int n = 0; n < NV; ++n) {
+        const int blk = wave * NV + n;
+        const int r = blk * 8 + (lane >> 3);
+        const int c = (lane & 7) ^ swz8(r);
+        int key = k0 + 8 * c;
+        key = key + 8 <= k_end ? key : k_end - 8;
+        g2lds16(vpage + (size_t)r * p.P + key, &sm.vt[buf][blk * 1024]);
+      }
+      // K rows: KPT keys x 4 dims per thread
+#pragma unroll
+      for (int e = 0; e < KPT; ++e) {
+        int key = k0 + kg * KPT + e;
+        key = key < k_end ? key : k_end - 1;
+        kr[e] = *reinterpret_cast<const u32x2*>(kpage + (size_t)key * D + dq * 4);
+      }
+    };
+
+    issue(0, 0);
+    for (int tile = 0; tile < ntiles; ++tile) {
+      const int cur = tile & 1;
+      const int k0 = k_beg + tile * kTileKeys;
+      wait_vmcnt<0>();
+      // phi, page sums, normaliser; write phi(K)^T into LDS
+      float f[KPT][4];
+#pragma unroll
+      for (int e = 0; e < KPT; ++e) {
+        const bool ok = k0 + kg * KPT + e < k_end;
+        const float x[4] = {bf16_lo(kr[e].x), bf16_hi(kr[e].x), bf16_lo(kr[e].y), bf16_hi(kr[e].y)};
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const float y = ok ? phi(x[c]) : 0.f;
+          f[e][c] = y;
+          zacc[c] += y;
+          kacc[c] += ok ? (double)x[c] : 0.0;
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int row = dq * 4 + c;
+        uint32_t w[KPT / 2];
+#pragma unroll
+        for (int e = 0; e < KPT / 2; ++e) w[e] = pack_bf16(f[2 * e][c], f[2 * e + 1][c]);
+        const int key0 = kg * KPT;                 // first key of this thread
+        const int chunk = key0 >> 3, within = (key0 & 7) * 2;
+        uint8_t* dst = &sm.fk[cur][row * kRowBytes + ((chunk ^ swz8(row)) << 4) + within];
+        if constexpr (KPT == 8) {
+          *reinterpret_cast<u32x4*>(dst) = u32x4{w[0], w[1], w[2], w[3]};
+        } else {
+          *reinterpret_cast<u32x2*>(dst) = u32x2{w[0], w[1]};
+        }
+      }
+      __syncthreads();
+      if (tile + 1 < ntiles) issue(tile + 1, cur ^ 1);
+      // S^T[j][i] += sum_key V^T[j][key] * phiK^T[i][key]
+      const uint8_t* vt = sm.vt[cur];
+      const uint8_t* fk = sm.fk[cur];
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const int chunk = 2 * ks + (lane >> 5);
+#pragma unroll
+        for (int t = 0; t < TPW; ++t) {
+          const int ti = wave * TPW + t;
+          const int mj = ti / NT, ni = ti % NT;
+          const int ra = mj * 32 + (lane & 31);
+          const int rb = ni * 32 + (lane & 31);
+          const u32x4 a = ld_lds16(vt + ra * kRowBytes + ((chunk ^ swz8(ra)) << 4));
+          const u32x4 bb = ld_lds16(fk + rb * kRowBytes + ((chunk ^ swz8(rb)) << 4));
+          acc[t] = mfma32(a, bb, acc[t]);
+        }
+      }
+    }
+    // page-part key sums: reduce over the KG key groups in a fixed order
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < 4; ++c) sm.red[kg * D + dq * 4 + c] = kacc[c];
+    __syncthreads();
+    if (tid < D) {
+      double s = 0.0;
+      for (int g = 0; g < KG; ++g) s += sm.red[g * D + tid];
+      p.ws_k[((size_t)bh * n_units + u) * D + tid] = s;
+    }
+    __syncthreads();
+  }
+
+  // normaliser partial
+  float* redf = reinterpret_cast<float*>(sm.red);
+#pragma unroll
+  for (int c = 0; c < 4; ++c) redf[kg * D + dq * 4 + c] = zacc[c];
+  __syncthreads();
+  const size_t g_index = (size_t)bh * p.n_groups + grp;
+  if (tid < D) {
+    float s = 0.f;
+    for (int g = 0; g < KG; ++g) s += redf[g * D + tid];
+    p.ws_z[g_index * D + tid] = s;
+  }
+  // state partial: lane holds column i = 32 ni + lane%32, rows j of the tile
+  float* out = p.ws_S + g_index * D * D;
+#pragma unroll
+  for (int t = 0; t < TPW; ++t) {
+    const int ti = wave * TPW + t;
+    const int mj = ti / NT, ni = ti % NT;
+    const int i = ni * 32 + (lane & 31);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int j = mj * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      out[j * D + i] = acc[t][r];
+    }
+  }
+}
+
+// fp32 inputs: plain VALU contraction (small shapes; fp32 end to end).
+template <int D>
+__global__ __launch_bounds__(256) void state_f32_kernel(StateParams p) {
+  constexpr int T = 32;
+  constexpr int EPT = D * D / 256;  // state elements per thread (contiguous i)
+  __shared__ float fk[T][D + 1];
+  __shared__ float vt[D][T + 1];
+  __shared__ float kraw[T][D + 1];
+  const int tid = threadIdx.x;
+  const int bh = blockIdx.x / p.n_groups, grp = blockIdx.x % p.n_groups;
+  const int b = bh / p.H, h = bh % p.H;
+  const int n_units = p.n_pages * p.parts;
+  const int u_begin = grp * p.upw, u_end = min(n_units, u_begin + p.upw);
+  const float* kb = static_cast<const float*>(p.k);
+  const float* vb = static_cast<const float*>(p.v);
+  const int j = (tid * EPT) / D, i0 = (tid * EPT) % D;
+  float acc[EPT];
+  for (int e = 0; e < EPT; ++e) acc[e] = 0.f;
+  float zacc = 0.f;
+  for (int u = u_begin; u < u_end; ++u) {
+    const int page = p.first_page + u / p.parts, part = u % p.parts;
+    const int k_beg = part * p.part_len, k_end = min(p.P, k_beg + p.part_len);
+    const int slot = clampi(p.page_table[(size_t)b * p.max_pages + page], 0, p.num_slots - 1);
+    const size_t head_base = (size_t)slot * p.H + h;
+    const float* kpage = kb + head_base * p.P * D;
+    const float* vpage = vb + head_base * D * p.P;
+    double kacc = 0.0;
+    for (int k0 = k_beg; k0 < k_end; k0 += T) {
+      const int nk = min(T, k_end - k0);
+      __syncthreads();
+      for (int x = tid; x < T * D; x += 256) {
+        const int key = x / D, dd = x % D;
+        const float kv = key < nk ? kpage[(size_t)(k0 + key) * D + dd] : 0.f;
+        kraw[key][dd] = kv;
+        fk[key][dd] = key < nk ? phi(kv) : 0.f;
+      }
+      for (int x = tid; x < T * D; x += 256) {
+        const int dd = x / T, key = x % T;
+        vt[dd][key] = key < nk ? vpage[(size_t)dd * p.P + k0 + key] : 0.f;
+      }
+      __syncthreads();
+      if (tid < D) {
+        for (int key = 0; key < nk; ++key) {
+          kacc += (double)kraw[key][tid];
+          zacc += fk[key][tid];
+        }
+      }
+      for (int key = 0; key < nk; ++key) {
+        const float vv = vt[j][key];
+        for (int e = 0; e < EPT; ++e) acc[e] += vv * fk[key][i0 + e];
+      }
+    }
+    if (tid < D) p.ws_k[((size_t)bh * n_units + u) * D + tid] = kacc;
+  }
+  const size_t g_index = (size_t)bh * p.n_groups + grp;
+  if (tid < D) p.ws_z[g_index * D + tid] = zacc;
+  for (int e = 0; e < EPT; ++e) p.ws_S[g_index * D * D + j * D + i0 + e] = acc[e];
+}
+
+// Fixed-order reduction of the partials into the caller's state.
+template <int D>
+__global__ __launch_bounds__(256) void state_reduce_kernel(StateReduceParams r) {
+  const int bh = blockIdx.x;
+  const int e = blockIdx.y * 256 + threadIdx.x;
+  const int nS = D * D, nz = D, nk = r.n_pages * D;
+  if (e < nS) {
+    float s = 0.f;
+    for (int g = 0; g < r.n_groups; ++g) s += r.ws_S[((size_t)bh * r.n_groups + g) * nS + e];
+    r.kv_state[(size_t)bh * nS + e] += s;
+  } else if (e < nS + nz) {
+    const int i = e - nS;
+    float s = 0.f;
+    for (int g = 0; g < r.n_groups; ++g) s += r.ws_z[((size_t)bh * r.n_groups + g) * D + i];
+    r.k_state[(size_t)bh * D + i] += s;
+  } else if (e < nS + nz + nk) {
+    const int x = e - nS - nz;
+    const int pg = x / D, dd = x % D;
+    double s = 0.0;
+    for (int part = 0; part < r.parts; ++part)
+      s += r.ws_k[(((size_t)bh * r.n_pages + pg) * r.parts + part) * D + dd];
+    r.page_kmean[((size_t)bh * r.max_pages + r.first_page + pg) * D + dd] = s / (double)r.P;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_state_update(int dtype, int d, int B, const StateParams& p,
+                               const StateReduceParams& r, hipStream_t s) {
+  const dim3 grid(B * p.H * p.n_groups);
+  if (dtype == HSA_DTYPE_BF16) {
+    if (d == 128) state_bf16_kernel<128><<<grid, 256, 0, s>>>(p);
+    else state_bf16_kernel<64><<<grid, 256, 0, s>>>(p);
+  } else {
+    if (d == 128) state_f32_kernel<128><<<grid, 256, 0, s>>>(p);
+    else state_f32_kernel<64><<<grid, 256, 0, s>>>(p);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int total = d * d + d + p.n_pages * d;
+  const dim3 rgrid(B * p.H, (total + 255) / 256);
+  if (d == 128) state_reduce_kernel<128><<<rgrid, 256, 0, s>>>(r);
+  else state_reduce_kernel<64><<<rgrid, 256, 0, s>>>(r);
+  return hipGetLastError();
+}
+
+}  // namespace hsa

@@ -1,0 +1,203 @@
+"""ctypes binding of libhsa.so (include/hsa.h).
+
+Argument marshalling only: tensors are passed as raw device pointers, the
+per-head budgets as a host int32 array, and the stream as the current torch
+stream. Every step of the computation runs in the library's HIP kernels.
+There is no fallback: if the library is not built, loading it raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib", "libhsa.so")
+
+HSA_DTYPE_BF16 = 0
+HSA_DTYPE_F32 = 1
+STATUS = {0: "HSA_OK", 1: "HSA_ERR_INVALID_ARG", 2: "HSA_ERR_UNSUPPORTED",
+          3: "HSA_ERR_OUT_OF_RANGE", 4: "HSA_ERR_WORKSPACE", 5: "HSA_ERR_DEVICE"}
+
+c_i32, c_vp, c_sz = ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t
+
+
+class HsaConfig(ctypes.Structure):
+    _fields_ = [("batch", c_i32), ("num_heads", c_i32), ("head_dim", c_i32),
+                ("page_size", c_i32), ("dtype", c_i32), ("sm_scale", ctypes.c_float)]
+
+
+class HsaKvPool(ctypes.Structure):
+    _fields_ = [("k", c_vp), ("v", c_vp), ("page_table", c_vp),
+                ("num_slots", c_i32), ("max_pages", c_i32)]
+
+
+class HsaError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn} failed: {STATUS.get(status, status)}")
+        self.status = status
+
+
+class LibraryNotBuilt(RuntimeError):
+    pass
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libhsa.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise LibraryNotBuilt(f"{LIB_PATH} missing: build it with `python -m paper_2609_34606_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    P = ctypes.POINTER
+    L.hsa_status_string.restype = ctypes.c_char_p
+    L.hsa_status_string.argtypes = [ctypes.c_int]
+    for n, extra in (("hsa_state_update_workspace_size", [c_i32]),
+                     ("hsa_page_select_workspace_size", [c_i32]),
+                     ("hsa_sparse_attn_workspace_size", [c_i32, c_i32, c_i32]),
+                     ("hsa_forward_workspace_size", [c_i32, c_i32, c_i32])):
+        f = getattr(L, n)
+        f.restype = c_sz
+        f.argtypes = [P(HsaConfig)] + extra
+    L.hsa_state_update.restype = ctypes.c_int
+    L.hsa_state_update.argtypes = [P(HsaConfig), P(HsaKvPool), c_i32, c_i32, c_vp, c_vp, c_vp,
+                                   c_vp, c_sz, c_vp]
+    L.hsa_page_select.restype = ctypes.c_int
+    L.hsa_page_select.argtypes = [P(HsaConfig), c_vp, c_i32, c_vp, c_i32, c_i32, c_vp, c_i32,
+                                  c_vp, c_vp, c_vp, c_sz, c_vp]
+    L.hsa_sparse_attn.restype = ctypes.c_int
+    L.hsa_sparse_attn.argtypes = [P(HsaConfig), c_vp, c_i32, P(HsaKvPool), c_vp, c_i32, c_vp,
+                                  c_i32, c_i32, c_vp, c_vp, c_vp, c_sz, c_vp]
+    L.hsa_forward.restype = ctypes.c_int
+    L.hsa_forward.argtypes = [P(HsaConfig), c_vp, c_i32, P(HsaKvPool), c_i32, c_i32, c_vp,
+                              c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]
+    _lib = L
+    return L
+
+
+# ------------------------------------------------------------------ helpers
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if hasattr(t, "data_ptr"):
+        if not t.is_contiguous():
+            raise ValueError("tensor arguments must be contiguous")
+        return t.data_ptr()
+    return int(t)
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is not None:
+        return int(stream)
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _budgets(k_h: Optional[Sequence[int]]):
+    if k_h is None:
+        return None, None
+    arr = np.ascontiguousarray(np.asarray(k_h, dtype=np.int32))
+    return arr, arr.ctypes.data_as(c_vp)
+
+
+def _check(fn: str, status: int):
+    if status != 0:
+        raise HsaError(fn, status)
+
+
+def _workspace(nbytes: int, device):
+    import torch
+    if nbytes == 0:
+        return None
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def config(batch: int, num_heads: int, head_dim: int, page_size: int, dtype,
+           sm_scale: float = 0.0) -> HsaConfig:
+    if not isinstance(dtype, int):
+        dtype = HSA_DTYPE_BF16 if str(dtype).endswith("bfloat16") or dtype == "bf16" else HSA_DTYPE_F32
+    return HsaConfig(batch, num_heads, head_dim, page_size, dtype, sm_scale)
+
+
+def kv_pool(k_pool, v_pool, page_table) -> HsaKvPool:
+    return HsaKvPool(_ptr(k_pool), _ptr(v_pool), _ptr(page_table), int(k_pool.shape[0]),
+                     int(page_table.shape[-1]))
+
+
+# ------------------------------------------------------------------ C ABI calls
+def hsa_state_update_workspace_size(cfg: HsaConfig, n_pages: int) -> int:
+    return lib().hsa_state_update_workspace_size(ctypes.byref(cfg), n_pages)
+
+
+def hsa_page_select_workspace_size(cfg: HsaConfig, n_q: int) -> int:
+    return lib().hsa_page_select_workspace_size(ctypes.byref(cfg), n_q)
+
+
+def hsa_sparse_attn_workspace_size(cfg: HsaConfig, n_q: int, k_max: int, n_cur_pages: int) -> int:
+    return lib().hsa_sparse_attn_workspace_size(ctypes.byref(cfg), n_q, k_max, n_cur_pages)
+
+
+def hsa_forward_workspace_size(cfg: HsaConfig, n_q: int, k_max: int, n_cur_pages: int) -> int:
+    return lib().hsa_forward_workspace_size(ctypes.byref(cfg), n_q, k_max, n_cur_pages)
+
+
+def hsa_status_string(status: int) -> str:
+    return lib().hsa_status_string(status).decode()
+
+
+def hsa_state_update(cfg, pool, first_page, n_pages, kv_state, k_state, page_kmean,
+                     ws=None, stream=None, check=True) -> int:
+    if ws is None:
+        ws = _workspace(hsa_state_update_workspace_size(cfg, n_pages), kv_state.device)
+    st = lib().hsa_state_update(ctypes.byref(cfg), ctypes.byref(pool), first_page, n_pages,
+                                _ptr(kv_state), _ptr(k_state), _ptr(page_kmean), _ptr(ws),
+                                0 if ws is None else ws.numel(), _stream(stream))
+    if check:
+        _check("hsa_state_update", st)
+    return st
+
+
+def hsa_page_select(cfg, q, n_q, page_kmean, max_pages, n_cand, k_h, k_max, sel,
+                    sel_score=None, ws=None, stream=None, check=True) -> int:
+    if ws is None:
+        ws = _workspace(hsa_page_select_workspace_size(cfg, n_q), q.device)
+    _keep, kp = _budgets(k_h)
+    st = lib().hsa_page_select(ctypes.byref(cfg), _ptr(q), n_q, _ptr(page_kmean), max_pages,
+                               n_cand, kp, k_max, _ptr(sel), _ptr(sel_score), _ptr(ws),
+                               0 if ws is None else ws.numel(), _stream(stream))
+    if check:
+        _check("hsa_page_select", st)
+    return st
+
+
+def hsa_sparse_attn(cfg, q, n_q, pool, sel, k_max, k_h, cur_first_page, n_cur_pages, o_sp,
+                    lse=None, ws=None, stream=None, check=True) -> int:
+    if ws is None:
+        ws = _workspace(hsa_sparse_attn_workspace_size(cfg, n_q, k_max, n_cur_pages), q.device)
+    _keep, kp = _budgets(k_h)
+    st = lib().hsa_sparse_attn(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool), _ptr(sel),
+                               k_max, kp, cur_first_page, n_cur_pages, _ptr(o_sp), _ptr(lse),
+                               _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream))
+    if check:
+        _check("hsa_sparse_attn", st)
+    return st
+
+
+def hsa_forward(cfg, q, n_q, pool, n_cand, n_cur_pages, k_h, k_max, kv_state, k_state,
+                page_kmean, g_lin, g_sp, o, sel_out=None, ws=None, stream=None,
+                check=True) -> int:
+    if ws is None:
+        ws = _workspace(hsa_forward_workspace_size(cfg, n_q, k_max, n_cur_pages), q.device)
+    _keep, kp = _budgets(k_h)
+    st = lib().hsa_forward(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool), n_cand,
+                           n_cur_pages, kp, k_max, _ptr(kv_state), _ptr(k_state),
+                           _ptr(page_kmean), _ptr(g_lin), _ptr(g_sp), _ptr(o), _ptr(sel_out),
+                           _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream))
+    if check:
+        _check("hsa_forward", st)
+    return st
