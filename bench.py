@@ -219,6 +219,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layers", type=int, default=0, help="c5 only: override the layer count")
     ap.add_argument("--chunks", type=int, default=0, help="c5 only: override the chunk count")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="after the run, copy a MIB-sized device buffer 3 times (a plain copy of "
+                         "known size, to scale HBM byte counters)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -229,6 +232,15 @@ def main():
     from synth_inputs import WORKLOADS
     wl = WORKLOADS[args.config]
     res = bench_streaming(args, wl) if wl.layers > 1 else bench_single(args, wl)
+    if args.copy_calibration:
+        import torch
+        n = args.copy_calibration << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        res["copy_calibration_bytes"] = n
     print(json.dumps(res), flush=True)
 
 

@@ -18,6 +18,7 @@ constexpr size_t kAlign = 256;
 constexpr int kStateTargetGroups = 512;  // ~2 workgroups per CU on 256 CUs
 constexpr int kStateMinPartKeys = 256;
 constexpr int kQsumRows = 32;
+constexpr int kPartPerHead = 4;  // partial slots per head for split key lists
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -130,6 +131,23 @@ size_t select_ws_bytes(const hsa_config_t* c, int n_q) {
   return align_up((size_t)c->batch * qsum_splits(n_q) * c->num_heads * c->head_dim * 8);
 }
 
+size_t sel_ws_bytes(const hsa_config_t* c, int k_max) {
+  return align_up((size_t)c->batch * c->num_heads * std::max(k_max, 1) * 4);
+}
+
+// partial outputs of split key lists (bf16 kernels only)
+size_t partial_ws_bytes(const hsa_config_t* c, int n_q) {
+  if (c->dtype != HSA_DTYPE_BF16) return 0;
+  return attention_partial_bytes(c->batch, c->head_dim, n_q, kPartPerHead * c->num_heads);
+}
+
+void set_partials(AttnParams& p, const hsa_config_t* c, int n_q, void* base) {
+  const size_t cells = (size_t)c->batch * kPartPerHead * c->num_heads * ((n_q + 127) / 128);
+  p.part_o = static_cast<float*>(base);
+  p.part_lse = reinterpret_cast<float*>(static_cast<uint8_t*>(base) +
+                                        align_up(cells * 128 * c->head_dim * 4));
+}
+
 hsa_status_t from_hip(hipError_t e) { return e == hipSuccess ? HSA_OK : HSA_ERR_DEVICE; }
 
 hsa_status_t check_ws(void* ws, size_t have, size_t need) {
@@ -202,14 +220,13 @@ size_t hsa_page_select_workspace_size(const hsa_config_t* cfg, int32_t n_q) {
 size_t hsa_sparse_attn_workspace_size(const hsa_config_t* cfg, int32_t n_q, int32_t k_max,
                                       int32_t n_cur_pages) {
   if (check_cfg(cfg) != HSA_OK || n_q < 1 || k_max < 0 || n_cur_pages < 0) return 0;
-  return 0;
+  return partial_ws_bytes(cfg, n_q);
 }
 
 size_t hsa_forward_workspace_size(const hsa_config_t* cfg, int32_t n_q, int32_t k_max,
                                   int32_t n_cur_pages) {
   if (check_cfg(cfg) != HSA_OK || n_q < 1 || k_max < 0 || n_cur_pages < 0) return 0;
-  return select_ws_bytes(cfg, n_q) +
-         align_up((size_t)cfg->batch * cfg->num_heads * std::max(k_max, 1) * 4);
+  return select_ws_bytes(cfg, n_q) + sel_ws_bytes(cfg, k_max) + partial_ws_bytes(cfg, n_q);
 }
 
 hsa_status_t hsa_state_update(const hsa_config_t* cfg, const hsa_kv_pool_t* pool,
@@ -293,8 +310,7 @@ hsa_status_t hsa_sparse_attn(const hsa_config_t* cfg, const void* q, int32_t n_q
   if ((long)cur_first_page + n_cur_pages > pool->max_pages) return HSA_ERR_OUT_OF_RANGE;
   if ((long)k_max + n_cur_pages > HSA_MAX_LIST) return HSA_ERR_UNSUPPORTED;
   if ((st = check_budgets(cfg, k_h, k_max)) != HSA_OK) return st;
-  (void)ws;
-  (void)ws_bytes;
+  if ((st = check_ws(ws, ws_bytes, partial_ws_bytes(cfg, n_q))) != HSA_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if ((st = validate_pages(cfg, pool, cur_first_page, n_cur_pages, s)) != HSA_OK) return st;
   if ((st = validate_selection(cfg, pool, sel, k_max, s)) != HSA_OK) return st;
@@ -317,6 +333,12 @@ hsa_status_t hsa_sparse_attn(const hsa_config_t* cfg, const void* q, int32_t n_q
   p.mode = ATTN_SPARSE;
   p.o_sp = o_sp;
   p.lse = lse;
+  int list_len[HSA_MAX_HEADS];
+  for (int h = 0; h < cfg->num_heads; ++h)
+    list_len[h] = std::min(k_h ? k_h[h] : k_max, pool->max_pages) + n_cur_pages;
+  plan_attention(p, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
+                 kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16);
+  if (cfg->dtype == HSA_DTYPE_BF16) set_partials(p, cfg, n_q, ws);
   return from_hip(launch_attention(cfg->dtype, cfg->head_dim, cfg->batch, p, s));
 }
 
@@ -343,6 +365,7 @@ hsa_status_t hsa_forward(const hsa_config_t* cfg, const void* q, int32_t n_q,
   if ((st = validate_pages(cfg, pool, 0, n_cand + n_cur_pages, s)) != HSA_OK) return st;
   uint8_t* base = static_cast<uint8_t*>(ws);
   int32_t* sel = sel_out ? sel_out : reinterpret_cast<int32_t*>(base + select_ws_bytes(cfg, n_q));
+  void* partials = base + select_ws_bytes(cfg, n_q) + sel_ws_bytes(cfg, k_max);
   st = run_select(cfg, q, n_q, page_kmean, pool->max_pages, n_cand, k_h, k_max, sel, nullptr, ws, s);
   if (st != HSA_OK) return st;
   AttnParams p{};
@@ -367,6 +390,11 @@ hsa_status_t hsa_forward(const hsa_config_t* cfg, const void* q, int32_t n_q,
   p.g_lin = g_lin;
   p.g_sp = g_sp;
   p.o = o;
+  int list_len[HSA_MAX_HEADS];
+  for (int h = 0; h < cfg->num_heads; ++h) list_len[h] = std::min(k_h[h], n_cand) + n_cur_pages;
+  plan_attention(p, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
+                 kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16);
+  if (cfg->dtype == HSA_DTYPE_BF16) set_partials(p, cfg, n_q, partials);
   return from_hip(launch_attention(cfg->dtype, cfg->head_dim, cfg->batch, p, s));
 }
 

@@ -10,14 +10,21 @@
 //
 // Work decomposition (bf16, d = 128 shown): a workgroup owns 128 queries of
 // one head, four waves of 32 queries each, and walks the head's key list in
-// tiles of 64 keys, double-buffered in LDS. Each wave computes the transposed
-// score tile S^T = K Q^T with 32x32x16 bf16 MFMAs so that a lane holds 32
-// scores of a single query: the running max needs one cross-lane exchange per
-// tile and the accumulator rescale is one multiply per register. The value
-// product is O^T += V^T P^T, reading the d-major value pages directly. Key
-// rows are fed to the score MFMA in a permuted order so that the score
-// registers of a lane already form the bf16 operand of the value MFMA.
+// tiles of 64 keys: key tiles in a 3-slot LDS ring (two in flight while one
+// is computed), value tiles in a 2-slot ring. Each wave computes the transposed score tile S^T = K Q^T with
+// 32x32x16 bf16 MFMAs so that a lane holds 32 scores of a single query: the
+// running max needs one cross-lane exchange per tile and the accumulator
+// rescale is one multiply per register. The value product is O^T += V^T P^T,
+// reading the d-major value pages directly. Key rows are fed to the score
+// MFMA in a permuted order so that the score registers of a lane already form
+// the bf16 operand of the value MFMA. Two workgroups (80 KB of LDS each)
+// share a CU.
 #include <float.h>
+
+#include <algorithm>
+#include <queue>
+#include <utility>
+#include <vector>
 
 #include "hsa_device.h"
 #include "hsa_kernels.h"
@@ -32,24 +39,42 @@ template <int D>
 struct AttnLayout {
   static constexpr int kRowK = 2 * D;                  // bytes per key row
   static constexpr int kChunksK = D / 8;               // 16-byte chunks per key row
-  static constexpr int kKTile = kBN * kRowK;           // K tile bytes
-  static constexpr int kVTile = D * kBN * 2;           // V^T tile bytes
-  static constexpr int kKV = 2 * (kKTile + kVTile);    // double buffer
-  static constexpr int kLin = 2 * D * D * 2;           // state hi + lo (bf16)
+  static constexpr int kKTile = kBN * kRowK;           // key tile bytes
+  static constexpr int kRowV = kBN * 2;                // bytes per value row (64 keys)
+  static constexpr int kVTile = D * kRowV;             // value tile bytes
+  static constexpr int kKStages = 3;                   // key tiles in the ring
+  static constexpr int kVStages = 2;                   // value tiles in the ring
+  static constexpr int kVBase = kKStages * kKTile;
+  static constexpr int kKV = kVBase + kVStages * kVTile;  // 80 KB at d = 128
+  static constexpr int kLinHalf = (D / 2) * D * 2 * 2; // half the state rows, hi + lo
+  static constexpr int kLin = kLinHalf + D * 4;        // + normaliser
   static constexpr int kBytes = kKV > kLin ? kKV : kLin;
-  static constexpr int kRowsPerInstK = 1024 / kRowK;   // K rows per 1-KB load
-  static constexpr int kInstK = kKTile / 1024 / 4;     // K loads per wave
-  static constexpr int kInstV = kVTile / 1024 / 4;     // V^T loads per wave
+  static constexpr int kRowsPerInstK = 1024 / kRowK;   // key rows per 1-KB load
+  static constexpr int kRowsPerInstV = 1024 / kRowV;   // value rows per 1-KB load
+  static constexpr int kInstK = kKTile / 1024 / 4;     // key loads per wave
+  static constexpr int kInstV = kVTile / 1024 / 4;     // value loads per wave
 };
 
-// Swizzle of 16-byte chunks within an LDS row: 16 consecutive rows read at
-// one logical chunk land on distinct bank groups.
+// query tiles per XCD run (see the workgroup-to-item mapping)
+constexpr int kXcdRun = 4;
+
+// Swizzles of 16-byte chunks within LDS rows: 16 consecutive rows read at one
+// logical chunk land on distinct bank groups.
 template <int D>
 __device__ __forceinline__ int swz_k(int row) {
   if constexpr (D == 128) return row & 15;
   else return (row >> 1) & 7;
 }
-__device__ __forceinline__ int swz_v(int row) { return (row >> 1) & 7; }
+__device__ __forceinline__ int swz_v(int row) { return (row >> 1) & 7; }  // 128-byte rows
+
+// Wave priority hooks around the MFMA-heavy phases (no-ops unless a build
+// defines them).
+#ifndef HSA_PRIO_MFMA
+#define HSA_PRIO_MFMA()
+#endif
+#ifndef HSA_PRIO_VALU
+#define HSA_PRIO_VALU()
+#endif
 
 // Score-tile row m holds key perm(m): bits 2 and 3 swapped, so that lane l's
 // score registers 0..7 are keys 8*(l/32)+0..7 and 8..15 are 16+8*(l/32)+0..7.
@@ -57,178 +82,23 @@ __device__ __forceinline__ int key_perm(int m) {
   return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1);
 }
 
-struct PageCursor {
-  int li, off;  // list index and offset within the page of the tile's first key
-};
-
-__device__ __forceinline__ void locate(const PageCursor& base, int x, int P, int& li, int& off) {
-  off = base.off + x;
-  li = base.li;
-  while (off >= P) { off -= P; ++li; }
-}
-
+// Output of one (head, 128-query tile) from its normalised sparse-branch
+// accumulators (acc * inv_l; lane holds query l%32, dims 32m + 8(r/4) +
+// 4(l/32) + r%4) and log-sum-exp. Sparse mode writes O_sp and the LSE;
+// final mode adds the linear branch and the gated fusion:
+//   O_lin^T = S^T phi(Q)^T / (phi(Q) . z), the state split into bf16 hi + lo
+//   parts (~16 bits kept) and staged through LDS in two halves of its rows;
+//   o = sigmoid(g_lin) O_lin + sigmoid(g_sp) O_sp, rounded to bf16.
+// Every thread of the workgroup must call it (it synchronises).
 template <int D>
-__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
+__device__ __forceinline__ void finish(const AttnParams& p, uint8_t* smem, int b, int h, int q_idx,
+                                       const u32x4 (&qf)[D / 16], const f32x16 (&acc)[D / 32],
+                                       float inv_l, float lse) {
   using L = AttnLayout<D>;
-  constexpr int KK = D / 16;   // 16-wide d slices
-  constexpr int NM = D / 32;   // 32-wide d blocks of the output
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[L::kBytes];
-  __shared__ int32_t slots[HSA_MAX_LIST];
-  __shared__ float zs[D];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int l32 = lane & 31, half = lane >> 5;
-  const int qtile = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int H = p.H, P = p.P;
-
-  // ---- key list: selected pages (up to the first invalid entry), then current pages
-  const int32_t* selrow = p.sel + ((size_t)b * H + h) * p.k_max;
-  int n_sel = 0;
-  while (n_sel < p.k_max) {
-    const int e = selrow[n_sel];
-    if (e < 0 || e >= p.max_pages) break;
-    ++n_sel;
-  }
-  const int n_list = n_sel + p.n_cur;
-  for (int i = tid; i < n_list; i += 256) {
-    const int lp = i < n_sel ? selrow[i] : p.cur_first + (i - n_sel);
-    slots[i] = clampi(p.page_table[(size_t)b * p.max_pages + lp], 0, p.num_slots - 1);
-  }
-  const int n_kv = n_list * P;
-  const int ntiles = (n_kv + kBN - 1) / kBN;
-
-  // ---- Q fragment: lane holds query (l%32) of this wave, d = 16kk + 8*half + 0..7
-  const uint16_t* qb = static_cast<const uint16_t*>(p.q);
-  const int q_idx = qtile * kBM + wave * 32 + l32;
-  const int q_ld = min(q_idx, p.n_q - 1);
-  u32x4 qf[KK];
-  {
-    const uint16_t* qrow = qb + (((size_t)b * p.n_q + q_ld) * H + h) * D + 8 * half;
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) qf[kk] = ld_global16(qrow + 16 * kk);
-  }
-  __syncthreads();  // slots visible
-
-  const uint16_t* kpool = static_cast<const uint16_t*>(p.k);
-  const uint16_t* vpool = static_cast<const uint16_t*>(p.v);
-  // buffer b: key tile at smem + b*kKTile, value tile at smem + 2*kKTile + b*kVTile
-
-  auto issue = [&](const PageCursor& cur, int tile, int buf) {
-    const int key0 = tile * kBN;
-#pragma unroll
-    for (int n = 0; n < L::kInstK; ++n) {
-      const int blk = wave * L::kInstK + n;
-      const int r = blk * L::kRowsPerInstK + lane / L::kChunksK;
-      const int c = (lane % L::kChunksK) ^ swz_k<D>(r);
-      int li, off;
-      locate(cur, r, P, li, off);
-      if (key0 + r >= n_kv) { li = n_list - 1; off = P - 1; }
-      const uint16_t* src = kpool + (((size_t)slots[li] * H + h) * P + off) * D + 8 * c;
-      g2lds16(src, smem + buf * L::kKTile + blk * 1024);
-    }
-#pragma unroll
-    for (int n = 0; n < L::kInstV; ++n) {
-      const int blk = wave * L::kInstV + n;
-      const int r = blk * 8 + (lane >> 3);
-      const int c = (lane & 7) ^ swz_v(r);
-      int li, off;
-      locate(cur, 8 * c, P, li, off);
-      if (key0 + 8 * c >= n_kv) { li = n_list - 1; off = P - 8; }
-      const uint16_t* src = vpool + (((size_t)slots[li] * H + h) * D + r) * P + off;
-      g2lds16(src, smem + 2 * L::kKTile + buf * L::kVTile + blk * 1024);
-    }
-  };
-
-  f32x16 acc[NM];
-#pragma unroll
-  for (int m = 0; m < NM; ++m) acc[m] = f32x16{0};
-  float m_run = -INFINITY, l_run = 0.f;
-  const float c2 = p.scale_log2;
-
-  PageCursor cur{0, 0};
-  if (ntiles > 0) issue(cur, 0, 0);
-  const int krow = key_perm(l32);
-  for (int tile = 0; tile < ntiles; ++tile) {
-    const int buf = tile & 1;
-    wait_vmcnt<0>();
-    __syncthreads();
-    PageCursor nxt = cur;
-    nxt.off += kBN;
-    while (nxt.off >= P) { nxt.off -= P; ++nxt.li; }
-    if (tile + 1 < ntiles) issue(nxt, tile + 1, buf ^ 1);
-
-    // S^T = K Q^T for the two 32-key halves of the tile
-    f32x16 s[2];
-    const uint8_t* kt = smem + buf * L::kKTile;
-#pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2) {
-      s[h2] = f32x16{0};
-      const int row = 32 * h2 + krow;
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        const int chunk = 2 * kk + half;
-        const u32x4 a = ld_lds16(kt + row * L::kRowK + ((chunk ^ swz_k<D>(row)) << 4));
-        s[h2] = mfma32(a, qf[kk], s[h2]);
-      }
-    }
-    // mask the tail of the key list
-    if ((tile + 1) * kBN > n_kv) {
-#pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = tile * kBN + 32 * h2 + 16 * (r >> 3) + 8 * half + (r & 7);
-          if (key >= n_kv) s[h2][r] = -INFINITY;
-        }
-    }
-    // online softmax (scores in raw units; exp2 with the folded scale)
-    float mx = s[0][0];
-#pragma unroll
-    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[0][r]);
-#pragma unroll
-    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[1][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c2);
-    const float mc = m_new * c2;
-    float rs = 0.f;
-    u32x4 pb[4];
-#pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2) {
-      float pv[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        pv[r] = __builtin_amdgcn_exp2f(fmaf(s[h2][r], c2, -mc));
-        rs += pv[r];
-      }
-#pragma unroll
-      for (int g = 0; g < 2; ++g)
-        pb[2 * h2 + g] = u32x4{pack_bf16(pv[8 * g + 0], pv[8 * g + 1]), pack_bf16(pv[8 * g + 2], pv[8 * g + 3]),
-                               pack_bf16(pv[8 * g + 4], pv[8 * g + 5]), pack_bf16(pv[8 * g + 6], pv[8 * g + 7])};
-    }
-    l_run = l_run * alpha + rs;
-    m_run = m_new;
-#pragma unroll
-    for (int m = 0; m < NM; ++m) acc[m] *= alpha;
-    // O^T += V^T P^T
-    const uint8_t* vt = smem + 2 * L::kKTile + buf * L::kVTile;
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const int chunk = 2 * ks + half;
-#pragma unroll
-      for (int m = 0; m < NM; ++m) {
-        const int row = 32 * m + l32;
-        const u32x4 a = ld_lds16(vt + row * 128 + ((chunk ^ swz_v(row)) << 4));
-        acc[m] = mfma32(a, pb[ks], acc[m]);
-      }
-    }
-    cur = nxt;
-  }
-
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
-  const float inv_l = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  constexpr int KK = D / 16, NM = D / 32;
+  const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, half = lane >> 5;
+  const int H = p.H;
   const bool q_ok = q_idx < p.n_q;
-
   if (p.mode == ATTN_SPARSE) {
     if (q_ok) {
       float* orow = p.o_sp + (((size_t)b * p.n_q + q_idx) * H + h) * D;
@@ -241,39 +111,34 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
               f32x4{acc[m][4 * g] * inv_l, acc[m][4 * g + 1] * inv_l, acc[m][4 * g + 2] * inv_l,
                     acc[m][4 * g + 3] * inv_l};
         }
-      if (p.lse && half == 0)
-        p.lse[((size_t)b * H + h) * p.n_q + q_idx] =
-            l_tot > 0.f ? m_run * p.sm_scale + __logf(l_tot) : -INFINITY;
+      if (p.lse && half == 0) p.lse[((size_t)b * H + h) * p.n_q + q_idx] = lse;
     }
     return;
   }
-
-  // ---- linear branch: O_lin^T = S^T phi(Q)^T / (phi(Q) . z), state split
-  // into bf16 hi + lo parts so the product keeps ~16 bits of the state.
-  __syncthreads();  // all waves are done with the key/value tiles
+  __syncthreads();  // all waves are done with the shared memory
+  constexpr int RH = D / 2;  // state rows per half
   uint8_t* sh = smem;
-  uint8_t* sl = smem + D * D * 2;
-  {
-    const float* st = p.kv_state + ((size_t)b * H + h) * D * D;
-    for (int e = 4 * tid; e < D * D; e += 1024) {
-      const f32x4 x = *reinterpret_cast<const f32x4*>(st + e);
+  uint8_t* sl = smem + RH * D * 2;
+  float* zs = reinterpret_cast<float*>(smem + L::kLinHalf);
+  if (tid < D) zs[tid] = p.k_state[((size_t)b * H + h) * D + tid];
+  const float* st = p.kv_state + ((size_t)b * H + h) * D * D;
+  auto stage_state = [&](int hf) {
+    for (int e = 4 * tid; e < RH * D; e += 1024) {
+      const f32x4 x = *reinterpret_cast<const f32x4*>(st + (size_t)hf * RH * D + e);
       const int j = e / D, i = e % D;
       const int off = j * (2 * D) + (((i >> 3) ^ swz_k<D>(j)) << 4) + (i & 7) * 2;
       const float hx[4] = {x.x, x.y, x.z, x.w};
-      float lo[4];
       uint32_t hw[2], lw[2];
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        hw[t] = pack_bf16(hx[2 * t], hx[2 * t + 1]);
-        lo[2 * t] = hx[2 * t] - bf16_lo(hw[t]);
-        lo[2 * t + 1] = hx[2 * t + 1] - bf16_hi(hw[t]);
-        lw[t] = pack_bf16(lo[2 * t], lo[2 * t + 1]);
+      for (int q2 = 0; q2 < 2; ++q2) {
+        hw[q2] = pack_bf16(hx[2 * q2], hx[2 * q2 + 1]);
+        lw[q2] = pack_bf16(hx[2 * q2] - bf16_lo(hw[q2]), hx[2 * q2 + 1] - bf16_hi(hw[q2]));
       }
       *reinterpret_cast<u32x2*>(sh + off) = u32x2{hw[0], hw[1]};
       *reinterpret_cast<u32x2*>(sl + off) = u32x2{lw[0], lw[1]};
     }
-    if (tid < D) zs[tid] = p.k_state[((size_t)b * H + h) * D + tid];
-  }
+  };
+  stage_state(0);
   __syncthreads();
   u32x4 fq[KK];
   float den = 0.f;
@@ -282,11 +147,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
     const uint32_t w[4] = {qf[kk].x, qf[kk].y, qf[kk].z, qf[kk].w};
     uint32_t o4[4];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      o4[t] = pack_bf16(phi(bf16_lo(w[t])), phi(bf16_hi(w[t])));
-      const int d0 = 16 * kk + 8 * half + 2 * t;
-      den = fmaf(bf16_lo(o4[t]), zs[d0], den);
-      den = fmaf(bf16_hi(o4[t]), zs[d0 + 1], den);
+    for (int q2 = 0; q2 < 4; ++q2) {
+      o4[q2] = pack_bf16(phi(bf16_lo(w[q2])), phi(bf16_hi(w[q2])));
+      const int d0 = 16 * kk + 8 * half + 2 * q2;
+      den = fmaf(bf16_lo(o4[q2]), zs[d0], den);
+      den = fmaf(bf16_hi(o4[q2]), zs[d0 + 1], den);
     }
     fq[kk] = u32x4{o4[0], o4[1], o4[2], o4[3]};
   }
@@ -299,30 +164,340 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
     if (p.g_sp) wsp = 1.f / (1.f + __expf(-p.g_sp[gi]));
   }
   const float a_lin = wl * inv_den, a_sp = wsp * inv_l;
-  void* orow_v = nullptr;
-  if (q_ok) orow_v = static_cast<uint16_t*>(p.o) + (((size_t)b * p.n_q + q_idx) * H + h) * D;
+  uint16_t* orow = q_ok ? static_cast<uint16_t*>(p.o) + (((size_t)b * p.n_q + q_idx) * H + h) * D
+                        : nullptr;
 #pragma unroll
-  for (int m = 0; m < NM; ++m) {
-    f32x16 al = f32x16{0};
-    const int row = 32 * m + l32;
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      const int off = row * (2 * D) + (((2 * kk + half) ^ swz_k<D>(row)) << 4);
-      al = mfma32(ld_lds16(sh + off), fq[kk], al);
-      al = mfma32(ld_lds16(sl + off), fq[kk], al);
+  for (int hf = 0; hf < 2; ++hf) {
+    if (hf == 1) {
+      __syncthreads();  // every wave is done with the first half
+      stage_state(1);
+      __syncthreads();
     }
-    if (q_ok) {
-      uint16_t* orow = static_cast<uint16_t*>(orow_v);
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int d0 = 32 * m + 8 * g + 4 * half;
-        float v[4];
+    for (int mm = 0; mm < NM / 2; ++mm) {
+      const int m = hf * (NM / 2) + mm;
+      f32x16 al = f32x16{0};
+      const int row = 32 * mm + l32;  // row within the staged half
 #pragma unroll
-        for (int t = 0; t < 4; ++t) v[t] = a_lin * al[4 * g + t] + a_sp * acc[m][4 * g + t];
-        *reinterpret_cast<u32x2*>(orow + d0) = u32x2{pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
+      for (int kk = 0; kk < KK; ++kk) {
+        const int off = row * (2 * D) + (((2 * kk + half) ^ swz_k<D>(row)) << 4);
+        al = mfma32(ld_lds16(sh + off), fq[kk], al);
+        al = mfma32(ld_lds16(sl + off), fq[kk], al);
+      }
+      if (q_ok) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int d0 = 32 * m + 8 * g + 4 * half;
+          float v[4];
+#pragma unroll
+          for (int q2 = 0; q2 < 4; ++q2) v[q2] = a_lin * al[4 * g + q2] + a_sp * acc[m][4 * g + q2];
+          *reinterpret_cast<u32x2*>(orow + d0) = u32x2{pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
+        }
       }
     }
   }
+}
+
+template <int D>
+__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
+  using L = AttnLayout<D>;
+  constexpr int KK = D / 16;   // 16-wide d slices
+  constexpr int NM = D / 32;   // 32-wide d blocks of the output
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[L::kBytes];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
+  const int l32 = lane & 31, half = lane >> 5;
+  const int H = p.H, P = p.P;
+  const int nqt = p.nqt;
+  const int b = blockIdx.y;
+  int qtile, h, split;
+  {
+    // Workgroups go to the 8 XCDs round-robin by id. Deal the items to the
+    // XCDs in runs of kXcdRun consecutive items (consecutive query tiles of
+    // one head and split, which read the same pages through one L2); every
+    // XCD gets a mix of heads. The grid is padded to a multiple of
+    // 8 * kXcdRun; padding workgroups exit here (gridDim.x % 8 == 0, so
+    // blockIdx.x % 8 is the XCD).
+    const int w = blockIdx.x, x = w & 7, k = w >> 3;
+    const int item = (k / kXcdRun) * (8 * kXcdRun) + x * kXcdRun + (k % kXcdRun);
+    if (item >= p.n_items) return;
+    int oh = 0;
+    while (oh + 1 < p.n_order && p.item_off[oh + 1] <= item) ++oh;
+    h = p.head_order[oh];
+    const int local = item - p.item_off[oh];
+    split = local / nqt;
+    qtile = local % nqt;
+  }
+
+  // ---- key list: selected pages (up to the first invalid entry), then current pages
+  const int32_t* selrow = p.sel + ((size_t)b * H + h) * p.k_max;
+  int n_sel = 0;
+  while (n_sel < p.k_max) {
+    const int e = selrow[n_sel];
+    if (e < 0 || e >= p.max_pages) break;
+    ++n_sel;
+  }
+  const int n_list = n_sel + p.n_cur;
+  const int32_t* ptrow = p.page_table + (size_t)b * p.max_pages;
+  auto head_of = [&](int li) -> size_t {
+    const int lp = li < n_sel ? selrow[li] : p.cur_first + (li - n_sel);
+    return (size_t)clampi(ptrow[lp], 0, p.num_slots - 1) * H + h;
+  };
+  // This item's share of the list: split `split` of n_split[h] near-equal
+  // parts of list_len[h] pages (the last split takes whatever the list holds
+  // beyond the plan).
+  const int ns = p.n_split[h];
+  int pg0 = 0, pg1 = n_list;
+  if (ns > 1) {
+    const int len = p.list_len[h], base = len / ns, rem = len % ns;
+    pg0 = min(n_list, split * base + min(split, rem));
+    pg1 = split == ns - 1 ? n_list : min(n_list, pg0 + base + (split < rem ? 1 : 0));
+  }
+  // Key tiles never straddle a page: each page is walked in tiles of 64 keys,
+  // the last one partial when 64 does not divide P.
+  const int tpp = (P + kBN - 1) / kBN;
+  const int ntiles = (pg1 - pg0) * tpp;
+
+  // ---- Q fragment: lane holds query (l%32) of this wave, d = 16kk + 8*half + 0..7
+  const uint16_t* qb = static_cast<const uint16_t*>(p.q);
+  const int q_idx = qtile * kBM + wave * 32 + l32;
+  const int q_ld = min(q_idx, p.n_q - 1);
+  u32x4 qf[KK];
+  {
+    const uint16_t* qrow = qb + (((size_t)b * p.n_q + q_ld) * H + h) * D + 8 * half;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) qf[kk] = ld_global16(qrow + 16 * kk);
+  }
+
+  const uint16_t* kpool = static_cast<const uint16_t*>(p.k);
+  const uint16_t* vpool = static_cast<const uint16_t*>(p.v);
+
+  // Per-lane byte offsets of the tile loads, fixed for the whole walk: key
+  // rows (16-byte chunk c of row r) and value rows (8 keys at chunk c of
+  // d-row r). A partial tile at the end of a page re-reads its last valid
+  // row/group instead of reading past the page.
+  auto k_row = [&](int n) { return (wave * L::kInstK + n) * L::kRowsPerInstK + lane / L::kChunksK; };
+  auto v_row = [&](int n) { return (wave * L::kInstV + n) * L::kRowsPerInstV + (lane >> 3); };
+  auto v_col = [&](int n) { return 8 * ((lane & 7) ^ swz_v(v_row(n))); };
+  uint32_t k_off[L::kInstK], v_off[L::kInstV];
+#pragma unroll
+  for (int n = 0; n < L::kInstK; ++n) {
+    const int r = k_row(n);
+    k_off[n] = (uint32_t)(r * D + 8 * ((lane % L::kChunksK) ^ swz_k<D>(r))) * 2u;
+  }
+#pragma unroll
+  for (int n = 0; n < L::kInstV; ++n) v_off[n] = (uint32_t)(v_row(n) * P + v_col(n)) * 2u;
+
+  // Load cursors: keys run two tiles ahead of the tile being computed
+  // (3-slot ring), values one tile ahead (2-slot ring).
+  int kli = pg0, kt = 0, vli = pg0, vt = 0;
+  size_t khead = pg0 < pg1 ? head_of(pg0) : 0, vhead = khead;
+  auto issue_k = [&](int buf) {
+    const int k0 = kt * kBN, nv = min(kBN, P - k0);
+    const char* src = reinterpret_cast<const char*>(kpool + (khead * P + k0) * D);
+    uint8_t* dst = smem + buf * L::kKTile + wave * L::kInstK * 1024;
+    if (nv == kBN) {
+#pragma unroll
+      for (int n = 0; n < L::kInstK; ++n) g2lds16(src + k_off[n], dst + n * 1024);
+    } else {
+#pragma unroll
+      for (int n = 0; n < L::kInstK; ++n) {
+        const int over = max(0, k_row(n) - (nv - 1));   // rows past the page end
+        g2lds16(src + (k_off[n] - (uint32_t)(over * D * 2)), dst + n * 1024);
+      }
+    }
+    if (++kt == tpp) {
+      kt = 0;
+      if (++kli < pg1) khead = head_of(kli);
+    }
+  };
+  auto issue_v = [&](int buf) {
+    const int k0 = vt * kBN, nv = min(kBN, P - k0);
+    const char* src = reinterpret_cast<const char*>(vpool + vhead * D * P + k0);
+    uint8_t* dst = smem + L::kVBase + buf * L::kVTile + wave * L::kInstV * 1024;
+    if (nv == kBN) {
+#pragma unroll
+      for (int n = 0; n < L::kInstV; ++n) g2lds16(src + v_off[n], dst + n * 1024);
+    } else {
+#pragma unroll
+      for (int n = 0; n < L::kInstV; ++n) {
+        const int over = max(0, v_col(n) - (nv - 8));
+        g2lds16(src + (v_off[n] - (uint32_t)(over * 2)), dst + n * 1024);
+      }
+    }
+    if (++vt == tpp) {
+      vt = 0;
+      if (++vli < pg1) vhead = head_of(vli);
+    }
+  };
+
+  f32x16 acc[NM];
+#pragma unroll
+  for (int m = 0; m < NM; ++m) acc[m] = f32x16{0};
+  float m_run = -INFINITY, l_run = 0.f;
+  const float c2 = p.scale_log2;
+  const int krow = key_perm(l32);
+
+  // prologue: K(0), V(0), K(1)
+  if (ntiles > 0) {
+    issue_k(0);
+    issue_v(0);
+    if (ntiles > 1) issue_k(1);
+  }
+  int t = 0, kbuf = 0;
+  for (int tile = 0; tile < ntiles; ++tile) {
+    // K(tile) and V(tile) have landed once at most the next key tile's loads
+    // are outstanding
+    if (tile + 1 < ntiles) wait_vmcnt<L::kInstK>();
+    else wait_vmcnt<0>();
+    __syncthreads();
+    if (tile + 1 < ntiles) issue_v((tile + 1) & 1);
+    if (tile + 2 < ntiles) issue_k(kbuf == 0 ? 2 : kbuf - 1);   // ring slot (tile+2) % 3
+    const int nv = min(kBN, P - t * kBN);
+
+    // S^T = K Q^T for the two 32-key halves of the tile
+    HSA_PRIO_MFMA();
+    f32x16 s[2];
+    const uint8_t* kt_l = smem + kbuf * L::kKTile;
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+      s[h2] = f32x16{0};
+      const int row = 32 * h2 + krow;
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        const int chunk = 2 * kk + half;
+        const u32x4 a = ld_lds16(kt_l + row * L::kRowK + ((chunk ^ swz_k<D>(row)) << 4));
+        s[h2] = mfma32(a, qf[kk], s[h2]);
+      }
+    }
+    HSA_PRIO_VALU();
+    // keys past the end of the page
+    if (nv < kBN) {
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = 32 * h2 + 16 * (r >> 3) + 8 * half + (r & 7);
+          if (key >= nv) s[h2][r] = -INFINITY;
+        }
+    }
+    // Online softmax against a reference max m_run (raw score units) that
+    // only moves when the tile max exceeds it by more than 8 in exp2 units:
+    // exponentials stay <= 256 and the final normalisation by the row sum is
+    // exact for any reference.
+    float mx = fmaxf(s[0][0], s[0][1]);
+#pragma unroll
+    for (int r = 2; r < 16; ++r) mx = fmaxf(mx, s[0][r]);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[1][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const bool grow = mx * c2 > m_run * c2 + 8.f;
+    if (__any(grow)) {
+      const float m_new = grow ? mx : m_run;
+      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c2);
+      l_run *= alpha;
+#pragma unroll
+      for (int m = 0; m < NM; ++m) acc[m] *= alpha;
+      m_run = m_new;
+    }
+    const float mc = m_run * c2;
+    float rs = 0.f;
+    u32x4 pb[4];
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+      float pv[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        pv[r] = __builtin_amdgcn_exp2f(fmaf(s[h2][r], c2, -mc));
+        rs += pv[r];
+      }
+#pragma unroll
+      for (int g = 0; g < 2; ++g)
+        pb[2 * h2 + g] =
+            u32x4{pack_bf16(pv[8 * g + 0], pv[8 * g + 1]), pack_bf16(pv[8 * g + 2], pv[8 * g + 3]),
+                  pack_bf16(pv[8 * g + 4], pv[8 * g + 5]), pack_bf16(pv[8 * g + 6], pv[8 * g + 7])};
+    }
+    l_run += rs;
+    // O^T += V^T P^T
+    HSA_PRIO_MFMA();
+    const uint8_t* vt_l = smem + L::kVBase + (tile & 1) * L::kVTile;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const int chunk = 2 * ks + half;
+#pragma unroll
+      for (int m = 0; m < NM; ++m) {
+        const int row = 32 * m + l32;
+        const u32x4 a = ld_lds16(vt_l + row * L::kRowV + ((chunk ^ swz_v(row)) << 4));
+        acc[m] = mfma32(a, pb[ks], acc[m]);
+      }
+    }
+    HSA_PRIO_VALU();
+    if (++t == tpp) t = 0;
+    kbuf = kbuf == 2 ? 0 : kbuf + 1;
+  }
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float inv_l = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  const float lse = l_tot > 0.f ? m_run * p.sm_scale + __logf(l_tot) : -INFINITY;
+  if (ns > 1) {
+    // partial result of this split: normalised output and log-sum-exp, in the
+    // accumulator register layout (register-major, lane fastest: coalesced)
+    const size_t cell = (((size_t)b * p.n_part + p.part_base[h] + split) * nqt + qtile) * 4 + wave;
+    float* po = p.part_o + cell * (NM * 16 * 64) + lane;
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) po[(m * 16 + r) * 64] = acc[m][r] * inv_l;
+    p.part_lse[cell * 64 + lane] = lse;
+    return;
+  }
+  finish<D>(p, smem, b, h, qtile * kBM + wave * 32 + l32, qf, acc, inv_l, lse);
+}
+
+// Merge of the splits of one (head, query tile): weights exp(lse_s - max),
+// summed over the splits in order, then the same finish as an unsplit item.
+template <int D>
+__global__ __launch_bounds__(256, 2) void combine_bf16_kernel(AttnParams p) {
+  using L = AttnLayout<D>;
+  constexpr int KK = D / 16, NM = D / 32;
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[L::kLin];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, half = lane >> 5;
+  const int b = blockIdx.y, nqt = p.nqt;
+  const int ch = blockIdx.x / nqt, qtile = blockIdx.x % nqt;
+  const int h = p.c_head[ch], ns = p.n_split[h];
+  const size_t cell0 = (((size_t)b * p.n_part + p.part_base[h]) * nqt + qtile) * 4 + wave;
+  const size_t cstride = (size_t)nqt * 4;  // cells between consecutive splits
+  float lmax = -INFINITY;
+  for (int s = 0; s < ns; ++s) lmax = fmaxf(lmax, p.part_lse[(cell0 + s * cstride) * 64 + lane]);
+  f32x16 acc[NM];
+#pragma unroll
+  for (int m = 0; m < NM; ++m) acc[m] = f32x16{0};
+  float wsum = 0.f;
+  for (int s = 0; s < ns; ++s) {
+    const size_t cell = cell0 + s * cstride;
+    const float ls = p.part_lse[cell * 64 + lane];
+    const float w = ls == -INFINITY ? 0.f : __expf(ls - lmax);
+    wsum += w;
+    const float* po = p.part_o + cell * (NM * 16 * 64) + lane;
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[m][r] = fmaf(w, po[(m * 16 + r) * 64], acc[m][r]);
+  }
+  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+  const float lse = wsum > 0.f ? lmax + __logf(wsum) : -INFINITY;
+  const int q_idx = qtile * kBM + wave * 32 + l32;
+  u32x4 qf[KK];
+  {
+    const int q_ld = min(q_idx, p.n_q - 1);
+    const uint16_t* qrow = static_cast<const uint16_t*>(p.q) + (((size_t)b * p.n_q + q_ld) * p.H + h) * D + 8 * half;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) qf[kk] = ld_global16(qrow + 16 * kk);
+  }
+  finish<D>(p, smem, b, h, q_idx, qf, acc, inv, lse);
 }
 
 // fp32 inputs: VALU attention, 64 queries per workgroup, 4 lanes per query.
@@ -434,11 +609,105 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
 
 }  // namespace
 
+size_t attention_partial_bytes(int B, int d, int n_q, int max_part) {
+  const size_t nqt = (n_q + kBM - 1) / kBM;
+  const size_t cells = (size_t)B * max_part * nqt;
+  const size_t o = cells * kBM * d * 4, l = cells * 4 * 64 * 4;
+  return ((o + 255) / 256 + (l + 255) / 256) * 256;
+}
+
+void plan_attention(AttnParams& p, int H, int d, int n_q, int P, const int* list_len, int max_part,
+                    bool split) {
+  const int nqt = (n_q + kBM - 1) / kBM;
+  const int tpp = (P + kBN - 1) / kBN;
+  // Cost model (units: one 64-key tile of one item on one of 512 slots,
+  // two workgroups on each of 256 CUs): an item costs its tiles plus a fixed
+  // prologue/epilogue; splitting a head adds a combine pass whose time is
+  // dominated by writing and reading the partial outputs.
+  constexpr double kSlots = 512.0, kOverheadTiles = 3.0, kTileUs = 2.4;
+  constexpr double kCombineUsFixed = 8.0, kPartialBytesPerUs = 4.0e6;
+  auto evaluate = [&](int T, int* ns) -> double {
+    int n_part = 0;
+    for (int h = 0; h < H; ++h) {
+      ns[h] = T > 0 ? std::max(1, (list_len[h] + T - 1) / T) : 1;
+      if (ns[h] > 1) n_part += ns[h];
+    }
+    if (n_part > max_part) return 1e30;
+    std::vector<std::pair<double, int>> groups;  // (cost, count)
+    for (int h = 0; h < H; ++h) {
+      const int len = list_len[h], base = len / ns[h], rem = len % ns[h];
+      for (int s = 0; s < ns[h]; ++s)
+        groups.push_back({(base + (s < rem ? 1 : 0)) * (double)tpp + kOverheadTiles, nqt});
+    }
+    std::sort(groups.begin(), groups.end(), [](auto& a, auto& b) { return a.first > b.first; });
+    std::priority_queue<double, std::vector<double>, std::greater<double>> slots;
+    for (int i = 0; i < (int)kSlots; ++i) slots.push(0.0);
+    for (auto& g : groups)
+      for (int i = 0; i < g.second; ++i) {
+        const double t = slots.top();
+        slots.pop();
+        slots.push(t + g.first);
+      }
+    double makespan = 0.0;
+    while (!slots.empty()) {
+      makespan = std::max(makespan, slots.top());
+      slots.pop();
+    }
+    double us = makespan * kTileUs;
+    if (n_part > 0) us += kCombineUsFixed + 2.0 * n_part * nqt * (double)kBM * d * 4 / kPartialBytesPerUs;
+    return us;
+  };
+  int best_ns[HSA_MAX_HEADS], ns[HSA_MAX_HEADS];
+  double best = evaluate(0, best_ns);
+  if (split) {
+    for (int T : {16, 12, 8, 6, 5, 4, 3, 2}) {
+      const double c = evaluate(T, ns);
+      if (c < best * 0.97) {  // split only for a clear gain
+        best = c;
+        std::copy(ns, ns + H, best_ns);
+      }
+    }
+  }
+  p.nqt = nqt;
+  // heads in order of decreasing split size (largest items dispatched first)
+  std::vector<int> order(H);
+  for (int h = 0; h < H; ++h) order[h] = h;
+  auto split_size = [&](int h) { return (list_len[h] + best_ns[h] - 1) / best_ns[h]; };
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return split_size(a) > split_size(b); });
+  p.n_order = H;
+  int items = 0, n_part = 0, n_chead = 0;
+  for (int i = 0; i < H; ++i) {
+    const int h = order[i];
+    p.head_order[i] = h;
+    p.item_off[i] = items;
+    items += best_ns[h] * nqt;
+  }
+  p.item_off[H] = items;
+  p.n_items = items;
+  for (int h = 0; h < H; ++h) {
+    p.n_split[h] = best_ns[h];
+    p.list_len[h] = list_len[h];
+    p.part_base[h] = 0;
+    if (best_ns[h] > 1) {
+      p.part_base[h] = n_part;
+      n_part += best_ns[h];
+      p.c_head[n_chead++] = h;
+    }
+  }
+  p.n_part = n_part;
+  p.n_chead = n_chead;
+}
+
 hipError_t launch_attention(int dtype, int d, int B, const AttnParams& p, hipStream_t s) {
   if (dtype == HSA_DTYPE_BF16) {
-    const dim3 grid((p.n_q + kBM - 1) / kBM, p.H, B);
+    const dim3 grid((p.n_items + 8 * kXcdRun - 1) / (8 * kXcdRun) * (8 * kXcdRun), B);
     if (d == 128) attn_bf16_kernel<128><<<grid, 256, 0, s>>>(p);
     else attn_bf16_kernel<64><<<grid, 256, 0, s>>>(p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || p.n_chead == 0) return e;
+    const dim3 cgrid(p.n_chead * p.nqt, B);
+    if (d == 128) combine_bf16_kernel<128><<<cgrid, 256, 0, s>>>(p);
+    else combine_bf16_kernel<64><<<cgrid, 256, 0, s>>>(p);
   } else {
     const dim3 grid((p.n_q + 63) / 64, p.H, B);
     if (d == 128) attn_f32_kernel<128><<<grid, 256, 0, s>>>(p);

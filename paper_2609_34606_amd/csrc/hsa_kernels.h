@@ -85,7 +85,32 @@ struct AttnParams {
   // sparse mode
   float* o_sp;              // [B, n_q, H, d]
   float* lse;               // [B, H, n_q] nullable
+  // Work schedule of the bf16 kernels (see plan_attention). Attention items
+  // of one batch entry are numbered head by head in head_order, each head
+  // contributing n_split[h] * nqt items (split-major, query tile fastest).
+  int32_t nqt;                           // query tiles of kBM queries
+  int32_t n_items;                       // attention items per batch entry
+  int32_t n_order;                       // heads listed in head_order
+  int32_t head_order[HSA_MAX_HEADS];
+  int32_t item_off[HSA_MAX_HEADS + 1];   // first item of head_order[i]
+  int32_t n_split[HSA_MAX_HEADS];        // splits of head h (by head index)
+  int32_t list_len[HSA_MAX_HEADS];       // pages the splits of head h cover
+  int32_t part_base[HSA_MAX_HEADS];      // first partial slot of head h (n_split > 1)
+  int32_t n_part;                        // partial slots per batch entry
+  float* part_o;                         // [B, n_part, nqt, 4 waves, 16*d/32 regs, 64 lanes]
+  float* part_lse;                       // [B, n_part, nqt, 4 waves, 64 lanes]
+  // combine items: n_chead heads with n_split > 1, nqt items each
+  int32_t n_chead;
+  int32_t c_head[HSA_MAX_HEADS];
 };
+
+// Chooses the split of each head's page list and the item order for
+// list_len[h] pages per head (H heads, head dim d, n_q queries, page size P);
+// at most max_part partial slots. split = false keeps every head whole.
+void plan_attention(AttnParams& p, int H, int d, int n_q, int P, const int* list_len,
+                    int max_part, bool split);
+// Workspace bytes for max_part partial slots.
+size_t attention_partial_bytes(int B, int d, int n_q, int max_part);
 
 hipError_t launch_attention(int dtype, int d, int B, const AttnParams& p,
                             hipStream_t s);

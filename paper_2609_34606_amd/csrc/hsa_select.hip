@@ -33,7 +33,9 @@ __device__ __forceinline__ void load8<float>(const float* p, float (&x)[8]) {
   x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
 }
 
-// Column sums of a block of query rows, fp64: ws_qs[b][split][c].
+// Column sums of a block of query rows, fp64: ws_qs[b][split][c]. Rows are
+// read eight at a time so that the loads are in flight together; the sum
+// still runs over the rows in increasing order.
 template <typename T>
 __global__ __launch_bounds__(256) void qsum_kernel(QsumParams p) {
   const int b = blockIdx.y, split = blockIdx.x;
@@ -43,7 +45,17 @@ __global__ __launch_bounds__(256) void qsum_kernel(QsumParams p) {
   const int nvec = p.HD / 8;
   for (int vc = threadIdx.x; vc < nvec; vc += blockDim.x) {
     double s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    for (int r = r0; r < r1; ++r) {
+    int r = r0;
+    for (; r + 8 <= r1; r += 8) {
+      float x[8][8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) load8<T>(q + (size_t)(r + u) * p.HD + vc * 8, x[u]);
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s[e] += (double)x[u][e];
+    }
+    for (; r < r1; ++r) {
       float x[8];
       load8<T>(q + (size_t)r * p.HD + vc * 8, x);
 #pragma unroll
@@ -74,6 +86,8 @@ __device__ __forceinline__ Best shfl_xor_best(Best v, int m) {
 
 template <int D>
 __global__ __launch_bounds__(256) void select_kernel(SelectParams p) {
+  constexpr int DS = D / 16;  // d values per lane when 16 lanes share a candidate
+  __shared__ double qparts[4][D];
   __shared__ double qbar[D];
   __shared__ double score[HSA_MAX_CAND];
   __shared__ uint8_t taken[HSA_MAX_CAND];
@@ -81,27 +95,96 @@ __global__ __launch_bounds__(256) void select_kernel(SelectParams p) {
   const int bh = blockIdx.x, b = bh / p.H, h = bh % p.H;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
 
-  // mean query of head h, summing the splits in order
-  if (tid < D) {
-    double s = 0.0;
-    for (int k = 0; k < p.n_split; ++k)
-      s += p.ws_qs[((size_t)b * p.n_split + k) * (p.H * D) + h * D + tid];
-    qbar[tid] = s / (double)p.n_q;
+  // mean query of head h: two threads per column each sum half of the splits
+  // (in order), then the halves are added in a fixed order
+  {
+    const int col = tid % D, part = tid / D;  // D = 128: parts 0, 1; D = 64: 0..3
+    const int nparts = 256 / D;
+    const int per = (p.n_split + nparts - 1) / nparts;
+    const int k0 = part * per, k1 = min(p.n_split, k0 + per);
+    const double* src = p.ws_qs + (size_t)b * p.n_split * (p.H * D) + h * D + col;
+    double sacc = 0.0;
+    int k = k0;
+    for (; k + 8 <= k1; k += 8) {
+      double x[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) x[u] = src[(size_t)(k + u) * (p.H * D)];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) sacc += x[u];
+    }
+    for (; k < k1; ++k) sacc += src[(size_t)k * (p.H * D)];
+    qparts[part][col] = sacc;
+    __syncthreads();
+    if (tid < D) {
+      double t = 0.0;
+      for (int q = 0; q < nparts; ++q) t += qparts[q][tid];
+      qbar[tid] = t / (double)p.n_q;
+    }
+    __syncthreads();
   }
-  __syncthreads();
+
+  // scores: 16 lanes per candidate, DS consecutive dims each, reduced in a
+  // fixed butterfly order
   const double* km = p.page_kmean + (size_t)bh * p.max_pages * D;
-  for (int c = tid; c < p.n_cand; c += 256) {
-    const double* kr = km + (size_t)c * D;
-    double s = 0.0;
-    for (int d = 0; d < D; ++d) s = fma(qbar[d], kr[d], s);
-    score[c] = s / sqrt((double)D);
-    taken[c] = 0;
+  const int sub = tid & 15;
+  double qv[DS];
+#pragma unroll
+  for (int e = 0; e < DS; ++e) qv[e] = qbar[sub * DS + e];
+  const double rsd = sqrt((double)D);
+  for (int c0 = 0; c0 < p.n_cand; c0 += 16 * 2) {
+    double part[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int c = c0 + u * 16 + (tid >> 4);
+      part[u] = 0.0;
+      if (c < p.n_cand) {
+        const double* kr = km + (size_t)c * D + sub * DS;
+#pragma unroll
+        for (int e = 0; e < DS; ++e) part[u] = fma(qv[e], kr[e], part[u]);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      double v = part[u];
+      v += __shfl_xor(v, 8);
+      v += __shfl_xor(v, 4);
+      v += __shfl_xor(v, 2);
+      v += __shfl_xor(v, 1);
+      const int c = c0 + u * 16 + (tid >> 4);
+      if (sub == 0 && c < p.n_cand) {
+        score[c] = v / rsd;
+        taken[c] = 0;
+      }
+    }
   }
   __syncthreads();
 
   const int k_eff = min(p.k_h[h], p.n_cand);
   int32_t* sel = p.sel + (size_t)bh * p.k_max;
   double* sc = p.sel_score ? p.sel_score + (size_t)bh * p.k_max : nullptr;
+  for (int r = k_eff + tid; r < p.k_max; r += 256) {
+    sel[r] = -1;
+    if (sc) sc[r] = 0.0;
+  }
+  if (k_eff == 0) return;
+  if (p.n_cand <= 2048) {
+    // rank of each candidate in the (score desc, index asc) order; ranks are
+    // a permutation for comparable scores (rows start at -1 in case a NaN
+    // score breaks that)
+    for (int r = tid; r < k_eff; r += 256) sel[r] = -1;
+    __syncthreads();
+    for (int c = tid; c < p.n_cand; c += 256) {
+      const Best me{score[c], c};
+      int rank = 0;
+      for (int o = 0; o < p.n_cand; ++o) rank += before(Best{score[o], o}, me) ? 1 : 0;
+      if (rank < k_eff) {
+        sel[rank] = c;
+        if (sc) sc[rank] = me.s;
+      }
+    }
+    return;
+  }
+  // long candidate lists: k_eff rounds of block-wide arg-max
   for (int r = 0; r < k_eff; ++r) {
     Best best{-DBL_MAX, INT32_MAX};
     bool have = false;
@@ -129,10 +212,6 @@ __global__ __launch_bounds__(256) void select_kernel(SelectParams p) {
       if (sc) sc[r] = ok ? bb.s : 0.0;
     }
     __syncthreads();
-  }
-  for (int r = k_eff + tid; r < p.k_max; r += 256) {
-    sel[r] = -1;
-    if (sc) sc[r] = 0.0;
   }
 }
 

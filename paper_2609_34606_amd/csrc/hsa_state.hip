@@ -248,28 +248,48 @@ __global__ __launch_bounds__(256) void state_f32_kernel(StateParams p) {
   for (int e = 0; e < EPT; ++e) p.ws_S[g_index * D * D + j * D + i0 + e] = acc[e];
 }
 
-// Fixed-order reduction of the partials into the caller's state.
+// Fixed-order reduction of the partials into the caller's state: each thread
+// owns 16 bytes of the output and adds the partials in increasing order,
+// eight loads in flight at a time.
+typedef double f64x2 __attribute__((ext_vector_type(2)));
+
+template <typename V>
+__device__ __forceinline__ V sum_groups(const V* src, size_t stride, int n) {
+  V s = V{0};
+  int g = 0;
+  for (; g + 8 <= n; g += 8) {
+    V x[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) x[u] = src[(size_t)(g + u) * stride];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s += x[u];
+  }
+  for (; g < n; ++g) s += src[(size_t)g * stride];
+  return s;
+}
+
 template <int D>
 __global__ __launch_bounds__(256) void state_reduce_kernel(StateReduceParams r) {
+  constexpr int nS = D * D / 4, nz = D / 4;  // in float4 units
   const int bh = blockIdx.x;
   const int e = blockIdx.y * 256 + threadIdx.x;
-  const int nS = D * D, nz = D, nk = r.n_pages * D;
+  const int nk = r.n_pages * D / 2;          // in double2 units
   if (e < nS) {
-    float s = 0.f;
-    for (int g = 0; g < r.n_groups; ++g) s += r.ws_S[((size_t)bh * r.n_groups + g) * nS + e];
-    r.kv_state[(size_t)bh * nS + e] += s;
+    const f32x4* src = reinterpret_cast<const f32x4*>(r.ws_S) + (size_t)bh * r.n_groups * nS + e;
+    f32x4* dst = reinterpret_cast<f32x4*>(r.kv_state) + (size_t)bh * nS + e;
+    *dst += sum_groups(src, nS, r.n_groups);
   } else if (e < nS + nz) {
     const int i = e - nS;
-    float s = 0.f;
-    for (int g = 0; g < r.n_groups; ++g) s += r.ws_z[((size_t)bh * r.n_groups + g) * D + i];
-    r.k_state[(size_t)bh * D + i] += s;
+    const f32x4* src = reinterpret_cast<const f32x4*>(r.ws_z) + (size_t)bh * r.n_groups * nz + i;
+    f32x4* dst = reinterpret_cast<f32x4*>(r.k_state) + (size_t)bh * nz + i;
+    *dst += sum_groups(src, nz, r.n_groups);
   } else if (e < nS + nz + nk) {
     const int x = e - nS - nz;
-    const int pg = x / D, dd = x % D;
-    double s = 0.0;
-    for (int part = 0; part < r.parts; ++part)
-      s += r.ws_k[(((size_t)bh * r.n_pages + pg) * r.parts + part) * D + dd];
-    r.page_kmean[((size_t)bh * r.max_pages + r.first_page + pg) * D + dd] = s / (double)r.P;
+    const int pg = x / (D / 2), dd = x % (D / 2);
+    const f64x2* src = reinterpret_cast<const f64x2*>(r.ws_k) + ((size_t)bh * r.n_pages + pg) * r.parts * (D / 2) + dd;
+    const f64x2 s = sum_groups(src, D / 2, r.parts);
+    f64x2* dst = reinterpret_cast<f64x2*>(r.page_kmean) + ((size_t)bh * r.max_pages + r.first_page + pg) * (D / 2) + dd;
+    *dst = s / (double)r.P;
   }
 }
 
@@ -287,7 +307,7 @@ hipError_t launch_state_update(int dtype, int d, int B, const StateParams& p,
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int total = d * d + d + p.n_pages * d;
+  const int total = d * d / 4 + d / 4 + p.n_pages * d / 2;
   const dim3 rgrid(B * p.H, (total + 255) / 256);
   if (d == 128) state_reduce_kernel<128><<<rgrid, 256, 0, s>>>(r);
   else state_reduce_kernel<64><<<rgrid, 256, 0, s>>>(r);
