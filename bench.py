@@ -60,6 +60,37 @@ def time_loop(fn, iters, torch):
     return s.elapsed_time(e) / iters
 
 
+def kernel_source_hash() -> str:
+    """Hash of the attention kernel sources; HBM traffic figures measured with
+    rocprofv3 counters apply only to the sources they were measured on."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("hsa_attn.hip", "hsa_device.h"):
+        with open(os.path.join(ROOT, "paper_2609_34606_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per attention launch from the committed counter summary of
+    this workload, if it was taken on the current kernel sources, else None."""
+    path = os.path.join(ROOT, "profiles", f"attn_{workload}_hbm_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    try:
+        return int(float(kv["hbm_bytes_per_launch"]))
+    except (KeyError, ValueError):
+        return None
+
+
 def cpu_baseline(wl, dev, k_h, heads):
     """The fp64 oracle on this host's cores over a bounded sample of heads."""
     import numpy as np
@@ -115,7 +146,11 @@ def bench_single(args, wl):
                                                wl.n_cand, k_h, k_max, sel, ws=ws), args.steps, torch)
     ms_fwd = time_loop(lambda: layer.forward(q, wl.n_cand, wl.n_cur, k_h, k_max=k_max, out=out),
                        args.steps, torch)
-    ms_attn = max(ms_fwd - ms_sel, 1e-6)
+    # the attention launch alone: sparse branch + linear branch + merge for the
+    # selection just computed (one kernel, plus a combine kernel when the
+    # schedule splits long page lists)
+    ms_attn = time_loop(lambda: layer.forward_selected(q, sel, wl.n_cand, wl.n_cur, k_h, k_max=k_max,
+                                                       out=out), args.steps, torch)
     k_eff = [min(k, wl.n_cand) for k in k_h]
     fa = attn_flops(wl, k_eff, n_q)
     fl = linear_flops(wl, n_q)
@@ -137,12 +172,13 @@ def bench_single(args, wl):
         "phases_ms": {"state_update_cold": round(ms_state, 4),
                       "state_update_warm_current_pages": round(ms_warm, 4),
                       "page_select": round(ms_sel, 4), "forward": round(ms_fwd, 4),
-                      "attention_kernel_est": round(ms_attn, 4)},
+                      "attention_launch": round(ms_attn, 4)},
         "state_update_hbm_gbs": round(bs / (ms_state * 1e-3) / 1e9, 1),
         "state_update_hbm_frac": round(bs / (ms_state * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
-                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None,
-                     "kernel": "attn_bf16_kernel<128> (hsa_forward minus hsa_page_select)",
+                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                     "traffic": measured_traffic(wl.name),
+                     "kernel": "attn_bf16_kernel (hsa_forward_selected launch)",
                      "flops_per_launch": fa},
     }
     if not args.no_cpu_baseline:

@@ -194,6 +194,23 @@ hsa_status_t hsa_forward(const hsa_config_t* cfg, const void* q, int32_t n_q,
                          const float* g_sp, void* o, int32_t* sel_out, void* ws,
                          size_t ws_bytes, void* stream);
 
+/*
+ * hsa_forward_selected -- steps 2-4 of hsa_forward for a page selection the
+ * caller already holds (for instance from hsa_page_select): the sparse branch
+ * over sel[b][h] (entries up to the first one outside [0, max_pages)) plus the
+ * current pages [n_cand, n_cand + n_cur_pages), the linear branch and the
+ * gated fusion. hsa_forward is hsa_page_select followed by this call.
+ * sel: device int32 [B, H, k_max]. k_h: host int32 [H], upper bounds on the
+ * valid entries of each row (the work split is planned from them). Other
+ * arguments as hsa_forward. ws: hsa_forward_workspace_size(...) bytes.
+ */
+hsa_status_t hsa_forward_selected(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                                  const hsa_kv_pool_t* pool, const int32_t* sel,
+                                  int32_t k_max, const int32_t* k_h, int32_t n_cand,
+                                  int32_t n_cur_pages, const float* kv_state,
+                                  const float* k_state, const float* g_lin, const float* g_sp,
+                                  void* o, void* ws, size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

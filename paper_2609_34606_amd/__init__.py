@@ -13,6 +13,7 @@ from .hsa import (  # noqa: F401
     LibraryNotBuilt,
     config,
     hsa_forward,
+    hsa_forward_selected,
     hsa_forward_workspace_size,
     hsa_page_select,
     hsa_page_select_workspace_size,

@@ -342,16 +342,19 @@ hsa_status_t hsa_sparse_attn(const hsa_config_t* cfg, const void* q, int32_t n_q
   return from_hip(launch_attention(cfg->dtype, cfg->head_dim, cfg->batch, p, s));
 }
 
-hsa_status_t hsa_forward(const hsa_config_t* cfg, const void* q, int32_t n_q,
-                         const hsa_kv_pool_t* pool, int32_t n_cand, int32_t n_cur_pages,
-                         const int32_t* k_h, int32_t k_max, const float* kv_state,
-                         const float* k_state, const double* page_kmean, const float* g_lin,
-                         const float* g_sp, void* o, int32_t* sel_out, void* ws, size_t ws_bytes,
-                         void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Checks shared by hsa_forward and hsa_forward_selected.
+hsa_status_t check_forward(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                           const hsa_kv_pool_t* pool, int32_t n_cand, int32_t n_cur_pages,
+                           const int32_t* k_h, int32_t k_max, const float* kv_state,
+                           const float* k_state, const void* o) {
   hsa_status_t st = check_cfg(cfg);
   if (st != HSA_OK) return st;
   if ((st = check_pool(pool)) != HSA_OK) return st;
-  if (!q || !k_h || !kv_state || !k_state || !page_kmean || !o) return HSA_ERR_INVALID_ARG;
+  if (!q || !k_h || !kv_state || !k_state || !o) return HSA_ERR_INVALID_ARG;
   if (n_q < 1 || n_cand < 0 || n_cur_pages < 0 || k_max < 1) return HSA_ERR_INVALID_ARG;
   if ((long)n_cand + n_cur_pages > pool->max_pages) return HSA_ERR_OUT_OF_RANGE;
   if (n_cand > HSA_MAX_CAND) return HSA_ERR_UNSUPPORTED;
@@ -359,15 +362,15 @@ hsa_status_t hsa_forward(const hsa_config_t* cfg, const void* q, int32_t n_q,
   if ((st = check_budgets(cfg, k_h, k_max)) != HSA_OK) return st;
   for (int h = 0; h < cfg->num_heads; ++h)
     if (n_cur_pages == 0 && std::min(k_h[h], n_cand) == 0) return HSA_ERR_INVALID_ARG;
-  const size_t need = hsa_forward_workspace_size(cfg, n_q, k_max, n_cur_pages);
-  if ((st = check_ws(ws, ws_bytes, need)) != HSA_OK) return st;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if ((st = validate_pages(cfg, pool, 0, n_cand + n_cur_pages, s)) != HSA_OK) return st;
-  uint8_t* base = static_cast<uint8_t*>(ws);
-  int32_t* sel = sel_out ? sel_out : reinterpret_cast<int32_t*>(base + select_ws_bytes(cfg, n_q));
-  void* partials = base + select_ws_bytes(cfg, n_q) + sel_ws_bytes(cfg, k_max);
-  st = run_select(cfg, q, n_q, page_kmean, pool->max_pages, n_cand, k_h, k_max, sel, nullptr, ws, s);
-  if (st != HSA_OK) return st;
+  return HSA_OK;
+}
+
+// Sparse branch + linear branch + gated fusion for a selection in `sel`.
+hsa_status_t run_attend(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                        const hsa_kv_pool_t* pool, const int32_t* sel, int32_t k_max,
+                        const int32_t* k_h, int32_t n_cand, int32_t n_cur_pages,
+                        const float* kv_state, const float* k_state, const float* g_lin,
+                        const float* g_sp, void* o, void* partials, hipStream_t s) {
   AttnParams p{};
   p.q = q;
   p.k = pool->k;
@@ -396,6 +399,54 @@ hsa_status_t hsa_forward(const hsa_config_t* cfg, const void* q, int32_t n_q,
                  kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16);
   if (cfg->dtype == HSA_DTYPE_BF16) set_partials(p, cfg, n_q, partials);
   return from_hip(launch_attention(cfg->dtype, cfg->head_dim, cfg->batch, p, s));
+}
+
+}  // namespace
+
+extern "C" {
+
+hsa_status_t hsa_forward(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                         const hsa_kv_pool_t* pool, int32_t n_cand, int32_t n_cur_pages,
+                         const int32_t* k_h, int32_t k_max, const float* kv_state,
+                         const float* k_state, const double* page_kmean, const float* g_lin,
+                         const float* g_sp, void* o, int32_t* sel_out, void* ws, size_t ws_bytes,
+                         void* stream) {
+  hsa_status_t st = check_forward(cfg, q, n_q, pool, n_cand, n_cur_pages, k_h, k_max, kv_state,
+                                  k_state, o);
+  if (st != HSA_OK) return st;
+  if (!page_kmean) return HSA_ERR_INVALID_ARG;
+  const size_t need = hsa_forward_workspace_size(cfg, n_q, k_max, n_cur_pages);
+  if ((st = check_ws(ws, ws_bytes, need)) != HSA_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = validate_pages(cfg, pool, 0, n_cand + n_cur_pages, s)) != HSA_OK) return st;
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  int32_t* sel = sel_out ? sel_out : reinterpret_cast<int32_t*>(base + select_ws_bytes(cfg, n_q));
+  void* partials = base + select_ws_bytes(cfg, n_q) + sel_ws_bytes(cfg, k_max);
+  st = run_select(cfg, q, n_q, page_kmean, pool->max_pages, n_cand, k_h, k_max, sel, nullptr, ws, s);
+  if (st != HSA_OK) return st;
+  return run_attend(cfg, q, n_q, pool, sel, k_max, k_h, n_cand, n_cur_pages, kv_state, k_state,
+                    g_lin, g_sp, o, partials, s);
+}
+
+hsa_status_t hsa_forward_selected(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                                  const hsa_kv_pool_t* pool, const int32_t* sel, int32_t k_max,
+                                  const int32_t* k_h, int32_t n_cand, int32_t n_cur_pages,
+                                  const float* kv_state, const float* k_state,
+                                  const float* g_lin, const float* g_sp, void* o, void* ws,
+                                  size_t ws_bytes, void* stream) {
+  hsa_status_t st = check_forward(cfg, q, n_q, pool, n_cand, n_cur_pages, k_h, k_max, kv_state,
+                                  k_state, o);
+  if (st != HSA_OK) return st;
+  if (!sel) return HSA_ERR_INVALID_ARG;
+  const size_t need = hsa_forward_workspace_size(cfg, n_q, k_max, n_cur_pages);
+  if ((st = check_ws(ws, ws_bytes, need)) != HSA_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = validate_pages(cfg, pool, n_cand, n_cur_pages, s)) != HSA_OK) return st;
+  if ((st = validate_selection(cfg, pool, sel, k_max, s)) != HSA_OK) return st;
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  void* partials = base + select_ws_bytes(cfg, n_q) + sel_ws_bytes(cfg, k_max);
+  return run_attend(cfg, q, n_q, pool, sel, k_max, k_h, n_cand, n_cur_pages, kv_state, k_state,
+                    g_lin, g_sp, o, partials, s);
 }
 
 }  // extern "C"

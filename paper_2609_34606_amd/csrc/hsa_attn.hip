@@ -22,6 +22,7 @@
 #include <float.h>
 
 #include <algorithm>
+#include <mutex>
 #include <queue>
 #include <utility>
 #include <vector>
@@ -54,9 +55,6 @@ struct AttnLayout {
   static constexpr int kInstK = kKTile / 1024 / 4;     // key loads per wave
   static constexpr int kInstV = kVTile / 1024 / 4;     // value loads per wave
 };
-
-// query tiles per XCD run (see the workgroup-to-item mapping)
-constexpr int kXcdRun = 4;
 
 // Swizzles of 16-byte chunks within LDS rows: 16 consecutive rows read at one
 // logical chunk land on distinct bank groups.
@@ -209,23 +207,28 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   const int l32 = lane & 31, half = lane >> 5;
   const int H = p.H, P = p.P;
-  const int nqt = p.nqt;
+  const int nqt = p.sc.nqt;
   const int b = blockIdx.y;
   int qtile, h, split;
   {
-    // Workgroups go to the 8 XCDs round-robin by id. Deal the items to the
-    // XCDs in runs of kXcdRun consecutive items (consecutive query tiles of
-    // one head and split, which read the same pages through one L2); every
-    // XCD gets a mix of heads. The grid is padded to a multiple of
-    // 8 * kXcdRun; padding workgroups exit here (gridDim.x % 8 == 0, so
-    // blockIdx.x % 8 is the XCD).
-    const int w = blockIdx.x, x = w & 7, k = w >> 3;
-    const int item = (k / kXcdRun) * (8 * kXcdRun) + x * kXcdRun + (k % kXcdRun);
-    if (item >= p.n_items) return;
+    // Workgroups go to the 8 XCDs round-robin by id (gridDim.x = 8 *
+    // xcd_items, so blockIdx.x % 8 is the XCD). Each XCD runs its own list
+    // of chunks of consecutive items of one (head, split): query tiles that
+    // read the same pages share them through one L2 instead of every XCD
+    // fetching every head.
+    const int w = blockIdx.x, x = w & 7;
+    int k = w >> 3, c = p.sc.xcd_chunk[x];
+    const int c_end = p.sc.xcd_chunk[x + 1];
+    while (c < c_end && k >= p.sc.chunk_len[c]) {
+      k -= p.sc.chunk_len[c];
+      ++c;
+    }
+    if (c >= c_end) return;
+    const int item = p.sc.chunk_start[c] + k;
     int oh = 0;
-    while (oh + 1 < p.n_order && p.item_off[oh + 1] <= item) ++oh;
-    h = p.head_order[oh];
-    const int local = item - p.item_off[oh];
+    while (oh + 1 < p.sc.n_order && p.sc.item_off[oh + 1] <= item) ++oh;
+    h = p.sc.head_order[oh];
+    const int local = item - p.sc.item_off[oh];
     split = local / nqt;
     qtile = local % nqt;
   }
@@ -247,10 +250,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
   // This item's share of the list: split `split` of n_split[h] near-equal
   // parts of list_len[h] pages (the last split takes whatever the list holds
   // beyond the plan).
-  const int ns = p.n_split[h];
+  const int ns = p.sc.n_split[h];
   int pg0 = 0, pg1 = n_list;
   if (ns > 1) {
-    const int len = p.list_len[h], base = len / ns, rem = len % ns;
+    const int len = p.sc.list_len[h], base = len / ns, rem = len % ns;
     pg0 = min(n_list, split * base + min(split, rem));
     pg1 = split == ns - 1 ? n_list : min(n_list, pg0 + base + (split < rem ? 1 : 0));
   }
@@ -443,7 +446,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
   if (ns > 1) {
     // partial result of this split: normalised output and log-sum-exp, in the
     // accumulator register layout (register-major, lane fastest: coalesced)
-    const size_t cell = (((size_t)b * p.n_part + p.part_base[h] + split) * nqt + qtile) * 4 + wave;
+    const size_t cell = (((size_t)b * p.sc.n_part + p.sc.part_base[h] + split) * nqt + qtile) * 4 + wave;
     float* po = p.part_o + cell * (NM * 16 * 64) + lane;
 #pragma unroll
     for (int m = 0; m < NM; ++m)
@@ -465,10 +468,10 @@ __global__ __launch_bounds__(256, 2) void combine_bf16_kernel(AttnParams p) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, half = lane >> 5;
-  const int b = blockIdx.y, nqt = p.nqt;
+  const int b = blockIdx.y, nqt = p.sc.nqt;
   const int ch = blockIdx.x / nqt, qtile = blockIdx.x % nqt;
-  const int h = p.c_head[ch], ns = p.n_split[h];
-  const size_t cell0 = (((size_t)b * p.n_part + p.part_base[h]) * nqt + qtile) * 4 + wave;
+  const int h = p.sc.c_head[ch], ns = p.sc.n_split[h];
+  const size_t cell0 = (((size_t)b * p.sc.n_part + p.sc.part_base[h]) * nqt + qtile) * 4 + wave;
   const size_t cstride = (size_t)nqt * 4;  // cells between consecutive splits
   float lmax = -INFINITY;
   for (int s = 0; s < ns; ++s) lmax = fmaxf(lmax, p.part_lse[(cell0 + s * cstride) * 64 + lane]);
@@ -616,96 +619,211 @@ size_t attention_partial_bytes(int B, int d, int n_q, int max_part) {
   return ((o + 255) / 256 + (l + 255) / 256) * 256;
 }
 
+namespace {
+
+// One chunk of the schedule: len consecutive items starting at start, all of
+// one (head, split) and so of equal cost (in 64-key tiles).
+struct Chunk {
+  int start, len;
+  double cost;
+};
+
+// Workgroup w of a launch runs on XCD w % 8, and each XCD hands its
+// workgroups, in order, to whichever of its 64 slots (32 CUs x 2) frees
+// first. Simulates that for the chunks given XCD by XCD (list scheduling):
+// chunks are taken largest item first, each goes to the XCD where its items
+// can all start earliest. Returns the simulated makespan; fills xcd_of.
+double deal_chunks(const std::vector<Chunk>& chunks, std::vector<int>& xcd_of) {
+  constexpr int kXcd = 8, kSlotsPerXcd = 64;
+  // slot finish times of each XCD, kept sorted ascending
+  std::vector<double> slot(kXcd * kSlotsPerXcd, 0.0);
+  xcd_of.assign(chunks.size(), 0);
+  for (size_t ci = 0; ci < chunks.size(); ++ci) {
+    const Chunk& c = chunks[ci];
+    const int L = std::min(c.len, kSlotsPerXcd);
+    int best = 0;
+    for (int x = 1; x < kXcd; ++x)
+      if (slot[x * kSlotsPerXcd + L - 1] < slot[best * kSlotsPerXcd + L - 1]) best = x;
+    xcd_of[ci] = best;
+    double* s = slot.data() + best * kSlotsPerXcd;
+    const double unit = c.cost / c.len;
+    for (int k = 0; k < c.len; ++k) {  // list-schedule the chunk's items
+      const double v = s[0] + unit;
+      double* pos = std::upper_bound(s + 1, s + kSlotsPerXcd, v);
+      std::copy(s + 1, pos, s);
+      pos[-1] = v;
+    }
+  }
+  double makespan = 0.0;
+  for (int x = 0; x < kXcd; ++x) makespan = std::max(makespan, slot[x * kSlotsPerXcd + kSlotsPerXcd - 1]);
+  return makespan;
+}
+
+// Inputs of a schedule, the key of the schedule cache.
+struct PlanKey {
+  int H, d, n_q, P, max_part, split;
+  int list_len[HSA_MAX_HEADS];
+  bool operator==(const PlanKey& o) const {
+    return H == o.H && d == o.d && n_q == o.n_q && P == o.P && max_part == o.max_part &&
+           split == o.split && std::equal(list_len, list_len + H, o.list_len);
+  }
+};
+
+void plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_len, int max_part,
+                   bool split);
+
+}  // namespace
+
 void plan_attention(AttnParams& p, int H, int d, int n_q, int P, const int* list_len, int max_part,
                     bool split) {
+  constexpr int kCache = 8;
+  static std::mutex mu;
+  static PlanKey keys[kCache];
+  static AttnSchedule scheds[kCache];
+  static int n_cached = 0, next = 0;
+  PlanKey key{H, d, n_q, P, max_part, split ? 1 : 0, {}};
+  std::copy(list_len, list_len + H, key.list_len);
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    for (int i = 0; i < n_cached; ++i)
+      if (keys[i] == key) {
+        p.sc = scheds[i];
+        return;
+      }
+  }
+  plan_schedule(p, H, d, n_q, P, list_len, max_part, split);
+  std::lock_guard<std::mutex> lock(mu);
+  keys[next] = key;
+  scheds[next] = p.sc;
+  next = (next + 1) % kCache;
+  n_cached = std::min(n_cached + 1, kCache);
+}
+
+namespace {
+
+void plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_len, int max_part,
+                   bool split) {
   const int nqt = (n_q + kBM - 1) / kBM;
   const int tpp = (P + kBN - 1) / kBN;
-  // Cost model (units: one 64-key tile of one item on one of 512 slots,
-  // two workgroups on each of 256 CUs): an item costs its tiles plus a fixed
-  // prologue/epilogue; splitting a head adds a combine pass whose time is
-  // dominated by writing and reading the partial outputs.
-  constexpr double kSlots = 512.0, kOverheadTiles = 3.0, kTileUs = 2.4;
+  // Cost model (unit: one 64-key tile of one item with two workgroups on a
+  // CU): an item costs its tiles plus a fixed prologue/epilogue; splitting a
+  // head adds a combine pass whose time is dominated by writing and reading
+  // the partial outputs.
+  constexpr double kOverheadTiles = 3.0, kTileUs = 2.25;
   constexpr double kCombineUsFixed = 8.0, kPartialBytesPerUs = 4.0e6;
-  auto evaluate = [&](int T, int* ns) -> double {
-    int n_part = 0;
-    for (int h = 0; h < H; ++h) {
-      ns[h] = T > 0 ? std::max(1, (list_len[h] + T - 1) / T) : 1;
-      if (ns[h] > 1) n_part += ns[h];
-    }
-    if (n_part > max_part) return 1e30;
-    std::vector<std::pair<double, int>> groups;  // (cost, count)
-    for (int h = 0; h < H; ++h) {
-      const int len = list_len[h], base = len / ns[h], rem = len % ns[h];
-      for (int s = 0; s < ns[h]; ++s)
-        groups.push_back({(base + (s < rem ? 1 : 0)) * (double)tpp + kOverheadTiles, nqt});
-    }
-    std::sort(groups.begin(), groups.end(), [](auto& a, auto& b) { return a.first > b.first; });
-    std::priority_queue<double, std::vector<double>, std::greater<double>> slots;
-    for (int i = 0; i < (int)kSlots; ++i) slots.push(0.0);
-    for (auto& g : groups)
-      for (int i = 0; i < g.second; ++i) {
-        const double t = slots.top();
-        slots.pop();
-        slots.push(t + g.first);
+  // Items of one batch entry are numbered head by head (heads in decreasing
+  // split size), split-major, query tile fastest. The chunks of a (head,
+  // split) group read the same pages, so each XCD should run few groups;
+  // cutting groups into more chunks balances the XCDs better.
+  auto build = [&](const int* ns, int per_group, std::vector<int>& order, std::vector<Chunk>& chunks) {
+    order.resize(H);
+    for (int h = 0; h < H; ++h) order[h] = h;
+    auto split_size = [&](int h) { return (list_len[h] + ns[h] - 1) / ns[h]; };
+    std::stable_sort(order.begin(), order.end(),
+                     [&](int a, int b) { return split_size(a) > split_size(b); });
+    int items = 0;
+    for (int h = 0; h < H; ++h) items += ns[h] * nqt;
+    const int min_len = (items + HSA_MAX_CHUNKS - 1) / HSA_MAX_CHUNKS;
+    const int len_c = std::max(min_len, (nqt + per_group - 1) / per_group);
+    chunks.clear();
+    for (int i = 0, it = 0; i < H; ++i) {
+      const int h = order[i], base = list_len[h] / ns[h], rem = list_len[h] % ns[h];
+      for (int sp = 0; sp < ns[h]; ++sp, it += nqt) {
+        const double c = (base + (sp < rem ? 1 : 0)) * (double)tpp + kOverheadTiles;
+        for (int a = 0; a < nqt; a += len_c) {
+          const int len = std::min(len_c, nqt - a);
+          chunks.push_back({it + a, len, c * len});
+        }
       }
-    double makespan = 0.0;
-    while (!slots.empty()) {
-      makespan = std::max(makespan, slots.top());
-      slots.pop();
     }
-    double us = makespan * kTileUs;
+    // largest item cost first (stable: groups stay in item order)
+    std::stable_sort(chunks.begin(), chunks.end(),
+                     [](const Chunk& a, const Chunk& b) { return a.cost / a.len > b.cost / b.len; });
+  };
+  std::vector<int> order, xcd_of;
+  std::vector<Chunk> chunks;
+  auto evaluate = [&](const int* ns, int per_group) -> double {
+    int n_part = 0;
+    for (int h = 0; h < H; ++h)
+      if (ns[h] > 1) n_part += ns[h];
+    if (n_part > max_part) return 1e30;
+    build(ns, per_group, order, chunks);
+    double us = deal_chunks(chunks, xcd_of) * kTileUs;
     if (n_part > 0) us += kCombineUsFixed + 2.0 * n_part * nqt * (double)kBM * d * 4 / kPartialBytesPerUs;
     return us;
   };
+  // Search the split (pages per split T) and the cut; a split or a finer cut
+  // has to win clearly, since both cost locality.
   int best_ns[HSA_MAX_HEADS], ns[HSA_MAX_HEADS];
-  double best = evaluate(0, best_ns);
-  if (split) {
-    for (int T : {16, 12, 8, 6, 5, 4, 3, 2}) {
-      const double c = evaluate(T, ns);
-      if (c < best * 0.97) {  // split only for a clear gain
+  for (int h = 0; h < H; ++h) best_ns[h] = 1;
+  int best_g = 2;
+  double best = evaluate(best_ns, 2);
+  for (int T : {0, 16, 12, 8, 6, 5, 4, 3, 2}) {
+    if (T > 0 && !split) break;
+    for (int h = 0; h < H; ++h) ns[h] = T > 0 ? std::max(1, (list_len[h] + T - 1) / T) : 1;
+    for (int g : {2, 4}) {
+      if (T == 0 && g == 2) continue;
+      const double c = evaluate(ns, g) * (T > 0 ? 1.03 : 1.0) * (g > 2 ? 1.02 : 1.0);
+      if (c < best) {
         best = c;
+        best_g = g;
         std::copy(ns, ns + H, best_ns);
       }
     }
   }
-  p.nqt = nqt;
-  // heads in order of decreasing split size (largest items dispatched first)
-  std::vector<int> order(H);
-  for (int h = 0; h < H; ++h) order[h] = h;
-  auto split_size = [&](int h) { return (list_len[h] + best_ns[h] - 1) / best_ns[h]; };
-  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return split_size(a) > split_size(b); });
-  p.n_order = H;
+  evaluate(best_ns, best_g);  // rebuild order, chunks and xcd_of of the choice
+  p.sc.nqt = nqt;
+  p.sc.n_order = H;
   int items = 0, n_part = 0, n_chead = 0;
   for (int i = 0; i < H; ++i) {
     const int h = order[i];
-    p.head_order[i] = h;
-    p.item_off[i] = items;
+    p.sc.head_order[i] = h;
+    p.sc.item_off[i] = items;
     items += best_ns[h] * nqt;
   }
-  p.item_off[H] = items;
-  p.n_items = items;
+  p.sc.item_off[H] = items;
+  p.sc.n_items = items;
   for (int h = 0; h < H; ++h) {
-    p.n_split[h] = best_ns[h];
-    p.list_len[h] = list_len[h];
-    p.part_base[h] = 0;
+    p.sc.n_split[h] = best_ns[h];
+    p.sc.list_len[h] = list_len[h];
+    p.sc.part_base[h] = 0;
     if (best_ns[h] > 1) {
-      p.part_base[h] = n_part;
+      p.sc.part_base[h] = n_part;
       n_part += best_ns[h];
-      p.c_head[n_chead++] = h;
+      p.sc.c_head[n_chead++] = h;
     }
   }
-  p.n_part = n_part;
-  p.n_chead = n_chead;
+  p.sc.n_part = n_part;
+  p.sc.n_chead = n_chead;
+  // each XCD runs its chunks in the order they were dealt to it
+  int n = 0, widest = 0;
+  for (int x = 0; x < 8; ++x) {
+    p.sc.xcd_chunk[x] = n;
+    int cnt = 0;
+    for (size_t ci = 0; ci < chunks.size(); ++ci)
+      if (xcd_of[ci] == x) {
+        p.sc.chunk_start[n] = chunks[ci].start;
+        p.sc.chunk_len[n] = chunks[ci].len;
+        cnt += chunks[ci].len;
+        ++n;
+      }
+    widest = std::max(widest, cnt);
+  }
+  p.sc.xcd_chunk[8] = n;
+  p.sc.n_chunks = n;
+  p.sc.xcd_items = widest;
 }
+
+}  // namespace
 
 hipError_t launch_attention(int dtype, int d, int B, const AttnParams& p, hipStream_t s) {
   if (dtype == HSA_DTYPE_BF16) {
-    const dim3 grid((p.n_items + 8 * kXcdRun - 1) / (8 * kXcdRun) * (8 * kXcdRun), B);
+    const dim3 grid(8 * std::max(1, p.sc.xcd_items), B);
     if (d == 128) attn_bf16_kernel<128><<<grid, 256, 0, s>>>(p);
     else attn_bf16_kernel<64><<<grid, 256, 0, s>>>(p);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || p.n_chead == 0) return e;
-    const dim3 cgrid(p.n_chead * p.nqt, B);
+    if (e != hipSuccess || p.sc.n_chead == 0) return e;
+    const dim3 cgrid(p.sc.n_chead * p.sc.nqt, B);
     if (d == 128) combine_bf16_kernel<128><<<cgrid, 256, 0, s>>>(p);
     else combine_bf16_kernel<64><<<cgrid, 256, 0, s>>>(p);
   } else {

@@ -10,6 +10,8 @@
 
 namespace hsa {
 
+constexpr int HSA_MAX_CHUNKS = 256;
+
 // ------------------------------------------------------------ state update
 struct StateParams {
   const void* k;            // [num_slots, H, P, d]
@@ -65,6 +67,31 @@ enum AttnMode : int32_t {
   ATTN_SPARSE = 1,  // write o_sp (fp32) and lse
 };
 
+// Work schedule of the bf16 attention kernels, chosen by plan_attention.
+struct AttnSchedule {
+  // Attention items of one batch entry are numbered head by head in head_order, each head
+  // contributing n_split[h] * nqt items (split-major, query tile fastest).
+  int32_t nqt;                           // query tiles of kBM queries
+  int32_t n_items;                       // attention items per batch entry
+  int32_t n_order;                       // heads listed in head_order
+  int32_t head_order[HSA_MAX_HEADS];
+  int32_t item_off[HSA_MAX_HEADS + 1];   // first item of head_order[i]
+  int32_t n_split[HSA_MAX_HEADS];        // splits of head h (by head index)
+  int32_t list_len[HSA_MAX_HEADS];       // pages the splits of head h cover
+  int32_t part_base[HSA_MAX_HEADS];      // first partial slot of head h (n_split > 1)
+  int32_t n_part;                        // partial slots per batch entry
+  // Items are cut into chunks of consecutive items of one (head, split);
+  // XCD x runs chunks [xcd_chunk[x], xcd_chunk[x+1]) in that order.
+  int32_t n_chunks;
+  int32_t chunk_start[HSA_MAX_CHUNKS];
+  int32_t chunk_len[HSA_MAX_CHUNKS];
+  int32_t xcd_chunk[9];
+  int32_t xcd_items;                     // most items on one XCD
+  // combine items: n_chead heads with n_split > 1, nqt items each
+  int32_t n_chead;
+  int32_t c_head[HSA_MAX_HEADS];
+};
+
 struct AttnParams {
   const void* q;            // [B, n_q, H, d]
   const void* k;            // pool keys
@@ -85,28 +112,16 @@ struct AttnParams {
   // sparse mode
   float* o_sp;              // [B, n_q, H, d]
   float* lse;               // [B, H, n_q] nullable
-  // Work schedule of the bf16 kernels (see plan_attention). Attention items
-  // of one batch entry are numbered head by head in head_order, each head
-  // contributing n_split[h] * nqt items (split-major, query tile fastest).
-  int32_t nqt;                           // query tiles of kBM queries
-  int32_t n_items;                       // attention items per batch entry
-  int32_t n_order;                       // heads listed in head_order
-  int32_t head_order[HSA_MAX_HEADS];
-  int32_t item_off[HSA_MAX_HEADS + 1];   // first item of head_order[i]
-  int32_t n_split[HSA_MAX_HEADS];        // splits of head h (by head index)
-  int32_t list_len[HSA_MAX_HEADS];       // pages the splits of head h cover
-  int32_t part_base[HSA_MAX_HEADS];      // first partial slot of head h (n_split > 1)
-  int32_t n_part;                        // partial slots per batch entry
   float* part_o;                         // [B, n_part, nqt, 4 waves, 16*d/32 regs, 64 lanes]
   float* part_lse;                       // [B, n_part, nqt, 4 waves, 64 lanes]
-  // combine items: n_chead heads with n_split > 1, nqt items each
-  int32_t n_chead;
-  int32_t c_head[HSA_MAX_HEADS];
+  AttnSchedule sc;                       // work schedule of the bf16 kernels
 };
 
 // Chooses the split of each head's page list and the item order for
 // list_len[h] pages per head (H heads, head dim d, n_q queries, page size P);
 // at most max_part partial slots. split = false keeps every head whole.
+// Fills p.sc; the last few schedules are cached (thread-safe), so a call
+// with the inputs of a recent one costs a table lookup.
 void plan_attention(AttnParams& p, int H, int d, int n_q, int P, const int* list_len,
                     int max_part, bool split);
 // Workspace bytes for max_part partial slots.

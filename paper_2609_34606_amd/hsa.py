@@ -76,6 +76,9 @@ def lib():
     L.hsa_forward.restype = ctypes.c_int
     L.hsa_forward.argtypes = [P(HsaConfig), c_vp, c_i32, P(HsaKvPool), c_i32, c_i32, c_vp,
                               c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]
+    L.hsa_forward_selected.restype = ctypes.c_int
+    L.hsa_forward_selected.argtypes = [P(HsaConfig), c_vp, c_i32, P(HsaKvPool), c_vp, c_i32, c_vp,
+                                       c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]
     _lib = L
     return L
 
@@ -200,4 +203,18 @@ def hsa_forward(cfg, q, n_q, pool, n_cand, n_cur_pages, k_h, k_max, kv_state, k_
                            _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream))
     if check:
         _check("hsa_forward", st)
+    return st
+
+
+def hsa_forward_selected(cfg, q, n_q, pool, sel, k_max, k_h, n_cand, n_cur_pages, kv_state,
+                         k_state, g_lin, g_sp, o, ws=None, stream=None, check=True) -> int:
+    if ws is None:
+        ws = _workspace(hsa_forward_workspace_size(cfg, n_q, k_max, n_cur_pages), q.device)
+    _keep, kp = _budgets(k_h)
+    st = lib().hsa_forward_selected(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool), _ptr(sel),
+                                    k_max, kp, n_cand, n_cur_pages, _ptr(kv_state), _ptr(k_state),
+                                    _ptr(g_lin), _ptr(g_sp), _ptr(o), _ptr(ws),
+                                    0 if ws is None else ws.numel(), _stream(stream))
+    if check:
+        _check("hsa_forward_selected", st)
     return st

@@ -69,3 +69,15 @@ class HsaLayer:
                        self.k_state, self.page_kmean, g_lin, g_sp, out, sel_out=sel_out, ws=ws,
                        stream=stream)
         return out
+
+    def forward_selected(self, q, sel, n_cand: int, n_cur: int, k_h: Sequence[int],
+                         k_max: Optional[int] = None, g_lin=None, g_sp=None, out=None, stream=None):
+        """The forward pass for a selection already in `sel` ([B,H,k_max] int32)."""
+        B, n_q = q.shape[0], q.shape[1]
+        k_max = int(sel.shape[-1]) if k_max is None else k_max
+        if out is None:
+            out = self.torch.empty_like(q)
+        ws = self.workspace("fwd", _h.hsa_forward_workspace_size(self.cfg, n_q, k_max, n_cur))
+        _h.hsa_forward_selected(self.cfg, q, n_q, self.pool, sel, k_max, k_h, n_cand, n_cur,
+                                self.kv_state, self.k_state, g_lin, g_sp, out, ws=ws, stream=stream)
+        return out

@@ -139,3 +139,74 @@ def test_determinism():
     for k in a:
         np.testing.assert_array_equal(a[k], b[k], err_msg=k)
     torch.cuda.synchronize()
+
+
+def test_forward_selected_matches_forward():
+    import torch
+    from paper_2609_34606_amd import HsaLayer
+    wl = SMALL.replace(seed=31)
+    case = make_case(wl)
+    dev = upload(case)
+    say(f"[case] forward_selected {wl}")
+    B, n_q, H, d = dev["q"].shape
+    layer = HsaLayer(B, H, d, wl.page_size, dev["q"].dtype, dev["q"].device, k_pool=dev["k_pool"],
+                     v_pool=dev["v_pool"], page_table=dev["page_table"])
+    layer.fold(0, wl.n_pages)
+    k_h = list(case.k_h)
+    sel = torch.empty((B, H, max(k_h)), dtype=torch.int32, device=dev["q"].device)
+    a = layer.forward(dev["q"], wl.n_cand, wl.n_cur, k_h, g_lin=dev["g_lin"], g_sp=dev["g_sp"],
+                      sel_out=sel)
+    b = layer.forward_selected(dev["q"], sel, wl.n_cand, wl.n_cur, k_h, g_lin=dev["g_lin"],
+                               g_sp=dev["g_sp"])
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def test_streaming_incremental_state_and_outputs():
+    # Chunks of 3 pages appended one by one; at chunk t the history is the
+    # 3(t-1) earlier pages and the state covers every page written so far.
+    import torch
+    from oracle import hsa_oracle as O
+    from paper_2609_34606_amd import HsaLayer
+    T = 4
+    wl = SMALL.replace(heads=2, n_q=150, page_size=200, n_cand=3 * (T - 1), n_cur=3, k_h=(2, 5),
+                       seed=41)
+    case = make_case(wl)            # pages 0..11 of the whole stream
+    dev = upload(case)
+    B, _, H, d = dev["q"].shape
+    layer = HsaLayer(B, H, d, wl.page_size, dev["q"].dtype, dev["q"].device, k_pool=dev["k_pool"],
+                     v_pool=dev["v_pool"], page_table=dev["page_table"])
+    for t in range(1, T + 1):
+        say(f"[case] streaming chunk {t}")
+        qc = make_case(wl, chunk=t).q   # a fresh query chunk
+        q = torch.from_numpy(qc).to("cuda:0").to(torch.bfloat16)
+        n_cand = 3 * (t - 1)
+        layer.fold(n_cand, 3)
+        sel = torch.full((B, H, 5), -7, dtype=torch.int32, device="cuda:0")
+        o = layer.forward(q, n_cand, 3, list(case.k_h), k_max=5, sel_out=sel)
+        torch.cuda.synchronize()
+        ref = O.hsa_forward(qc, case.k_pool, case.v_pool, case.page_table, n_cand, 3,
+                            list(case.k_h), k_max=5, state_pages=range(3 * t))
+        np.testing.assert_array_equal(sel.cpu().numpy(), ref["sel"])
+        from hsa_testlib import BF16_TOL, assert_close
+        assert_close(f"O chunk {t}", o.float().cpu().numpy(), ref["O"], **BF16_TOL)
+    # the incremental state equals a cold fold of the same pages
+    cold = HsaLayer(B, H, d, wl.page_size, dev["q"].dtype, dev["q"].device, k_pool=dev["k_pool"],
+                    v_pool=dev["v_pool"], page_table=dev["page_table"])
+    cold.fold(0, 3 * T)
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(layer.kv_state.cpu().numpy(), cold.kv_state.cpu().numpy(),
+                               rtol=1e-5, atol=1e-4)
+    np.testing.assert_allclose(layer.k_state.cpu().numpy(), cold.k_state.cpu().numpy(), rtol=1e-6)
+    np.testing.assert_array_equal(layer.page_kmean.cpu().numpy(), cold.page_kmean.cpu().numpy())
+
+
+def test_c5_last_chunk_full_size():
+    # streaming workload at its longest history: chunk 60, 177 history pages
+    from synth_inputs.configs import streaming_chunk
+    wl = streaming_chunk(WORKLOADS["c5"], 60)
+    WORKLOADS["_c5_t60"] = wl
+    try:
+        _full_size("_c5_t60", rows_k=96)
+    finally:
+        del WORKLOADS["_c5_t60"]
