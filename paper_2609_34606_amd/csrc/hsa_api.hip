@@ -16,7 +16,6 @@ namespace {
 
 constexpr size_t kAlign = 256;
 constexpr int kStateTargetGroups = 512;  // ~2 workgroups per CU on 256 CUs
-constexpr int kStateMinPartKeys = 256;
 constexpr int kQsumRows = 32;
 constexpr int kPartPerHead = 4;  // partial slots per head for split key lists
 
@@ -94,21 +93,38 @@ struct StatePlan {
 };
 
 StatePlan plan_state(const hsa_config_t* c, int n_pages) {
-  StatePlan pl{1, c->page_size, 1, n_pages};
-  const long units = (long)c->batch * c->num_heads * n_pages;
-  if (units >= kStateTargetGroups) {
-    pl.upw = (int)(units / kStateTargetGroups);
-    pl.n_groups = (n_pages + pl.upw - 1) / pl.upw;
-  } else if (units > 0) {
-    int parts = (int)((kStateTargetGroups + units - 1) / units);
-    parts = std::min(parts, std::max(1, c->page_size / kStateMinPartKeys));
+  // A unit is one of `parts` equal key ranges of a page; each workgroup
+  // folds upw consecutive units. The pass runs two workgroups per CU, i.e.
+  // rounds of kStateTargetGroups; the cost model (in 64-key tiles per slot)
+  // counts whole rounds, a fixed cost per workgroup (pipeline fill and the
+  // partial-state write) and the reduction of the partial states.
+  StatePlan best{1, c->page_size, 1, std::max(n_pages, 1)};
+  if (n_pages <= 0) return best;
+  const long bh = (long)c->batch * c->num_heads;
+  constexpr double kGroupTiles = 2.5, kReduceTilesPerGroup = 0.004;
+  double best_cost = 1e300;
+  for (int parts = 1; parts <= 16; ++parts) {
     int len = (c->page_size + parts - 1) / parts;
     len = (len + 7) / 8 * 8;
-    pl.part_len = len;
-    pl.parts = (c->page_size + len - 1) / len;
-    pl.n_groups = n_pages * pl.parts;
+    const int parts_eff = (c->page_size + len - 1) / len;
+    if (parts > 1 && parts_eff != parts) continue;  // same split as a smaller count
+    const long units = (long)n_pages * parts_eff;
+    const int tiles = (len + 63) / 64;
+    for (int r = 1; r <= 8; ++r) {
+      const long gpb = (long)r * kStateTargetGroups / bh;  // groups per (b, h)
+      if (gpb < 1) continue;
+      const long upw = (units + gpb - 1) / gpb;
+      const long groups = (units + upw - 1) / upw;
+      const long g_all = bh * groups;
+      const long rounds = (g_all + kStateTargetGroups - 1) / kStateTargetGroups;
+      const double cost = rounds * (upw * (double)tiles + kGroupTiles) + kReduceTilesPerGroup * g_all;
+      if (cost < best_cost * 0.999) {
+        best_cost = cost;
+        best = StatePlan{parts_eff, len, (int)upw, (int)groups};
+      }
+    }
   }
-  return pl;
+  return best;
 }
 
 struct StateWs {

@@ -237,15 +237,15 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
   const int32_t* selrow = p.sel + ((size_t)b * H + h) * p.k_max;
   int n_sel = 0;
   while (n_sel < p.k_max) {
-    const int e = selrow[n_sel];
+    const int e = ld_const(selrow + n_sel);
     if (e < 0 || e >= p.max_pages) break;
     ++n_sel;
   }
   const int n_list = n_sel + p.n_cur;
   const int32_t* ptrow = p.page_table + (size_t)b * p.max_pages;
   auto head_of = [&](int li) -> size_t {
-    const int lp = li < n_sel ? selrow[li] : p.cur_first + (li - n_sel);
-    return (size_t)clampi(ptrow[lp], 0, p.num_slots - 1) * H + h;
+    const int lp = li < n_sel ? ld_const(selrow + li) : p.cur_first + (li - n_sel);
+    return (size_t)clampi(ld_const(ptrow + lp), 0, p.num_slots - 1) * H + h;
   };
   // This item's share of the list: split `split` of n_split[h] near-equal
   // parts of list_len[h] pages (the last split takes whatever the list holds
@@ -354,7 +354,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
     // are outstanding
     if (tile + 1 < ntiles) wait_vmcnt<L::kInstK>();
     else wait_vmcnt<0>();
-    __syncthreads();
+    lds_barrier();
     if (tile + 1 < ntiles) issue_v((tile + 1) & 1);
     if (tile + 2 < ntiles) issue_k(kbuf == 0 ? 2 : kbuf - 1);   // ring slot (tile+2) % 3
     const int nv = min(kBN, P - t * kBN);

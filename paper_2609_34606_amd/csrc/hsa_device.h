@@ -65,6 +65,27 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
 }
 
+// Workgroup barrier for LDS tiles filled by prefetch. __syncthreads() (and
+// any LDS release fence) makes every wave wait for all of its outstanding
+// global loads, because global_load_lds writes LDS under the vector-memory
+// counter; that would drain a prefetch ring at each tile. This barrier waits
+// only for the wave's own LDS reads and writes; the caller makes the
+// global_load_lds data of the tile it is about to read complete with
+// wait_vmcnt before it. The memory clobber keeps the compiler from moving
+// memory accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Load through the constant address space: for data that no thread writes
+// while the kernel runs, read at a wave-uniform address. The compiler then
+// uses a scalar load (counted by lgkmcnt), which leaves the vmcnt
+// accounting of in-flight tile loads untouched.
+template <typename T>
+__device__ __forceinline__ T ld_const(const T* p) {
+  return *(const __attribute__((address_space(4))) T*)(p);
+}
+
 __device__ __forceinline__ int clampi(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
 
 }  // namespace hsa

@@ -13,6 +13,8 @@
 // keys contiguous) and mapped through phi on the way. The contraction is
 // bf16 MFMA with fp32 accumulation; partial states per workgroup are reduced
 // in a fixed order by a second kernel (deterministic, no atomics).
+#include <type_traits>
+
 #include "hsa_device.h"
 #include "hsa_kernels.h"
 
@@ -26,13 +28,24 @@ constexpr int kRowBytes = kTileKeys * 2;  // one LDS row: 64 bf16 keys
 // read at the same logical chunk hit distinct bank groups.
 __device__ __forceinline__ int swz8(int row) { return ((row >> 1) ^ (row >> 4)) & 7; }
 
+constexpr int kUnitsPerBatch = 8;       // page sums staged in LDS per batch
+
 template <int D>
 struct StateSmem {
-  uint8_t vt[2][D * kRowBytes];   // V^T tile: [d_v][64 keys] bf16
-  uint8_t fk[2][D * kRowBytes];   // phi(K)^T tile: [d_k][64 keys] bf16
+  uint8_t vt[3][D * kRowBytes];   // V^T tiles: [d_v][64 keys] bf16, 3-stage ring
+  uint8_t fk[D * kRowBytes];      // phi(K)^T tile: [d_k][64 keys] bf16
   double red[8 * 128];            // cross-thread reductions (8 KB)
+  double ksum[kUnitsPerBatch * D];  // key sums of the batch's units
 };
 
+// One workgroup folds units [u_begin, u_end) of one (batch, head); a unit is
+// one part of one page. Units go in batches of up to kUnitsPerBatch; the
+// 64-key tiles of a batch run as one flat sequence across unit boundaries
+// with two tiles in flight: while tile t is converted and contracted, the
+// loads of tiles t+1 and t+2 are outstanding (V into a 3-slot LDS ring, K
+// into two alternating register sets). No global store happens inside that
+// loop, so the only vector-memory waits there are the in-order ones below;
+// the batch's page sums are kept in LDS and written once it is done.
 template <int D>
 __global__ __launch_bounds__(256, 2) void state_bf16_kernel(StateParams p) {
   constexpr int DQ = D / 4;                // 4-wide d groups per key row
@@ -41,6 +54,7 @@ __global__ __launch_bounds__(256, 2) void state_bf16_kernel(StateParams p) {
   constexpr int NV = D / 32;               // V^T 1-KB load instructions per wave
   constexpr int NT = D / 32;               // 32-wide output blocks per dim
   constexpr int TPW = NT * NT / 4;         // output tiles per wave
+  constexpr int kLoads = NV + KPT;         // load instructions per tile per thread
   static_assert(KPT == 8 || KPT == 4, "layout");
   __shared__ __attribute__((aligned(16))) StateSmem<D> sm;
 
@@ -49,117 +63,198 @@ __global__ __launch_bounds__(256, 2) void state_bf16_kernel(StateParams p) {
   const int b = bh / p.H, h = bh % p.H;
   const int n_units = p.n_pages * p.parts;
   const int u_begin = grp * p.upw;
-  const int u_end = min(n_units, u_begin + p.upw);
+  const int u_end = min(n_units, u_begin + p.upw);  // the plan gives every group >= 1 unit
 
   const uint16_t* __restrict__ kb = static_cast<const uint16_t*>(p.k);
   const uint16_t* __restrict__ vb = static_cast<const uint16_t*>(p.v);
-
   const int dq = tid % DQ, kg = tid / DQ;  // K-load role: 4 dims x KPT keys
+  const int tiles_full = (p.part_len + kTileKeys - 1) / kTileKeys;
+
+  // key range of unit u
+  auto unit_keys = [&](int u, int& k_beg, int& k_end) {
+    k_beg = (u % p.parts) * p.part_len;
+    k_end = min(p.P, k_beg + p.part_len);
+  };
+  auto unit_tiles = [&](int u) {
+    int k_beg, k_end;
+    unit_keys(u, k_beg, k_end);
+    return k_end - k_beg < p.part_len ? (k_end - k_beg + kTileKeys - 1) / kTileKeys : tiles_full;
+  };
+  auto head_base = [&](int u) {
+    const int page = p.first_page + u / p.parts;
+    const int slot = clampi(ld_const(p.page_table + (size_t)b * p.max_pages + page), 0, p.num_slots - 1);
+    return (size_t)slot * p.H + h;
+  };
+
+  // Per-lane byte offsets of the tile loads, fixed for the whole pass: V^T
+  // rows (8 keys at swizzled chunk c of d-row r, relative to the tile's
+  // first key) and K rows (KPT keys x 4 dims). A tile then costs one scalar
+  // base per tensor.
+  uint32_t v_off[NV], k_off[KPT];
+#pragma unroll
+  for (int n = 0; n < NV; ++n) {
+    const int r = (wave * NV + n) * 8 + (lane >> 3);
+    v_off[n] = (uint32_t)(r * p.P + 8 * ((lane & 7) ^ swz8(r))) * 2u;
+  }
+#pragma unroll
+  for (int e = 0; e < KPT; ++e) k_off[e] = (uint32_t)((kg * KPT + e) * D + dq * 4) * 2u;
 
   f32x16 acc[TPW];
 #pragma unroll
   for (int t = 0; t < TPW; ++t) acc[t] = f32x16{0};
   float zacc[4] = {0.f, 0.f, 0.f, 0.f};
 
-  for (int u = u_begin; u < u_end; ++u) {
-    const int page = p.first_page + u / p.parts;
-    const int part = u % p.parts;
-    const int k_beg = part * p.part_len;
-    const int k_end = min(p.P, k_beg + p.part_len);
-    const int slot = clampi(p.page_table[(size_t)b * p.max_pages + page], 0, p.num_slots - 1);
-    const size_t head_base = ((size_t)slot * p.H + h);
-    const uint16_t* kpage = kb + head_base * p.P * D;   // [P][D]
-    const uint16_t* vpage = vb + head_base * D * p.P;   // [D][P]
-    const int ntiles = (k_end - k_beg + kTileKeys - 1) / kTileKeys;
+  for (int ub = u_begin; ub < u_end; ub += kUnitsPerBatch) {
+    const int ue = min(u_end, ub + kUnitsPerBatch);
+    int total = 0;
+    for (int u = ub; u < ue; ++u) total += unit_tiles(u);
 
-    double kacc[4] = {0.0, 0.0, 0.0, 0.0};
-    u32x2 kr[KPT];
-
-    auto issue = [&](int tile, int buf) {
-      const int k0 = k_beg + tile * kTileKeys;
-      // V^T: NV instructions of 8 rows x 128 bytes per wave
+    // issue cursor: unit iu, tile it within it
+    int iu = ub, it = 0, iu_tiles = unit_tiles(ub);
+    auto issue = [&](u32x2 (&kr)[KPT], int slot_v) {
+      int k_beg, k_end;
+      unit_keys(iu, k_beg, k_end);
+      const size_t hb = head_base(iu);
+      const int k0 = k_beg + it * kTileKeys;
+      const char* vsrc = reinterpret_cast<const char*>(vb + hb * D * p.P + k0);   // [D][P]
+      const char* ksrc = reinterpret_cast<const char*>(kb + (hb * p.P + k0) * D); // [P][D]
+      uint8_t* vdst = &sm.vt[slot_v][wave * NV * 1024];
+      if (k0 + kTileKeys <= k_end) {
 #pragma unroll
-      for (int n = 0; n < NV; ++n) {
-        const int blk = wave * NV + n;
-        const int r = blk * 8 + (lane >> 3);
-        const int c = (lane & 7) ^ swz8(r);
-        int key = k0 + 8 * c;
-        key = key + 8 <= k_end ? key : k_end - 8;
-        g2lds16(vpage + (size_t)r * p.P + key, &sm.vt[buf][blk * 1024]);
+        for (int n = 0; n < NV; ++n) g2lds16(vsrc + v_off[n], vdst + n * 1024);
+#pragma unroll
+        for (int e = 0; e < KPT; ++e) kr[e] = *reinterpret_cast<const u32x2*>(ksrc + k_off[e]);
+      } else {
+        // partial tile: groups and rows past the unit's end re-read its last
+        // valid ones (their values are masked out)
+        const int nv = k_end - k0;
+#pragma unroll
+        for (int n = 0; n < NV; ++n) {
+          const int r = (wave * NV + n) * 8 + (lane >> 3);
+          const int c8 = 8 * ((lane & 7) ^ swz8(r));
+          const int over = max(0, c8 - (nv - 8));
+          g2lds16(vsrc + (v_off[n] - (uint32_t)(over * 2)), vdst + n * 1024);
+        }
+#pragma unroll
+        for (int e = 0; e < KPT; ++e) {
+          const int over = max(0, kg * KPT + e - (nv - 1));
+          kr[e] = *reinterpret_cast<const u32x2*>(ksrc + (k_off[e] - (uint32_t)(over * D * 2)));
+        }
       }
-      // K rows: KPT keys x 4 dims per thread
-#pragma unroll
-      for (int e = 0; e < KPT; ++e) {
-        int key = k0 + kg * KPT + e;
-        key = key < k_end ? key : k_end - 1;
-        kr[e] = *reinterpret_cast<const u32x2*>(kpage + (size_t)key * D + dq * 4);
+      // advance; past the batch's last tile the cursor stays on it
+      if (it + 1 < iu_tiles) {
+        ++it;
+      } else if (iu + 1 < ue) {
+        ++iu;
+        it = 0;
+        iu_tiles = unit_tiles(iu);
       }
     };
 
-    issue(0, 0);
-    for (int tile = 0; tile < ntiles; ++tile) {
-      const int cur = tile & 1;
-      const int k0 = k_beg + tile * kTileKeys;
-      wait_vmcnt<0>();
-      // phi, page sums, normaliser; write phi(K)^T into LDS
+    // Loads are issued unconditionally, two tiles ahead: past the end they
+    // re-read the last tile into a free slot and a register set that is
+    // never consumed. A fixed pattern keeps the in-order wait counts exact.
+    u32x2 krA[KPT], krB[KPT];
+    issue(krA, 0);
+    issue(krB, 1);
+
+    // consume cursor
+    int cu = ub, ct = 0, cu_tiles = unit_tiles(ub);
+    double kacc[4] = {0.0, 0.0, 0.0, 0.0};
+    auto body = [&](int t, u32x2 (&kr)[KPT]) {
+      wait_vmcnt<kLoads>();               // tile t has landed; tile t+1 may be in flight
+      __builtin_amdgcn_sched_barrier(0);  // keep every use of tile t below the wait
+      int k_beg, k_end;
+      unit_keys(cu, k_beg, k_end);
+      const int k0 = k_beg + ct * kTileKeys;
+      // phi, page sums, normaliser (registers only); rows past the unit's
+      // end (partial tiles only) contribute zeros
       float f[KPT][4];
+      auto convert = [&](auto full) {
 #pragma unroll
-      for (int e = 0; e < KPT; ++e) {
-        const bool ok = k0 + kg * KPT + e < k_end;
-        const float x[4] = {bf16_lo(kr[e].x), bf16_hi(kr[e].x), bf16_lo(kr[e].y), bf16_hi(kr[e].y)};
+        for (int e = 0; e < KPT; ++e) {
+          const bool ok = decltype(full)::value || k0 + kg * KPT + e < k_end;
+          const float x[4] = {bf16_lo(kr[e].x), bf16_hi(kr[e].x), bf16_lo(kr[e].y), bf16_hi(kr[e].y)};
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const float y = ok ? phi(x[c]) : 0.f;
-          f[e][c] = y;
-          zacc[c] += y;
-          kacc[c] += ok ? (double)x[c] : 0.0;
+          for (int c = 0; c < 4; ++c) {
+            const float y = ok ? phi(x[c]) : 0.f;
+            f[e][c] = y;
+            zacc[c] += y;
+            kacc[c] += ok ? (double)x[c] : 0.0;
+          }
         }
-      }
+      };
+      if (k0 + kTileKeys <= k_end) convert(std::true_type{});
+      else convert(std::false_type{});
+      // every wave is done with tile t-1 (fk and its V slot) and tile t's V
+      // has landed in LDS
+      lds_barrier();
+      issue(kr, (t + 2) % 3);
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
+      for (int c = 0; c < 4; ++c) {              // phi(K)^T into LDS
         const int row = dq * 4 + c;
         uint32_t w[KPT / 2];
 #pragma unroll
         for (int e = 0; e < KPT / 2; ++e) w[e] = pack_bf16(f[2 * e][c], f[2 * e + 1][c]);
-        const int key0 = kg * KPT;                 // first key of this thread
+        const int key0 = kg * KPT;
         const int chunk = key0 >> 3, within = (key0 & 7) * 2;
-        uint8_t* dst = &sm.fk[cur][row * kRowBytes + ((chunk ^ swz8(row)) << 4) + within];
+        uint8_t* dst = &sm.fk[row * kRowBytes + ((chunk ^ swz8(row)) << 4) + within];
         if constexpr (KPT == 8) {
           *reinterpret_cast<u32x4*>(dst) = u32x4{w[0], w[1], w[2], w[3]};
         } else {
           *reinterpret_cast<u32x2*>(dst) = u32x2{w[0], w[1]};
         }
       }
-      __syncthreads();
-      if (tile + 1 < ntiles) issue(tile + 1, cur ^ 1);
+      lds_barrier();
       // S^T[j][i] += sum_key V^T[j][key] * phiK^T[i][key]
-      const uint8_t* vt = sm.vt[cur];
-      const uint8_t* fk = sm.fk[cur];
+      const uint8_t* vt = sm.vt[t % 3];
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         const int chunk = 2 * ks + (lane >> 5);
 #pragma unroll
-        for (int t = 0; t < TPW; ++t) {
-          const int ti = wave * TPW + t;
+        for (int q = 0; q < TPW; ++q) {
+          const int ti = wave * TPW + q;
           const int mj = ti / NT, ni = ti % NT;
           const int ra = mj * 32 + (lane & 31);
           const int rb = ni * 32 + (lane & 31);
           const u32x4 a = ld_lds16(vt + ra * kRowBytes + ((chunk ^ swz8(ra)) << 4));
-          const u32x4 bb = ld_lds16(fk + rb * kRowBytes + ((chunk ^ swz8(rb)) << 4));
-          acc[t] = mfma32(a, bb, acc[t]);
+          const u32x4 bb = ld_lds16(sm.fk + rb * kRowBytes + ((chunk ^ swz8(rb)) << 4));
+          acc[q] = mfma32(a, bb, acc[q]);
         }
       }
-    }
-    // page-part key sums: reduce over the KG key groups in a fixed order
-    __syncthreads();
+      if (++ct == cu_tiles) {
+        // unit done: its key sums, reduced over the KG key groups in a fixed
+        // order, into the batch's LDS slot (red is next rewritten after at
+        // least two more barriers)
 #pragma unroll
-    for (int c = 0; c < 4; ++c) sm.red[kg * D + dq * 4 + c] = kacc[c];
-    __syncthreads();
-    if (tid < D) {
-      double s = 0.0;
-      for (int g = 0; g < KG; ++g) s += sm.red[g * D + tid];
-      p.ws_k[((size_t)bh * n_units + u) * D + tid] = s;
+        for (int c = 0; c < 4; ++c) sm.red[kg * D + dq * 4 + c] = kacc[c];
+        lds_barrier();
+        if (tid < D) {
+          double s = 0.0;
+          for (int g = 0; g < KG; ++g) s += sm.red[g * D + tid];
+          sm.ksum[(cu - ub) * D + tid] = s;
+        }
+#pragma unroll
+        for (int c = 0; c < 4; ++c) kacc[c] = 0.0;
+        ++cu;
+        ct = 0;
+        if (cu < ue) cu_tiles = unit_tiles(cu);
+      }
+    };
+    // every back edge follows a krB tile, so the wait tracking sees one fixed
+    // load order at the loop head
+    for (int t = 0; t < total; t += 2) {
+      body(t, krA);
+      if (t + 1 >= total) break;
+      body(t + 1, krB);
     }
+    // the two trailing re-reads complete before the ring is reused or the
+    // workgroup's LDS is released; then the batch's page sums go out
+    wait_vmcnt<0>();
+    __syncthreads();
+    double* dst = p.ws_k + ((size_t)bh * n_units + ub) * D;
+    for (int x = tid; x < (ue - ub) * D; x += 256) dst[x] = sm.ksum[x];
+    wait_vmcnt<0>();
     __syncthreads();
   }
 
@@ -177,14 +272,14 @@ __global__ __launch_bounds__(256, 2) void state_bf16_kernel(StateParams p) {
   // state partial: lane holds column i = 32 ni + lane%32, rows j of the tile
   float* out = p.ws_S + g_index * D * D;
 #pragma unroll
-  for (int t = 0; t < TPW; ++t) {
-    const int ti = wave * TPW + t;
+  for (int q = 0; q < TPW; ++q) {
+    const int ti = wave * TPW + q;
     const int mj = ti / NT, ni = ti % NT;
     const int i = ni * 32 + (lane & 31);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int j = mj * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      out[j * D + i] = acc[t][r];
+      out[j * D + i] = acc[q][r];
     }
   }
 }
