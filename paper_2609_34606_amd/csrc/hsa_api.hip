@@ -108,6 +108,8 @@ StatePlan plan_state(const hsa_config_t* c, int n_pages) {
     len = (len + 7) / 8 * 8;
     const int parts_eff = (c->page_size + len - 1) / len;
     if (parts > 1 && parts_eff != parts) continue;  // same split as a smaller count
+    // every unit must end at key >= 64 (the kernel's tile window)
+    if (parts > 1 && c->page_size >= 64 && len < 64) break;
     const long units = (long)n_pages * parts_eff;
     const int tiles = (len + 63) / 64;
     for (int r = 1; r <= 8; ++r) {

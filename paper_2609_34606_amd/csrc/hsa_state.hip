@@ -40,13 +40,14 @@ struct StateSmem {
 
 // One workgroup folds units [u_begin, u_end) of one (batch, head); a unit is
 // one part of one page. Units go in batches of up to kUnitsPerBatch; the
-// 64-key tiles of a batch run as one flat sequence across unit boundaries
-// with two tiles in flight: while tile t is converted and contracted, the
-// loads of tiles t+1 and t+2 are outstanding (V into a 3-slot LDS ring, K
-// into two alternating register sets). No global store happens inside that
-// loop, so the only vector-memory waits there are the in-order ones below;
+// 64-key tiles of a batch run as one flat sequence across unit boundaries.
+// While tile t is converted and contracted, K rows of tile t+1 (registers)
+// and V^T tiles t+1 and t+2 (3-slot LDS ring) are in flight. No global
+// store and no branch around a load happens inside that loop, and the
+// single register set keeps the load order fixed, so the only vector-memory
+// wait there is the in-order one that leaves the newest V tile in flight;
 // the batch's page sums are kept in LDS and written once it is done.
-template <int D>
+template <int D, bool kSmallP>
 __global__ __launch_bounds__(256, 2) void state_bf16_kernel(StateParams p) {
   constexpr int DQ = D / 4;                // 4-wide d groups per key row
   constexpr int KG = 256 / DQ;             // key groups
@@ -54,7 +55,6 @@ __global__ __launch_bounds__(256, 2) void state_bf16_kernel(StateParams p) {
   constexpr int NV = D / 32;               // V^T 1-KB load instructions per wave
   constexpr int NT = D / 32;               // 32-wide output blocks per dim
   constexpr int TPW = NT * NT / 4;         // output tiles per wave
-  constexpr int kLoads = NV + KPT;         // load instructions per tile per thread
   static_assert(KPT == 8 || KPT == 4, "layout");
   __shared__ __attribute__((aligned(16))) StateSmem<D> sm;
 
@@ -109,71 +109,82 @@ __global__ __launch_bounds__(256, 2) void state_bf16_kernel(StateParams p) {
     int total = 0;
     for (int u = ub; u < ue; ++u) total += unit_tiles(u);
 
-    // issue cursor: unit iu, tile it within it
-    int iu = ub, it = 0, iu_tiles = unit_tiles(ub);
-    auto issue = [&](u32x2 (&kr)[KPT], int slot_v) {
+    // Two cursors: K rows run one tile ahead (one register set), V^T tiles
+    // two tiles ahead (3-slot LDS ring). Each step issues K(t+1) first, then
+    // V(t+2), so waiting for K(t+1) at the next step leaves V(t+2) in flight.
+    struct Cursor { int u, t, n; };
+    auto cur_init = [&](Cursor& c) { c.u = ub; c.t = 0; c.n = unit_tiles(ub); };
+    auto cur_next = [&](Cursor& c) {   // stays on the batch's last tile
+      if (c.t + 1 < c.n) ++c.t;
+      else if (c.u + 1 < ue) { ++c.u; c.t = 0; c.n = unit_tiles(c.u); }
+    };
+    // Source window of a tile: 64 keys ending at the unit's end when fewer
+    // remain (every unit ends at key >= 64 when P >= 64), so that its loads
+    // are one scalar base plus the constant per-lane offsets; rows before
+    // the tile's first key are masked when converted. Pages shorter than a
+    // tile (kSmallP) clamp per lane instead.
+    auto tile_src = [&](const Cursor& c, int& ws, int& nv, size_t& hb) {
       int k_beg, k_end;
-      unit_keys(iu, k_beg, k_end);
-      const size_t hb = head_base(iu);
-      const int k0 = k_beg + it * kTileKeys;
-      const char* vsrc = reinterpret_cast<const char*>(vb + hb * D * p.P + k0);   // [D][P]
-      const char* ksrc = reinterpret_cast<const char*>(kb + (hb * p.P + k0) * D); // [P][D]
-      uint8_t* vdst = &sm.vt[slot_v][wave * NV * 1024];
-      if (k0 + kTileKeys <= k_end) {
+      unit_keys(c.u, k_beg, k_end);
+      const int k0 = k_beg + c.t * kTileKeys;
+      nv = min(kTileKeys, k_end - k0);
+      ws = kSmallP ? k0 : min(k0, k_end - kTileKeys);
+      hb = head_base(c.u);
+    };
+    auto issue_k = [&](u32x2 (&kr)[KPT], const Cursor& c) {
+      int ws, nv; size_t hb;
+      tile_src(c, ws, nv, hb);
+      const char* ksrc = reinterpret_cast<const char*>(kb + (hb * p.P + ws) * D); // [P][D]
 #pragma unroll
-        for (int n = 0; n < NV; ++n) g2lds16(vsrc + v_off[n], vdst + n * 1024);
-#pragma unroll
-        for (int e = 0; e < KPT; ++e) kr[e] = *reinterpret_cast<const u32x2*>(ksrc + k_off[e]);
-      } else {
-        // partial tile: groups and rows past the unit's end re-read its last
-        // valid ones (their values are masked out)
-        const int nv = k_end - k0;
-#pragma unroll
-        for (int n = 0; n < NV; ++n) {
-          const int r = (wave * NV + n) * 8 + (lane >> 3);
-          const int c8 = 8 * ((lane & 7) ^ swz8(r));
-          const int over = max(0, c8 - (nv - 8));
-          g2lds16(vsrc + (v_off[n] - (uint32_t)(over * 2)), vdst + n * 1024);
-        }
-#pragma unroll
-        for (int e = 0; e < KPT; ++e) {
-          const int over = max(0, kg * KPT + e - (nv - 1));
-          kr[e] = *reinterpret_cast<const u32x2*>(ksrc + (k_off[e] - (uint32_t)(over * D * 2)));
-        }
+      for (int e = 0; e < KPT; ++e) {
+        uint32_t off = k_off[e];
+        if constexpr (kSmallP) off -= (uint32_t)(max(0, kg * KPT + e - (nv - 1)) * D * 2);
+        kr[e] = *reinterpret_cast<const u32x2*>(ksrc + off);
       }
-      // advance; past the batch's last tile the cursor stays on it
-      if (it + 1 < iu_tiles) {
-        ++it;
-      } else if (iu + 1 < ue) {
-        ++iu;
-        it = 0;
-        iu_tiles = unit_tiles(iu);
+    };
+    auto issue_v = [&](const Cursor& c, int slot_v) {
+      int ws, nv; size_t hb;
+      tile_src(c, ws, nv, hb);
+      const char* vsrc = reinterpret_cast<const char*>(vb + hb * D * p.P + ws);   // [D][P]
+      uint8_t* vdst = &sm.vt[slot_v][wave * NV * 1024];
+#pragma unroll
+      for (int n = 0; n < NV; ++n) {
+        uint32_t off = v_off[n];
+        if constexpr (kSmallP) {
+          const int r = (wave * NV + n) * 8 + (lane >> 3);
+          off -= (uint32_t)(max(0, 8 * ((lane & 7) ^ swz8(r)) - (nv - 8)) * 2);
+        }
+        g2lds16(vsrc + off, vdst + n * 1024);
       }
     };
 
-    // Loads are issued unconditionally, two tiles ahead: past the end they
-    // re-read the last tile into a free slot and a register set that is
-    // never consumed. A fixed pattern keeps the in-order wait counts exact.
-    u32x2 krA[KPT], krB[KPT];
-    issue(krA, 0);
-    issue(krB, 1);
+    Cursor ck, cv;
+    cur_init(ck);
+    cur_init(cv);
+    u32x2 kr[KPT];
+    issue_v(cv, 0); cur_next(cv);
+    issue_k(kr, ck); cur_next(ck);
+    issue_v(cv, 1); cur_next(cv);
 
     // consume cursor
     int cu = ub, ct = 0, cu_tiles = unit_tiles(ub);
     double kacc[4] = {0.0, 0.0, 0.0, 0.0};
-    auto body = [&](int t, u32x2 (&kr)[KPT]) {
-      wait_vmcnt<kLoads>();               // tile t has landed; tile t+1 may be in flight
-      __builtin_amdgcn_sched_barrier(0);  // keep every use of tile t below the wait
+    for (int t = 0; t < total; ++t) {
+      wait_vmcnt<NV>();                   // K(t) and V(t) have landed; V(t+1) may be in flight
+      __builtin_amdgcn_sched_barrier(0);
+      // valid rows of this tile's window: [lo, hi)
       int k_beg, k_end;
       unit_keys(cu, k_beg, k_end);
       const int k0 = k_beg + ct * kTileKeys;
-      // phi, page sums, normaliser (registers only); rows past the unit's
-      // end (partial tiles only) contribute zeros
+      const int nv = min(kTileKeys, k_end - k0);
+      const int lo = kSmallP ? 0 : k0 - min(k0, k_end - kTileKeys);
+      const int hi = kSmallP ? nv : kTileKeys;
       float f[KPT][4];
       auto convert = [&](auto full) {
 #pragma unroll
         for (int e = 0; e < KPT; ++e) {
-          const bool ok = decltype(full)::value || k0 + kg * KPT + e < k_end;
+          const int row = kg * KPT + e;
+          const bool ok = decltype(full)::value || (row >= lo && row < hi);
           const float x[4] = {bf16_lo(kr[e].x), bf16_hi(kr[e].x), bf16_lo(kr[e].y), bf16_hi(kr[e].y)};
 #pragma unroll
           for (int c = 0; c < 4; ++c) {
@@ -184,14 +195,13 @@ __global__ __launch_bounds__(256, 2) void state_bf16_kernel(StateParams p) {
           }
         }
       };
-      if (k0 + kTileKeys <= k_end) convert(std::true_type{});
+      if (nv == kTileKeys) convert(std::true_type{});
       else convert(std::false_type{});
-      // every wave is done with tile t-1 (fk and its V slot) and tile t's V
-      // has landed in LDS
       lds_barrier();
-      issue(kr, (t + 2) % 3);
+      issue_k(kr, ck); cur_next(ck);
+      issue_v(cv, (t + 2) % 3); cur_next(cv);
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {              // phi(K)^T into LDS
+      for (int c = 0; c < 4; ++c) {
         const int row = dq * 4 + c;
         uint32_t w[KPT / 2];
 #pragma unroll
@@ -206,7 +216,6 @@ __global__ __launch_bounds__(256, 2) void state_bf16_kernel(StateParams p) {
         }
       }
       lds_barrier();
-      // S^T[j][i] += sum_key V^T[j][key] * phiK^T[i][key]
       const uint8_t* vt = sm.vt[t % 3];
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
@@ -223,9 +232,6 @@ __global__ __launch_bounds__(256, 2) void state_bf16_kernel(StateParams p) {
         }
       }
       if (++ct == cu_tiles) {
-        // unit done: its key sums, reduced over the KG key groups in a fixed
-        // order, into the batch's LDS slot (red is next rewritten after at
-        // least two more barriers)
 #pragma unroll
         for (int c = 0; c < 4; ++c) sm.red[kg * D + dq * 4 + c] = kacc[c];
         lds_barrier();
@@ -240,16 +246,10 @@ __global__ __launch_bounds__(256, 2) void state_bf16_kernel(StateParams p) {
         ct = 0;
         if (cu < ue) cu_tiles = unit_tiles(cu);
       }
-    };
-    // every back edge follows a krB tile, so the wait tracking sees one fixed
-    // load order at the loop head
-    for (int t = 0; t < total; t += 2) {
-      body(t, krA);
-      if (t + 1 >= total) break;
-      body(t + 1, krB);
     }
-    // the two trailing re-reads complete before the ring is reused or the
-    // workgroup's LDS is released; then the batch's page sums go out
+    // the trailing re-reads (the cursors stay on the batch's last tile)
+    // complete before the ring is reused or the workgroup's LDS is released;
+    // then the batch's page sums go out
     wait_vmcnt<0>();
     __syncthreads();
     double* dst = p.ws_k + ((size_t)bh * n_units + ub) * D;
@@ -394,8 +394,14 @@ hipError_t launch_state_update(int dtype, int d, int B, const StateParams& p,
                                const StateReduceParams& r, hipStream_t s) {
   const dim3 grid(B * p.H * p.n_groups);
   if (dtype == HSA_DTYPE_BF16) {
-    if (d == 128) state_bf16_kernel<128><<<grid, 256, 0, s>>>(p);
-    else state_bf16_kernel<64><<<grid, 256, 0, s>>>(p);
+    const bool small = p.P < kTileKeys;
+    if (d == 128) {
+      if (small) state_bf16_kernel<128, true><<<grid, 256, 0, s>>>(p);
+      else state_bf16_kernel<128, false><<<grid, 256, 0, s>>>(p);
+    } else {
+      if (small) state_bf16_kernel<64, true><<<grid, 256, 0, s>>>(p);
+      else state_bf16_kernel<64, false><<<grid, 256, 0, s>>>(p);
+    }
   } else {
     if (d == 128) state_f32_kernel<128><<<grid, 256, 0, s>>>(p);
     else state_f32_kernel<64><<<grid, 256, 0, s>>>(p);
