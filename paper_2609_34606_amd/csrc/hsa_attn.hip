@@ -65,14 +65,20 @@ __device__ __forceinline__ int swz_k(int row) {
 }
 __device__ __forceinline__ int swz_v(int row) { return (row >> 1) & 7; }  // 128-byte rows
 
-// Wave priority hooks around the MFMA-heavy phases (no-ops unless a build
-// defines them).
-#ifndef HSA_PRIO_MFMA
-#define HSA_PRIO_MFMA()
-#endif
-#ifndef HSA_PRIO_VALU
-#define HSA_PRIO_VALU()
-#endif
+// Schedule of a block of N (LDS read -> MFMA) pairs: the first kLdsAhead
+// reads, then one MFMA and one read alternately, then the last MFMAs. Each
+// MFMA's operand is then read kLdsAhead MFMAs before it is needed.
+constexpr int kLdsAhead = 4;
+template <int N>
+__device__ __forceinline__ void pipeline_lds_mfma() {
+  __builtin_amdgcn_sched_group_barrier(0x100, kLdsAhead, 0);  // LDS reads
+#pragma unroll
+  for (int i = 0; i < N - kLdsAhead; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);        // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);        // LDS read
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, kLdsAhead, 0);
+}
 
 // Score-tile row m holds key perm(m): bits 2 and 3 swapped, so that lane l's
 // score registers 0..7 are keys 8*(l/32)+0..7 and 8..15 are 16+8*(l/32)+0..7.
@@ -359,24 +365,30 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
     if (tile + 2 < ntiles) issue_k(kbuf == 0 ? 2 : kbuf - 1);   // ring slot (tile+2) % 3
     const int nv = min(kBN, P - t * kBN);
 
-    // S^T = K Q^T for the two 32-key halves of the tile
-    HSA_PRIO_MFMA();
+    // S^T = K Q^T for the two 32-key halves of the tile: the two MFMA chains
+    // alternate, and the key fragments are read from LDS kLdsAhead MFMAs
+    // before their use (an LDS read takes several MFMA durations).
     f32x16 s[2];
-    const uint8_t* kt_l = smem + kbuf * L::kKTile;
+    {
+      const uint8_t* kt_l = smem + kbuf * L::kKTile;
+      s[0] = f32x16{0};
+      s[1] = f32x16{0};
 #pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2) {
-      s[h2] = f32x16{0};
-      const int row = 32 * h2 + krow;
+      for (int kk = 0; kk < KK; ++kk)
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        const int chunk = 2 * kk + half;
-        const u32x4 a = ld_lds16(kt_l + row * L::kRowK + ((chunk ^ swz_k<D>(row)) << 4));
-        s[h2] = mfma32(a, qf[kk], s[h2]);
-      }
+        for (int h2 = 0; h2 < 2; ++h2) {
+          const int row = 32 * h2 + krow;
+          const int chunk = 2 * kk + half;
+          const u32x4 a = ld_lds16(kt_l + row * L::kRowK + ((chunk ^ swz_k<D>(row)) << 4));
+          s[h2] = mfma32(a, qf[kk], s[h2]);
+        }
+      pipeline_lds_mfma<2 * KK>();
     }
-    HSA_PRIO_VALU();
-    // keys past the end of the page
+    // keys past the end of the page (a partial tile: one in P/64). The empty
+    // asm keeps this a real branch: the compiler would otherwise apply the
+    // 32 selects to every tile, since they are no-ops on full ones.
     if (nv < kBN) {
+      asm volatile("" ::: "memory");
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
@@ -422,20 +434,21 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
                   pack_bf16(pv[8 * g + 4], pv[8 * g + 5]), pack_bf16(pv[8 * g + 6], pv[8 * g + 7])};
     }
     l_run += rs;
-    // O^T += V^T P^T
-    HSA_PRIO_MFMA();
-    const uint8_t* vt_l = smem + L::kVBase + (tile & 1) * L::kVTile;
+    // O^T += V^T P^T (NM independent chains), value fragments read ahead
+    {
+      const uint8_t* vt_l = smem + L::kVBase + (tile & 1) * L::kVTile;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const int chunk = 2 * ks + half;
+      for (int ks = 0; ks < 4; ++ks) {
+        const int chunk = 2 * ks + half;
 #pragma unroll
-      for (int m = 0; m < NM; ++m) {
-        const int row = 32 * m + l32;
-        const u32x4 a = ld_lds16(vt_l + row * L::kRowV + ((chunk ^ swz_v(row)) << 4));
-        acc[m] = mfma32(a, pb[ks], acc[m]);
+        for (int m = 0; m < NM; ++m) {
+          const int row = 32 * m + l32;
+          const u32x4 a = ld_lds16(vt_l + row * L::kRowV + ((chunk ^ swz_v(row)) << 4));
+          acc[m] = mfma32(a, pb[ks], acc[m]);
+        }
       }
+      pipeline_lds_mfma<4 * NM>();
     }
-    HSA_PRIO_VALU();
     if (++t == tpp) t = 0;
     kbuf = kbuf == 2 ? 0 : kbuf + 1;
   }
