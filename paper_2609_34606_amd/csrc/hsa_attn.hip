@@ -202,7 +202,7 @@ __device__ __forceinline__ void finish(const AttnParams& p, uint8_t* smem, int b
   }
 }
 
-template <int D>
+template <int D, bool kSmallP>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
   using L = AttnLayout<D>;
   constexpr int KK = D / 16;   // 16-wide d slices
@@ -299,45 +299,50 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
   for (int n = 0; n < L::kInstV; ++n) v_off[n] = (uint32_t)(v_row(n) * P + v_col(n)) * 2u;
 
   // Load cursors: keys run two tiles ahead of the tile being computed
-  // (3-slot ring), values one tile ahead (2-slot ring).
+  // (3-slot ring), values one tile ahead (2-slot ring). The last tile of a
+  // page (P not a multiple of 64) loads the 64-key window that ends at the
+  // page end: every load is then a scalar page base plus the constant
+  // per-lane offsets, with no branch, and the window's leading rows (keys
+  // of the previous tile) are masked. Pages shorter than a tile (kSmallP)
+  // clamp per lane instead. Past the last tile a cursor stays on it: the
+  // extra loads re-read it into ring slots nobody reads, so that every tile
+  // issues and waits alike; they are drained before the epilogue.
+  auto window = [&](int t) { return kSmallP ? t * kBN : min(t * kBN, P - kBN); };
   int kli = pg0, kt = 0, vli = pg0, vt = 0;
-  size_t khead = pg0 < pg1 ? head_of(pg0) : 0, vhead = khead;
+  const char* kbase = reinterpret_cast<const char*>(kpool) + (pg0 < pg1 ? head_of(pg0) : 0) * (size_t)P * D * 2;
+  const char* vbase = reinterpret_cast<const char*>(vpool) + (pg0 < pg1 ? head_of(pg0) : 0) * (size_t)D * P * 2;
   auto issue_k = [&](int buf) {
-    const int k0 = kt * kBN, nv = min(kBN, P - k0);
-    const char* src = reinterpret_cast<const char*>(kpool + (khead * P + k0) * D);
+    const char* src = kbase + (size_t)window(kt) * D * 2;
     uint8_t* dst = smem + buf * L::kKTile + wave * L::kInstK * 1024;
-    if (nv == kBN) {
 #pragma unroll
-      for (int n = 0; n < L::kInstK; ++n) g2lds16(src + k_off[n], dst + n * 1024);
-    } else {
-#pragma unroll
-      for (int n = 0; n < L::kInstK; ++n) {
-        const int over = max(0, k_row(n) - (nv - 1));   // rows past the page end
-        g2lds16(src + (k_off[n] - (uint32_t)(over * D * 2)), dst + n * 1024);
-      }
+    for (int n = 0; n < L::kInstK; ++n) {
+      uint32_t off = k_off[n];
+      if constexpr (kSmallP) off -= (uint32_t)(max(0, k_row(n) - (P - 1)) * D * 2);
+      g2lds16(src + off, dst + n * 1024);
     }
-    if (++kt == tpp) {
+    if (kt + 1 < tpp) {
+      ++kt;
+    } else if (kli + 1 < pg1) {
       kt = 0;
-      if (++kli < pg1) khead = head_of(kli);
+      ++kli;
+      kbase = reinterpret_cast<const char*>(kpool) + head_of(kli) * (size_t)P * D * 2;
     }
   };
   auto issue_v = [&](int buf) {
-    const int k0 = vt * kBN, nv = min(kBN, P - k0);
-    const char* src = reinterpret_cast<const char*>(vpool + vhead * D * P + k0);
+    const char* src = vbase + (size_t)window(vt) * 2;
     uint8_t* dst = smem + L::kVBase + buf * L::kVTile + wave * L::kInstV * 1024;
-    if (nv == kBN) {
 #pragma unroll
-      for (int n = 0; n < L::kInstV; ++n) g2lds16(src + v_off[n], dst + n * 1024);
-    } else {
-#pragma unroll
-      for (int n = 0; n < L::kInstV; ++n) {
-        const int over = max(0, v_col(n) - (nv - 8));
-        g2lds16(src + (v_off[n] - (uint32_t)(over * 2)), dst + n * 1024);
-      }
+    for (int n = 0; n < L::kInstV; ++n) {
+      uint32_t off = v_off[n];
+      if constexpr (kSmallP) off -= (uint32_t)(max(0, v_col(n) - (P - 8)) * 2);
+      g2lds16(src + off, dst + n * 1024);
     }
-    if (++vt == tpp) {
+    if (vt + 1 < tpp) {
+      ++vt;
+    } else if (vli + 1 < pg1) {
       vt = 0;
-      if (++vli < pg1) vhead = head_of(vli);
+      ++vli;
+      vbase = reinterpret_cast<const char*>(vpool) + head_of(vli) * (size_t)D * P * 2;
     }
   };
 
@@ -352,18 +357,16 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
   if (ntiles > 0) {
     issue_k(0);
     issue_v(0);
-    if (ntiles > 1) issue_k(1);
+    issue_k(1);
   }
   int t = 0, kbuf = 0;
   for (int tile = 0; tile < ntiles; ++tile) {
-    // K(tile) and V(tile) have landed once at most the next key tile's loads
-    // are outstanding
-    if (tile + 1 < ntiles) wait_vmcnt<L::kInstK>();
-    else wait_vmcnt<0>();
+    // K(tile) and V(tile) have landed once at most the next key tile's
+    // loads are outstanding
+    wait_vmcnt<L::kInstK>();
     lds_barrier();
-    if (tile + 1 < ntiles) issue_v((tile + 1) & 1);
-    if (tile + 2 < ntiles) issue_k(kbuf == 0 ? 2 : kbuf - 1);   // ring slot (tile+2) % 3
-    const int nv = min(kBN, P - t * kBN);
+    issue_v((tile + 1) & 1);
+    issue_k(kbuf == 0 ? 2 : kbuf - 1);   // ring slot (tile+2) % 3
 
     // S^T = K Q^T for the two 32-key halves of the tile: the two MFMA chains
     // alternate, and the key fragments are read from LDS kLdsAhead MFMAs
@@ -384,31 +387,35 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
         }
       pipeline_lds_mfma<2 * KK>();
     }
-    // keys past the end of the page (a partial tile: one in P/64). The empty
-    // asm keeps this a real branch: the compiler would otherwise apply the
-    // 32 selects to every tile, since they are no-ops on full ones.
+    // The last tile of a page: window rows holding keys outside the tile
+    // are masked (leading rows of the page-end window, or rows past the page
+    // for pages shorter than a tile). The empty asm keeps this a real branch:
+    // the compiler would otherwise apply the selects to every tile.
+    const int nv = min(kBN, P - t * kBN);
     if (nv < kBN) {
       asm volatile("" ::: "memory");
+      const int lo = kSmallP ? 0 : kBN - nv, hi = kSmallP ? nv : kBN;
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int key = 32 * h2 + 16 * (r >> 3) + 8 * half + (r & 7);
-          if (key >= nv) s[h2][r] = -INFINITY;
+          if (key < lo || key >= hi) s[h2][r] = -INFINITY;
         }
     }
     // Online softmax against a reference max m_run (raw score units) that
-    // only moves when the tile max exceeds it by more than 8 in exp2 units:
-    // exponentials stay <= 256 and the final normalisation by the row sum is
-    // exact for any reference.
+    // only moves when some score exceeds it by more than 8 in exp2 units:
+    // exponentials stay <= 256 and the final normalisation by the row sum
+    // is exact for any reference. The test uses each lane's own 32 scores;
+    // only when it fires are the two lane halves of a query combined.
     float mx = fmaxf(s[0][0], s[0][1]);
 #pragma unroll
     for (int r = 2; r < 16; ++r) mx = fmaxf(mx, s[0][r]);
 #pragma unroll
     for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[1][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const bool grow = mx * c2 > m_run * c2 + 8.f;
-    if (__any(grow)) {
+    if (__any(mx * c2 > m_run * c2 + 8.f)) {
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const bool grow = mx * c2 > m_run * c2 + 8.f;
       const float m_new = grow ? mx : m_run;
       const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c2);
       l_run *= alpha;
@@ -452,6 +459,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
     if (++t == tpp) t = 0;
     kbuf = kbuf == 2 ? 0 : kbuf + 1;
   }
+  wait_vmcnt<0>();  // the trailing re-reads
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   const float inv_l = l_tot > 0.f ? 1.f / l_tot : 0.f;
@@ -832,8 +840,14 @@ void plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_
 hipError_t launch_attention(int dtype, int d, int B, const AttnParams& p, hipStream_t s) {
   if (dtype == HSA_DTYPE_BF16) {
     const dim3 grid(8 * std::max(1, p.sc.xcd_items), B);
-    if (d == 128) attn_bf16_kernel<128><<<grid, 256, 0, s>>>(p);
-    else attn_bf16_kernel<64><<<grid, 256, 0, s>>>(p);
+    const bool small = p.P < kBN;
+    if (d == 128) {
+      if (small) attn_bf16_kernel<128, true><<<grid, 256, 0, s>>>(p);
+      else attn_bf16_kernel<128, false><<<grid, 256, 0, s>>>(p);
+    } else {
+      if (small) attn_bf16_kernel<64, true><<<grid, 256, 0, s>>>(p);
+      else attn_bf16_kernel<64, false><<<grid, 256, 0, s>>>(p);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.sc.n_chead == 0) return e;
     const dim3 cgrid(p.sc.n_chead * p.sc.nqt, B);
