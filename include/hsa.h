@@ -57,6 +57,16 @@ extern "C" {
 #define HSA_MAX_HEADS 64
 #define HSA_MAX_LIST 1024 /* k_max + n_cur_pages per head */
 #define HSA_MAX_CAND 8192 /* history pages a selection can score */
+#define HSA_MAX_BLOCKS 4096 /* key blocks of one head's list (adaptive calls) */
+
+/* Block geometry of the head-adaptive sparse branch (Sec. 3.3, granularity
+ * of the sparse branch): history pages are cut into blocks of
+ * HSA_BLOCK_HIST tokens, the current chunk's pages into blocks of
+ * HSA_BLOCK_CUR tokens, the query chunk into blocks of HSA_BLOCK_Q queries
+ * (the last block of a page or of the chunk may be shorter). */
+#define HSA_BLOCK_Q 64
+#define HSA_BLOCK_HIST 128
+#define HSA_BLOCK_CUR 64
 
 typedef enum hsa_status {
   HSA_OK = 0,
@@ -97,6 +107,16 @@ size_t hsa_sparse_attn_workspace_size(const hsa_config_t* cfg, int32_t n_q,
                                       int32_t k_max, int32_t n_cur_pages);
 size_t hsa_forward_workspace_size(const hsa_config_t* cfg, int32_t n_q,
                                   int32_t k_max, int32_t n_cur_pages);
+/* One workspace size for hsa_block_select, hsa_sparse_attn_adaptive and
+ * hsa_forward_adaptive. */
+size_t hsa_adaptive_workspace_size(const hsa_config_t* cfg, int32_t n_q,
+                                   int32_t k_max, int32_t n_cur_pages);
+
+/* Key blocks of a list of n_hist_pages history pages and n_cur_pages current
+ * pages: n_hist_pages * ceil(P / HSA_BLOCK_HIST) + n_cur_pages * ceil(P /
+ * HSA_BLOCK_CUR). With n_hist_pages = k_max it is the row length of the
+ * per-block outputs of hsa_block_select. Returns -1 on invalid input. */
+int32_t hsa_block_count(const hsa_config_t* cfg, int32_t n_hist_pages, int32_t n_cur_pages);
 
 /*
  * hsa_state_update -- fold logical pages [first_page, first_page+n_pages) of
@@ -210,6 +230,81 @@ hsa_status_t hsa_forward_selected(const hsa_config_t* cfg, const void* q, int32_
                                   int32_t n_cur_pages, const float* kv_state,
                                   const float* k_state, const float* g_lin, const float* g_sp,
                                   void* o, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Head-adaptive block-sparse sparse branch (Sec. 3.3 "Sparse branch" and
+ * "Head-level sparsity adaptation"; the appendix on the sparse branch defines
+ * the pooled map, the coverage rule and the Gini coefficient; Sec. 4.5 fixes
+ * (tau_max, tau_min) = (1.00, 0.35)).
+ *
+ * Per batch entry and head h the active pages are those of hsa_sparse_attn
+ * (sel[b][h][0..) up to the first entry outside [0, max_pages), then the
+ * current pages), cut into key blocks (HSA_BLOCK_HIST tokens per block in a
+ * history page, HSA_BLOCK_CUR in a current page) numbered j = 0..N-1 in list
+ * order, block by block inside each page. Query block i holds queries
+ * [HSA_BLOCK_Q i, HSA_BLOCK_Q (i+1)) of the chunk. With qbar_i and kbar_j the
+ * means of the block's queries and keys and s = sm_scale (0: 1/sqrt(d)):
+ *   p_i,j = softmax_j(s * qbar_i . kbar_j)                      (pooled map)
+ *   G     = (1/n_qb) sum_i (1/N) sum_m (N - 2m + 1) p_i,(m)      (Gini; p_i,(m)
+ *           the m-th largest weight of row i, m = 1..N)
+ *   tau   = tau_min + G (tau_max - tau_min)
+ * and query block i keeps the shortest prefix of its blocks in the order
+ * (weight descending, block id ascending) whose running weight reaches tau
+ * (every block if rounding keeps the total below tau, and every block when
+ * tau >= 1). All of it is fp64.
+ * Query block i then attends exactly to the keys of its kept blocks (App.
+ * A.1 eq. attention with a zero mask on them and -inf elsewhere).
+ * tau_min, tau_max: 0 <= tau_min <= tau_max <= 1. N must not exceed
+ * HSA_MAX_BLOCKS (UNSUPPORTED). Other arguments and errors as hsa_sparse_attn.
+ * ws: hsa_adaptive_workspace_size(cfg, n_q, k_max, n_cur_pages) bytes.
+ */
+
+/*
+ * hsa_block_select -- the block selection alone, for inspection: gini[b][h]
+ * = G, tau[b][h] = tau (device fp64 [B, H], nullable), n_kept[b][h][i] the
+ * kept count of query block i (device int32 [B, H, n_qb], nullable), kept
+ * [b][h][i][0..n_kept) the kept block ids in selection order and -1 after
+ * (device int32 [B, H, n_qb, kept_len], nullable), pooled[b][h][i][j] = p_i,j
+ * in block order, 0 past N (device fp64 [B, H, n_qb, kept_len], nullable),
+ * with n_qb = ceil(n_q / HSA_BLOCK_Q) and kept_len >= hsa_block_count(cfg,
+ * k_max, n_cur_pages) when kept or pooled is given.
+ */
+hsa_status_t hsa_block_select(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                              const hsa_kv_pool_t* pool, const int32_t* sel, int32_t k_max,
+                              int32_t cur_first_page, int32_t n_cur_pages, double tau_min,
+                              double tau_max, double* gini, double* tau, int32_t* n_kept,
+                              int32_t* kept, double* pooled, int32_t kept_len, void* ws,
+                              size_t ws_bytes, void* stream);
+
+/*
+ * hsa_sparse_attn_adaptive -- the block-sparse sparse branch: block selection
+ * as above, then for every query i of query block qb
+ *   o_sp[b][i][h] = sum_j softmax_j(scale * q_i . k_j) v_j,  lse[b][h][i] = log sum_j exp(...)
+ * over the keys j of the blocks qb keeps (fp32 outputs, lse nullable). k_h:
+ * host int32 [H] upper bounds on the valid entries of each sel row (the work
+ * split is planned from them), or NULL meaning k_max.
+ */
+hsa_status_t hsa_sparse_attn_adaptive(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                                      const hsa_kv_pool_t* pool, const int32_t* sel,
+                                      int32_t k_max, const int32_t* k_h, int32_t cur_first_page,
+                                      int32_t n_cur_pages, double tau_min, double tau_max,
+                                      float* o_sp, float* lse, void* ws, size_t ws_bytes,
+                                      void* stream);
+
+/*
+ * hsa_forward_adaptive -- hsa_forward with the block-sparse sparse branch:
+ * page selection over candidates [0, n_cand), block selection over the
+ * selected pages and the current pages [n_cand, n_cand + n_cur_pages), the
+ * block-sparse sparse branch, the linear branch and the gated fusion.
+ * Arguments and errors as hsa_forward plus the two thresholds.
+ */
+hsa_status_t hsa_forward_adaptive(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                                  const hsa_kv_pool_t* pool, int32_t n_cand,
+                                  int32_t n_cur_pages, const int32_t* k_h, int32_t k_max,
+                                  double tau_min, double tau_max, const float* kv_state,
+                                  const float* k_state, const double* page_kmean,
+                                  const float* g_lin, const float* g_sp, void* o,
+                                  int32_t* sel_out, void* ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -25,7 +25,8 @@ Readings (where the paper leaves a choice open; listed in the design notes):
     of a page is shorter when B does not divide the page); pages are never
     merged into one block; query blocks are consecutive runs of 64 queries;
   * the kept prefix uses the order (weight descending, block index
-    ascending); if rounding keeps the total below tau_h, every block is kept;
+    ascending); if rounding keeps the total below tau_h, every block is kept,
+    and tau_h >= 1 keeps every block (the running sum may round to 1 early);
   * key blocks of one head are numbered page by page in list order (the
     selected history pages first, then the current chunk's pages).
 
@@ -71,8 +72,13 @@ def block_means(x: np.ndarray, bounds: Sequence[Tuple[int, int]]) -> np.ndarray:
 
 
 def pooled_map(qbar: np.ndarray, kbar: np.ndarray, scale: float) -> np.ndarray:
-    """Block attention weights: row softmax of qbar kbar^T * scale. [NQ,N]."""
-    s = (np.asarray(qbar, np.float64) @ np.asarray(kbar, np.float64).T) * scale
+    """Block attention weights: row softmax of qbar kbar^T * scale. [NQ,N].
+
+    Each score is its own sum over d (not a blocked matrix product), so equal
+    key blocks get bit-equal weights and their tie falls to the block id."""
+    qbar = np.asarray(qbar, np.float64)
+    kbar = np.asarray(kbar, np.float64)
+    s = (qbar[:, None, :] * kbar[None, :, :]).sum(axis=-1) * scale
     s -= s.max(axis=1, keepdims=True)
     e = np.exp(s)
     return e / e.sum(axis=1, keepdims=True)
@@ -103,8 +109,12 @@ def coverage_threshold(g: float, tau_min: float = TAU_MIN, tau_max: float = TAU_
 
 def select_blocks(p_row: np.ndarray, tau: float) -> np.ndarray:
     """Shortest prefix of the descending order whose running sum (in that
-    order) reaches tau; all blocks when it never does."""
+    order) reaches tau; all blocks when it never does. A threshold of 1 or
+    more is the whole mass, so it keeps every block whatever the rounding of
+    the running sum."""
     order = block_order(p_row)
+    if tau >= 1.0:
+        return order
     c = np.cumsum(np.asarray(p_row, np.float64)[order])
     hit = np.nonzero(c >= tau)[0]
     k = (hit[0] + 1) if hit.size else order.size
@@ -180,7 +190,7 @@ def hsa_forward_adaptive(q, k_pool, v_pool, page_table, n_cand: int, n_cur: int,
     cur_pages = list(range(n_cand, n_cand + n_cur))
     out = {"O": np.zeros((B, nr, H, d)), "O_sp": np.zeros((B, nr, H, d)), "lse": np.zeros((B, H, nr)),
            "sel": np.full((B, H, max(1, max(k_h))), -1, np.int64), "gini": np.zeros((B, H)),
-           "tau": np.zeros((B, H)), "kept": {}, "rows": rows}
+           "tau": np.zeros((B, H)), "kept": {}, "pooled": {}, "rows": rows}
     for b in range(B):
         for h in heads:
             cand = [O.page_key_mean(k_pool[int(page_table[b, p]), h]) for p in range(n_cand)]
@@ -194,6 +204,7 @@ def hsa_forward_adaptive(q, k_pool, v_pool, page_table, n_cand: int, n_cur: int,
                               tau_min, tau_max, query_blocks=qsel)
             out["gini"][b, h], out["tau"][b, h] = r["gini"], r["tau"]
             out["kept"][(b, h)] = r["kept"]
+            out["pooled"][(b, h)] = r["pooled"]
             out["O_sp"][b, :, h] = r["O_sp"]
             out["lse"][b, h] = r["lse"]
             kl, vl = O.gather_pages(k_pool, v_pool, page_table, b, h, state_pages)

@@ -11,7 +11,14 @@ from .hsa import (  # noqa: F401
     HsaError,
     HsaKvPool,
     LibraryNotBuilt,
+    TAU_MAX,
+    TAU_MIN,
     config,
+    hsa_adaptive_workspace_size,
+    hsa_block_count,
+    hsa_block_select,
+    hsa_forward_adaptive,
+    hsa_sparse_attn_adaptive,
     hsa_forward,
     hsa_forward_selected,
     hsa_forward_workspace_size,

@@ -183,6 +183,140 @@ hsa_status_t check_budgets(const hsa_config_t* c, const int32_t* k_h, int k_max)
   return HSA_OK;
 }
 
+// ---------------------------------------------------------------- block-sparse mode
+static_assert(kQsumRows * 2 == kBlockQ, "query blocks are two query-sum splits");
+
+int blocks_per_page(int P, int B) { return (P + B - 1) / B; }
+
+int block_count(const hsa_config_t* c, int n_hist, int n_cur) {
+  return n_hist * blocks_per_page(c->page_size, kBlockHist) +
+         n_cur * blocks_per_page(c->page_size, kBlockCur);
+}
+
+// Workspace of the adaptive calls: [query sums][sel][block means][sorted
+// rows: running weight, block id][Gini terms][tile lists][list lengths]
+// [partial outputs].
+struct AdaptiveWs {
+  int n_qb, n_qt, n_blk_max, n_pad, cap, rpg;
+  size_t sel_off, kbar_off, rc_off, ri_off, rg_off, bl_off, bll_off, part_off, total;
+};
+
+AdaptiveWs adaptive_ws(const hsa_config_t* c, int n_q, int k_max, int n_cur) {
+  AdaptiveWs w{};
+  const size_t bh = (size_t)c->batch * c->num_heads, d = c->head_dim;
+  w.n_qb = (n_q + kBlockQ - 1) / kBlockQ;
+  w.n_qt = (n_q + 2 * kBlockQ - 1) / (2 * kBlockQ);
+  w.n_blk_max = block_count(c, k_max, n_cur);
+  w.n_pad = 64;
+  while (w.n_pad < w.n_blk_max) w.n_pad <<= 1;
+  w.cap = std::max(1, (k_max + n_cur) * blocks_per_page(c->page_size, 64));
+  w.rpg = 4;
+  while (w.rpg > 1 && block_rows_lds_bytes(c->head_dim, w.n_pad, w.rpg) > 65536) w.rpg >>= 1;
+  const size_t nb = std::max(1, w.n_blk_max);
+  w.sel_off = select_ws_bytes(c, n_q);
+  w.kbar_off = w.sel_off + sel_ws_bytes(c, k_max);
+  w.rc_off = w.kbar_off + align_up(bh * d * nb * 8);
+  w.ri_off = w.rc_off + align_up(bh * w.n_qb * nb * 8);
+  w.rg_off = w.ri_off + align_up(bh * w.n_qb * nb * 4);
+  w.bl_off = w.rg_off + align_up(bh * w.n_qb * 8);
+  w.bll_off = w.bl_off + align_up(bh * w.n_qt * (size_t)w.cap * 8);
+  w.part_off = w.bll_off + align_up(bh * w.n_qt * 4);
+  w.total = w.part_off + partial_ws_bytes(c, n_q);
+  return w;
+}
+
+hsa_status_t check_taus(double tau_min, double tau_max) {
+  if (!(tau_min >= 0.0 && tau_min <= tau_max && tau_max <= 1.0)) return HSA_ERR_INVALID_ARG;
+  return HSA_OK;
+}
+
+double pooled_scale(const hsa_config_t* c) {
+  return c->sm_scale > 0.f ? (double)c->sm_scale : 1.0 / sqrt((double)c->head_dim);
+}
+
+// Outputs of the selection that hsa_block_select exposes (all nullable).
+struct BlockSelOut {
+  double* gini = nullptr;
+  double* tau = nullptr;
+  int32_t* n_kept = nullptr;
+  int32_t* kept = nullptr;
+  double* pooled = nullptr;
+  int32_t kept_len = 0;
+};
+
+// Block selection over the lists of sel + [cur_first, cur_first + n_cur);
+// the query sums are computed first unless the page selection already left
+// them in the workspace.
+hsa_status_t run_block_select(const hsa_config_t* c, const void* q, int n_q,
+                              const hsa_kv_pool_t* pool, const int32_t* sel, int k_max,
+                              int cur_first, int n_cur, double tau_min, double tau_max,
+                              const AdaptiveWs& w, uint8_t* base, bool have_qsum,
+                              const BlockSelOut& out, hipStream_t s) {
+  QsumParams qp{};
+  qp.q = q;
+  qp.n_q = n_q;
+  qp.HD = c->num_heads * c->head_dim;
+  qp.rows_per_split = kQsumRows;
+  qp.n_split = qsum_splits(n_q);
+  qp.ws_qs = reinterpret_cast<double*>(base);
+  if (!have_qsum) {
+    const hipError_t e = launch_qsum(c->dtype, c->batch, qp, s);
+    if (e != hipSuccess) return HSA_ERR_DEVICE;
+  }
+  BlockSelParams p{};
+  p.k = pool->k;
+  p.page_table = pool->page_table;
+  p.sel = sel;
+  p.H = c->num_heads;
+  p.P = c->page_size;
+  p.n_q = n_q;
+  p.num_slots = pool->num_slots;
+  p.max_pages = pool->max_pages;
+  p.k_max = k_max;
+  p.cur_first = cur_first;
+  p.n_cur = n_cur;
+  p.n_qb = w.n_qb;
+  p.n_qt = w.n_qt;
+  p.n_blk_max = w.n_blk_max;
+  p.n_pad = w.n_pad;
+  p.rpg = w.rpg;
+  p.qs_split = qp.n_split;
+  p.scale = pooled_scale(c);
+  p.tau_min = tau_min;
+  p.tau_max = tau_max;
+  p.ws_qs = qp.ws_qs;
+  p.kbar_t = reinterpret_cast<double*>(base + w.kbar_off);
+  p.row_c = reinterpret_cast<double*>(base + w.rc_off);
+  p.row_i = reinterpret_cast<int32_t*>(base + w.ri_off);
+  p.row_g = reinterpret_cast<double*>(base + w.rg_off);
+  p.blist = reinterpret_cast<int2*>(base + w.bl_off);
+  p.blist_len = reinterpret_cast<int32_t*>(base + w.bll_off);
+  p.blist_cap = w.cap;
+  p.gini = out.gini;
+  p.tau = out.tau;
+  p.n_kept = out.n_kept;
+  p.kept = out.kept;
+  p.kept_len = out.kept_len;
+  p.pooled = out.pooled;
+  return from_hip(launch_block_select(c->dtype, c->head_dim, c->batch, p, s));
+}
+
+void set_block_lists(AttnParams& p, const AdaptiveWs& w, uint8_t* base) {
+  p.blist = reinterpret_cast<const int2*>(base + w.bl_off);
+  p.blist_len = reinterpret_cast<const int32_t*>(base + w.bll_off);
+  p.blist_cap = w.cap;
+}
+
+// Checks shared by the adaptive calls on top of their base call's checks.
+hsa_status_t check_adaptive(const hsa_config_t* c, int n_q, int k_max, int n_cur, double tau_min,
+                            double tau_max) {
+  hsa_status_t st = check_taus(tau_min, tau_max);
+  if (st != HSA_OK) return st;
+  if (block_count(c, k_max, n_cur) > HSA_MAX_BLOCKS) return HSA_ERR_UNSUPPORTED;
+  (void)n_q;
+  return HSA_OK;
+}
+
 hsa_status_t run_select(const hsa_config_t* c, const void* q, int n_q, const double* kmean,
                         int max_pages, int n_cand, const int32_t* k_h, int k_max, int32_t* sel,
                         double* sel_score, void* ws, hipStream_t s) {
@@ -206,6 +340,58 @@ hsa_status_t run_select(const hsa_config_t* c, const void* q, int n_q, const dou
   sp.sel = sel;
   sp.sel_score = sel_score;
   return from_hip(launch_page_select(c->dtype, c->head_dim, c->batch, qp, sp, s));
+}
+
+hsa_status_t check_sparse(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                          const hsa_kv_pool_t* pool, const int32_t* sel, int32_t k_max,
+                          const int32_t* k_h, int32_t cur_first_page, int32_t n_cur_pages,
+                          const float* o_sp) {
+  hsa_status_t st = check_cfg(cfg);
+  if (st != HSA_OK) return st;
+  if ((st = check_pool(pool)) != HSA_OK) return st;
+  if (!q || !o_sp || n_q < 1 || k_max < 0 || n_cur_pages < 0 || cur_first_page < 0)
+    return HSA_ERR_INVALID_ARG;
+  if (k_max > 0 && !sel) return HSA_ERR_INVALID_ARG;
+  if (k_max == 0 && n_cur_pages == 0) return HSA_ERR_INVALID_ARG;
+  if ((long)cur_first_page + n_cur_pages > pool->max_pages) return HSA_ERR_OUT_OF_RANGE;
+  if ((long)k_max + n_cur_pages > HSA_MAX_LIST) return HSA_ERR_UNSUPPORTED;
+  return check_budgets(cfg, k_h, k_max);
+}
+
+// The sparse branch alone; w != NULL walks the tile lists of a block
+// selection already in the workspace.
+hsa_status_t run_sparse(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                        const hsa_kv_pool_t* pool, const int32_t* sel, int32_t k_max,
+                        const int32_t* k_h, int32_t cur_first_page, int32_t n_cur_pages,
+                        float* o_sp, float* lse, void* partials, const AdaptiveWs* w,
+                        hipStream_t s) {
+  AttnParams p{};
+  p.q = q;
+  p.k = pool->k;
+  p.v = pool->v;
+  p.page_table = pool->page_table;
+  p.sel = sel;  // not read when k_max == 0
+  p.H = cfg->num_heads;
+  p.P = cfg->page_size;
+  p.n_q = n_q;
+  p.num_slots = pool->num_slots;
+  p.max_pages = pool->max_pages;
+  p.k_max = k_max;
+  p.cur_first = cur_first_page;
+  p.n_cur = n_cur_pages;
+  p.sm_scale = softmax_scale(cfg);
+  p.scale_log2 = p.sm_scale * 1.4426950408889634f;
+  p.mode = ATTN_SPARSE;
+  p.o_sp = o_sp;
+  p.lse = lse;
+  int list_len[HSA_MAX_HEADS];
+  for (int h = 0; h < cfg->num_heads; ++h)
+    list_len[h] = std::min(k_h ? k_h[h] : k_max, pool->max_pages) + n_cur_pages;
+  plan_attention(p, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
+                 kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16);
+  if (cfg->dtype == HSA_DTYPE_BF16) set_partials(p, cfg, n_q, partials);
+  if (w) set_block_lists(p, *w, static_cast<uint8_t*>(partials) - w->part_off);
+  return from_hip(launch_attention(cfg->dtype, cfg->head_dim, cfg->batch, p, s));
 }
 
 }  // namespace
@@ -318,46 +504,84 @@ hsa_status_t hsa_sparse_attn(const hsa_config_t* cfg, const void* q, int32_t n_q
                              const hsa_kv_pool_t* pool, const int32_t* sel, int32_t k_max,
                              const int32_t* k_h, int32_t cur_first_page, int32_t n_cur_pages,
                              float* o_sp, float* lse, void* ws, size_t ws_bytes, void* stream) {
+  hsa_status_t st = check_sparse(cfg, q, n_q, pool, sel, k_max, k_h, cur_first_page, n_cur_pages,
+                                 o_sp);
+  if (st != HSA_OK) return st;
+  if ((st = check_ws(ws, ws_bytes, partial_ws_bytes(cfg, n_q))) != HSA_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = validate_pages(cfg, pool, cur_first_page, n_cur_pages, s)) != HSA_OK) return st;
+  if ((st = validate_selection(cfg, pool, sel, k_max, s)) != HSA_OK) return st;
+  return run_sparse(cfg, q, n_q, pool, sel, k_max, k_h, cur_first_page, n_cur_pages, o_sp, lse, ws,
+                    nullptr, s);
+}
+
+size_t hsa_adaptive_workspace_size(const hsa_config_t* cfg, int32_t n_q, int32_t k_max,
+                                   int32_t n_cur_pages) {
+  if (check_cfg(cfg) != HSA_OK || n_q < 1 || k_max < 0 || n_cur_pages < 0) return 0;
+  if ((long)k_max + n_cur_pages > HSA_MAX_LIST) return 0;
+  return adaptive_ws(cfg, n_q, k_max, n_cur_pages).total;
+}
+
+int32_t hsa_block_count(const hsa_config_t* cfg, int32_t n_hist_pages, int32_t n_cur_pages) {
+  if (check_cfg(cfg) != HSA_OK || n_hist_pages < 0 || n_cur_pages < 0) return -1;
+  if ((long)n_hist_pages + n_cur_pages > HSA_MAX_LIST) return -1;
+  return block_count(cfg, n_hist_pages, n_cur_pages);
+}
+
+hsa_status_t hsa_block_select(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                              const hsa_kv_pool_t* pool, const int32_t* sel, int32_t k_max,
+                              int32_t cur_first_page, int32_t n_cur_pages, double tau_min,
+                              double tau_max, double* gini, double* tau, int32_t* n_kept,
+                              int32_t* kept, double* pooled, int32_t kept_len, void* ws,
+                              size_t ws_bytes, void* stream) {
   hsa_status_t st = check_cfg(cfg);
   if (st != HSA_OK) return st;
   if ((st = check_pool(pool)) != HSA_OK) return st;
-  if (!q || !o_sp || n_q < 1 || k_max < 0 || n_cur_pages < 0 || cur_first_page < 0)
+  if (!q || n_q < 1 || k_max < 0 || n_cur_pages < 0 || cur_first_page < 0)
     return HSA_ERR_INVALID_ARG;
   if (k_max > 0 && !sel) return HSA_ERR_INVALID_ARG;
   if (k_max == 0 && n_cur_pages == 0) return HSA_ERR_INVALID_ARG;
   if ((long)cur_first_page + n_cur_pages > pool->max_pages) return HSA_ERR_OUT_OF_RANGE;
   if ((long)k_max + n_cur_pages > HSA_MAX_LIST) return HSA_ERR_UNSUPPORTED;
-  if ((st = check_budgets(cfg, k_h, k_max)) != HSA_OK) return st;
-  if ((st = check_ws(ws, ws_bytes, partial_ws_bytes(cfg, n_q))) != HSA_OK) return st;
+  if ((st = check_adaptive(cfg, n_q, k_max, n_cur_pages, tau_min, tau_max)) != HSA_OK) return st;
+  if ((kept || pooled) && kept_len < block_count(cfg, k_max, n_cur_pages)) return HSA_ERR_INVALID_ARG;
+  const AdaptiveWs w = adaptive_ws(cfg, n_q, k_max, n_cur_pages);
+  if ((st = check_ws(ws, ws_bytes, w.total)) != HSA_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if ((st = validate_pages(cfg, pool, cur_first_page, n_cur_pages, s)) != HSA_OK) return st;
   if ((st = validate_selection(cfg, pool, sel, k_max, s)) != HSA_OK) return st;
-  AttnParams p{};
-  p.q = q;
-  p.k = pool->k;
-  p.v = pool->v;
-  p.page_table = pool->page_table;
-  p.sel = sel;  // not read when k_max == 0
-  p.H = cfg->num_heads;
-  p.P = cfg->page_size;
-  p.n_q = n_q;
-  p.num_slots = pool->num_slots;
-  p.max_pages = pool->max_pages;
-  p.k_max = k_max;
-  p.cur_first = cur_first_page;
-  p.n_cur = n_cur_pages;
-  p.sm_scale = softmax_scale(cfg);
-  p.scale_log2 = p.sm_scale * 1.4426950408889634f;
-  p.mode = ATTN_SPARSE;
-  p.o_sp = o_sp;
-  p.lse = lse;
-  int list_len[HSA_MAX_HEADS];
-  for (int h = 0; h < cfg->num_heads; ++h)
-    list_len[h] = std::min(k_h ? k_h[h] : k_max, pool->max_pages) + n_cur_pages;
-  plan_attention(p, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
-                 kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16);
-  if (cfg->dtype == HSA_DTYPE_BF16) set_partials(p, cfg, n_q, ws);
-  return from_hip(launch_attention(cfg->dtype, cfg->head_dim, cfg->batch, p, s));
+  BlockSelOut out;
+  out.gini = gini;
+  out.tau = tau;
+  out.n_kept = n_kept;
+  out.kept = kept;
+  out.pooled = pooled;
+  out.kept_len = kept_len;
+  return run_block_select(cfg, q, n_q, pool, sel, k_max, cur_first_page, n_cur_pages, tau_min,
+                          tau_max, w, static_cast<uint8_t*>(ws), false, out, s);
+}
+
+hsa_status_t hsa_sparse_attn_adaptive(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                                      const hsa_kv_pool_t* pool, const int32_t* sel,
+                                      int32_t k_max, const int32_t* k_h, int32_t cur_first_page,
+                                      int32_t n_cur_pages, double tau_min, double tau_max,
+                                      float* o_sp, float* lse, void* ws, size_t ws_bytes,
+                                      void* stream) {
+  hsa_status_t st = check_sparse(cfg, q, n_q, pool, sel, k_max, k_h, cur_first_page, n_cur_pages,
+                                 o_sp);
+  if (st != HSA_OK) return st;
+  if ((st = check_adaptive(cfg, n_q, k_max, n_cur_pages, tau_min, tau_max)) != HSA_OK) return st;
+  const AdaptiveWs w = adaptive_ws(cfg, n_q, k_max, n_cur_pages);
+  if ((st = check_ws(ws, ws_bytes, w.total)) != HSA_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = validate_pages(cfg, pool, cur_first_page, n_cur_pages, s)) != HSA_OK) return st;
+  if ((st = validate_selection(cfg, pool, sel, k_max, s)) != HSA_OK) return st;
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  st = run_block_select(cfg, q, n_q, pool, sel, k_max, cur_first_page, n_cur_pages, tau_min,
+                        tau_max, w, base, false, BlockSelOut(), s);
+  if (st != HSA_OK) return st;
+  return run_sparse(cfg, q, n_q, pool, sel, k_max, k_h, cur_first_page, n_cur_pages, o_sp, lse,
+                    base + w.part_off, &w, s);
 }
 
 }  // extern "C"
@@ -388,7 +612,8 @@ hsa_status_t run_attend(const hsa_config_t* cfg, const void* q, int32_t n_q,
                         const hsa_kv_pool_t* pool, const int32_t* sel, int32_t k_max,
                         const int32_t* k_h, int32_t n_cand, int32_t n_cur_pages,
                         const float* kv_state, const float* k_state, const float* g_lin,
-                        const float* g_sp, void* o, void* partials, hipStream_t s) {
+                        const float* g_sp, void* o, void* partials, hipStream_t s,
+                        const AdaptiveWs* w = nullptr, uint8_t* wbase = nullptr) {
   AttnParams p{};
   p.q = q;
   p.k = pool->k;
@@ -416,6 +641,7 @@ hsa_status_t run_attend(const hsa_config_t* cfg, const void* q, int32_t n_q,
   plan_attention(p, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
                  kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16);
   if (cfg->dtype == HSA_DTYPE_BF16) set_partials(p, cfg, n_q, partials);
+  if (w) set_block_lists(p, *w, wbase);
   return from_hip(launch_attention(cfg->dtype, cfg->head_dim, cfg->batch, p, s));
 }
 
@@ -465,6 +691,33 @@ hsa_status_t hsa_forward_selected(const hsa_config_t* cfg, const void* q, int32_
   void* partials = base + select_ws_bytes(cfg, n_q) + sel_ws_bytes(cfg, k_max);
   return run_attend(cfg, q, n_q, pool, sel, k_max, k_h, n_cand, n_cur_pages, kv_state, k_state,
                     g_lin, g_sp, o, partials, s);
+}
+
+hsa_status_t hsa_forward_adaptive(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                                  const hsa_kv_pool_t* pool, int32_t n_cand,
+                                  int32_t n_cur_pages, const int32_t* k_h, int32_t k_max,
+                                  double tau_min, double tau_max, const float* kv_state,
+                                  const float* k_state, const double* page_kmean,
+                                  const float* g_lin, const float* g_sp, void* o,
+                                  int32_t* sel_out, void* ws, size_t ws_bytes, void* stream) {
+  hsa_status_t st = check_forward(cfg, q, n_q, pool, n_cand, n_cur_pages, k_h, k_max, kv_state,
+                                  k_state, o);
+  if (st != HSA_OK) return st;
+  if (!page_kmean) return HSA_ERR_INVALID_ARG;
+  if ((st = check_adaptive(cfg, n_q, k_max, n_cur_pages, tau_min, tau_max)) != HSA_OK) return st;
+  const AdaptiveWs w = adaptive_ws(cfg, n_q, k_max, n_cur_pages);
+  if ((st = check_ws(ws, ws_bytes, w.total)) != HSA_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = validate_pages(cfg, pool, 0, n_cand + n_cur_pages, s)) != HSA_OK) return st;
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  int32_t* sel = sel_out ? sel_out : reinterpret_cast<int32_t*>(base + w.sel_off);
+  st = run_select(cfg, q, n_q, page_kmean, pool->max_pages, n_cand, k_h, k_max, sel, nullptr, ws, s);
+  if (st != HSA_OK) return st;
+  st = run_block_select(cfg, q, n_q, pool, sel, k_max, n_cand, n_cur_pages, tau_min, tau_max, w,
+                        base, true, BlockSelOut(), s);
+  if (st != HSA_OK) return st;
+  return run_attend(cfg, q, n_q, pool, sel, k_max, k_h, n_cand, n_cur_pages, kv_state, k_state,
+                    g_lin, g_sp, o, base + w.part_off, s, &w, base);
 }
 
 }  // extern "C"

@@ -202,7 +202,7 @@ __device__ __forceinline__ void finish(const AttnParams& p, uint8_t* smem, int b
   }
 }
 
-template <int D, bool kSmallP>
+template <int D, bool kSmallP, bool kList>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
   using L = AttnLayout<D>;
   constexpr int KK = D / 16;   // 16-wide d slices
@@ -238,35 +238,54 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
     split = local / nqt;
     qtile = local % nqt;
   }
+  const int ns = p.sc.n_split[h];
+  const int tpp = (P + kBN - 1) / kBN;
 
-  // ---- key list: selected pages (up to the first invalid entry), then current pages
+  // ---- key walk. Page mode: the selected pages (up to the first invalid
+  // entry), then the current pages, every page in tiles of 64 keys (a tile
+  // never straddles a page; the last one is partial when 64 does not divide
+  // P). List mode: the (b, h, query tile)'s own list of tiles, each with the
+  // query blocks that attend to it.
   const int32_t* selrow = p.sel + ((size_t)b * H + h) * p.k_max;
-  int n_sel = 0;
-  while (n_sel < p.k_max) {
-    const int e = ld_const(selrow + n_sel);
-    if (e < 0 || e >= p.max_pages) break;
-    ++n_sel;
-  }
-  const int n_list = n_sel + p.n_cur;
   const int32_t* ptrow = p.page_table + (size_t)b * p.max_pages;
+  int n_sel = 0;
+  if constexpr (!kList) {
+    while (n_sel < p.k_max) {
+      const int e = ld_const(selrow + n_sel);
+      if (e < 0 || e >= p.max_pages) break;
+      ++n_sel;
+    }
+  }
   auto head_of = [&](int li) -> size_t {
     const int lp = li < n_sel ? ld_const(selrow + li) : p.cur_first + (li - n_sel);
     return (size_t)clampi(ld_const(ptrow + lp), 0, p.num_slots - 1) * H + h;
   };
-  // This item's share of the list: split `split` of n_split[h] near-equal
-  // parts of list_len[h] pages (the last split takes whatever the list holds
-  // beyond the plan).
-  const int ns = p.sc.n_split[h];
-  int pg0 = 0, pg1 = n_list;
-  if (ns > 1) {
-    const int len = p.sc.list_len[h], base = len / ns, rem = len % ns;
-    pg0 = min(n_list, split * base + min(split, rem));
-    pg1 = split == ns - 1 ? n_list : min(n_list, pg0 + base + (split < rem ? 1 : 0));
+  // This item's share of the walk: split `split` of n_split[h] near-equal
+  // parts (of list_len[h] pages, the last split taking whatever the list
+  // holds beyond the plan; of the tile list in list mode).
+  int pg0 = 0, pg1 = 0, u0 = 0, u1 = 0, ntiles;
+  const int2* lst = nullptr;
+  if constexpr (kList) {
+    const size_t cell = ((size_t)b * H + h) * nqt + qtile;
+    const int len = ld_const(p.blist_len + cell);
+    lst = p.blist + cell * p.blist_cap;
+    u1 = len;
+    if (ns > 1) {
+      const int base = len / ns, rem = len % ns;
+      u0 = split * base + min(split, rem);
+      u1 = u0 + base + (split < rem ? 1 : 0);
+    }
+    ntiles = u1 - u0;
+  } else {
+    const int n_list = n_sel + p.n_cur;
+    pg1 = n_list;
+    if (ns > 1) {
+      const int len = p.sc.list_len[h], base = len / ns, rem = len % ns;
+      pg0 = min(n_list, split * base + min(split, rem));
+      pg1 = split == ns - 1 ? n_list : min(n_list, pg0 + base + (split < rem ? 1 : 0));
+    }
+    ntiles = (pg1 - pg0) * tpp;
   }
-  // Key tiles never straddle a page: each page is walked in tiles of 64 keys,
-  // the last one partial when 64 does not divide P.
-  const int tpp = (P + kBN - 1) / kBN;
-  const int ntiles = (pg1 - pg0) * tpp;
 
   // ---- Q fragment: lane holds query (l%32) of this wave, d = 16kk + 8*half + 0..7
   const uint16_t* qb = static_cast<const uint16_t*>(p.q);
@@ -309,10 +328,13 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
   // issues and waits alike; they are drained before the epilogue.
   auto window = [&](int t) { return kSmallP ? t * kBN : min(t * kBN, P - kBN); };
   int kli = pg0, kt = 0, vli = pg0, vt = 0;
-  const char* kbase = reinterpret_cast<const char*>(kpool) + (pg0 < pg1 ? head_of(pg0) : 0) * (size_t)P * D * 2;
-  const char* vbase = reinterpret_cast<const char*>(vpool) + (pg0 < pg1 ? head_of(pg0) : 0) * (size_t)D * P * 2;
-  auto issue_k = [&](int buf) {
-    const char* src = kbase + (size_t)window(kt) * D * 2;
+  const char* kbase = nullptr;
+  const char* vbase = nullptr;
+  if constexpr (!kList) {
+    kbase = reinterpret_cast<const char*>(kpool) + (pg0 < pg1 ? head_of(pg0) : 0) * (size_t)P * D * 2;
+    vbase = reinterpret_cast<const char*>(vpool) + (pg0 < pg1 ? head_of(pg0) : 0) * (size_t)D * P * 2;
+  }
+  auto load_k = [&](int buf, const char* src) {
     uint8_t* dst = smem + buf * L::kKTile + wave * L::kInstK * 1024;
 #pragma unroll
     for (int n = 0; n < L::kInstK; ++n) {
@@ -320,6 +342,19 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
       if constexpr (kSmallP) off -= (uint32_t)(max(0, k_row(n) - (P - 1)) * D * 2);
       g2lds16(src + off, dst + n * 1024);
     }
+  };
+  auto load_v = [&](int buf, const char* src) {
+    uint8_t* dst = smem + L::kVBase + buf * L::kVTile + wave * L::kInstV * 1024;
+#pragma unroll
+    for (int n = 0; n < L::kInstV; ++n) {
+      uint32_t off = v_off[n];
+      if constexpr (kSmallP) off -= (uint32_t)(max(0, v_col(n) - (P - 8)) * 2);
+      g2lds16(src + off, dst + n * 1024);
+    }
+  };
+  // page mode: cursors (list position, tile) advance through the pages
+  auto issue_k = [&](int buf) {
+    load_k(buf, kbase + (size_t)window(kt) * D * 2);
     if (kt + 1 < tpp) {
       ++kt;
     } else if (kli + 1 < pg1) {
@@ -329,14 +364,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
     }
   };
   auto issue_v = [&](int buf) {
-    const char* src = vbase + (size_t)window(vt) * 2;
-    uint8_t* dst = smem + L::kVBase + buf * L::kVTile + wave * L::kInstV * 1024;
-#pragma unroll
-    for (int n = 0; n < L::kInstV; ++n) {
-      uint32_t off = v_off[n];
-      if constexpr (kSmallP) off -= (uint32_t)(max(0, v_col(n) - (P - 8)) * 2);
-      g2lds16(src + off, dst + n * 1024);
-    }
+    load_v(buf, vbase + (size_t)window(vt) * 2);
     if (vt + 1 < tpp) {
       ++vt;
     } else if (vli + 1 < pg1) {
@@ -344,6 +372,15 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
       ++vli;
       vbase = reinterpret_cast<const char*>(vpool) + head_of(vli) * (size_t)D * P * 2;
     }
+  };
+  // list mode: the tile of entry e; entries past the item's range repeat its
+  // last tile (loads into ring slots nobody reads, as in page mode)
+  auto entry = [&](int u) { return ld_const(lst + min(u, u1 - 1)); };
+  auto issue_k_at = [&](int buf, int2 e) {
+    load_k(buf, reinterpret_cast<const char*>(kpool) + ((size_t)e.x * P + window(e.y >> 2)) * D * 2);
+  };
+  auto issue_v_at = [&](int buf, int2 e) {
+    load_v(buf, reinterpret_cast<const char*>(vpool) + (size_t)e.x * D * P * 2 + (size_t)window(e.y >> 2) * 2);
   };
 
   f32x16 acc[NM];
@@ -353,11 +390,23 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
   const float c2 = p.scale_log2;
   const int krow = key_perm(l32);
 
-  // prologue: K(0), V(0), K(1)
+  // prologue: K(0), V(0), K(1). List mode keeps the entries of the tile
+  // being computed (ec), of the next value issue (ev) and of the next key
+  // issue (ek) in scalar registers, read one iteration ahead.
+  int2 ec = make_int2(0, 0), ev = ec, ek = ec;
   if (ntiles > 0) {
-    issue_k(0);
-    issue_v(0);
-    issue_k(1);
+    if constexpr (kList) {
+      ec = entry(u0);
+      ev = entry(u0 + 1);
+      issue_k_at(0, ec);
+      issue_v_at(0, ec);
+      issue_k_at(1, ev);
+      ek = entry(u0 + 2);
+    } else {
+      issue_k(0);
+      issue_v(0);
+      issue_k(1);
+    }
   }
   int t = 0, kbuf = 0;
   for (int tile = 0; tile < ntiles; ++tile) {
@@ -365,96 +414,114 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
     // loads are outstanding
     wait_vmcnt<L::kInstK>();
     lds_barrier();
-    issue_v((tile + 1) & 1);
-    issue_k(kbuf == 0 ? 2 : kbuf - 1);   // ring slot (tile+2) % 3
-
-    // S^T = K Q^T for the two 32-key halves of the tile: the two MFMA chains
-    // alternate, and the key fragments are read from LDS kLdsAhead MFMAs
-    // before their use (an LDS read takes several MFMA durations).
-    f32x16 s[2];
-    {
-      const uint8_t* kt_l = smem + kbuf * L::kKTile;
-      s[0] = f32x16{0};
-      s[1] = f32x16{0};
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk)
-#pragma unroll
-        for (int h2 = 0; h2 < 2; ++h2) {
-          const int row = 32 * h2 + krow;
-          const int chunk = 2 * kk + half;
-          const u32x4 a = ld_lds16(kt_l + row * L::kRowK + ((chunk ^ swz_k<D>(row)) << 4));
-          s[h2] = mfma32(a, qf[kk], s[h2]);
-        }
-      pipeline_lds_mfma<2 * KK>();
+    if constexpr (kList) {
+      issue_v_at((tile + 1) & 1, ev);
+      issue_k_at(kbuf == 0 ? 2 : kbuf - 1, ek);   // ring slot (tile+2) % 3
+    } else {
+      issue_v((tile + 1) & 1);
+      issue_k(kbuf == 0 ? 2 : kbuf - 1);
     }
-    // The last tile of a page: window rows holding keys outside the tile
-    // are masked (leading rows of the page-end window, or rows past the page
-    // for pages shorter than a tile). The empty asm keeps this a real branch:
-    // the compiler would otherwise apply the selects to every tile.
-    const int nv = min(kBN, P - t * kBN);
-    if (nv < kBN) {
-      asm volatile("" ::: "memory");
-      const int lo = kSmallP ? 0 : kBN - nv, hi = kSmallP ? nv : kBN;
+    // list mode: waves of a query block that does not keep this tile skip it
+    const int tc = kList ? (ec.y >> 2) : t;
+    const bool active = !kList || ((ec.y >> (wave >> 1)) & 1);
+    if (active) {
+      // S^T = K Q^T for the two 32-key halves of the tile: the two MFMA chains
+      // alternate, and the key fragments are read from LDS kLdsAhead MFMAs
+      // before their use (an LDS read takes several MFMA durations).
+      f32x16 s[2];
+      {
+        const uint8_t* kt_l = smem + kbuf * L::kKTile;
+        s[0] = f32x16{0};
+        s[1] = f32x16{0};
 #pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2)
+        for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+          for (int h2 = 0; h2 < 2; ++h2) {
+            const int row = 32 * h2 + krow;
+            const int chunk = 2 * kk + half;
+            const u32x4 a = ld_lds16(kt_l + row * L::kRowK + ((chunk ^ swz_k<D>(row)) << 4));
+            s[h2] = mfma32(a, qf[kk], s[h2]);
+          }
+        pipeline_lds_mfma<2 * KK>();
+      }
+      // The last tile of a page: window rows holding keys outside the tile
+      // are masked (leading rows of the page-end window, or rows past the page
+      // for pages shorter than a tile). The empty asm keeps this a real branch:
+      // the compiler would otherwise apply the selects to every tile.
+      const int nv = min(kBN, P - tc * kBN);
+      if (nv < kBN) {
+        asm volatile("" ::: "memory");
+        const int lo = kSmallP ? 0 : kBN - nv, hi = kSmallP ? nv : kBN;
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = 32 * h2 + 16 * (r >> 3) + 8 * half + (r & 7);
+            if (key < lo || key >= hi) s[h2][r] = -INFINITY;
+          }
+      }
+      // Online softmax against a reference max m_run (raw score units) that
+      // only moves when some score exceeds it by more than 8 in exp2 units:
+      // exponentials stay <= 256 and the final normalisation by the row sum
+      // is exact for any reference. The test uses each lane's own 32 scores;
+      // only when it fires are the two lane halves of a query combined.
+      float mx = fmaxf(s[0][0], s[0][1]);
+#pragma unroll
+      for (int r = 2; r < 16; ++r) mx = fmaxf(mx, s[0][r]);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[1][r]);
+      if (__any(mx * c2 > m_run * c2 + 8.f)) {
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const bool grow = mx * c2 > m_run * c2 + 8.f;
+        const float m_new = grow ? mx : m_run;
+        const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c2);
+        l_run *= alpha;
+#pragma unroll
+        for (int m = 0; m < NM; ++m) acc[m] *= alpha;
+        m_run = m_new;
+      }
+      const float mc = m_run * c2;
+      float rs = 0.f;
+      u32x4 pb[4];
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        float pv[16];
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int key = 32 * h2 + 16 * (r >> 3) + 8 * half + (r & 7);
-          if (key < lo || key >= hi) s[h2][r] = -INFINITY;
+          pv[r] = __builtin_amdgcn_exp2f(fmaf(s[h2][r], c2, -mc));
+          rs += pv[r];
         }
-    }
-    // Online softmax against a reference max m_run (raw score units) that
-    // only moves when some score exceeds it by more than 8 in exp2 units:
-    // exponentials stay <= 256 and the final normalisation by the row sum
-    // is exact for any reference. The test uses each lane's own 32 scores;
-    // only when it fires are the two lane halves of a query combined.
-    float mx = fmaxf(s[0][0], s[0][1]);
 #pragma unroll
-    for (int r = 2; r < 16; ++r) mx = fmaxf(mx, s[0][r]);
-#pragma unroll
-    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[1][r]);
-    if (__any(mx * c2 > m_run * c2 + 8.f)) {
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const bool grow = mx * c2 > m_run * c2 + 8.f;
-      const float m_new = grow ? mx : m_run;
-      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c2);
-      l_run *= alpha;
-#pragma unroll
-      for (int m = 0; m < NM; ++m) acc[m] *= alpha;
-      m_run = m_new;
-    }
-    const float mc = m_run * c2;
-    float rs = 0.f;
-    u32x4 pb[4];
-#pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2) {
-      float pv[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        pv[r] = __builtin_amdgcn_exp2f(fmaf(s[h2][r], c2, -mc));
-        rs += pv[r];
+        for (int g = 0; g < 2; ++g)
+          pb[2 * h2 + g] =
+              u32x4{pack_bf16(pv[8 * g + 0], pv[8 * g + 1]), pack_bf16(pv[8 * g + 2], pv[8 * g + 3]),
+                    pack_bf16(pv[8 * g + 4], pv[8 * g + 5]), pack_bf16(pv[8 * g + 6], pv[8 * g + 7])};
       }
+      l_run += rs;
+      // O^T += V^T P^T (NM independent chains), value fragments read ahead
+      {
+        const uint8_t* vt_l = smem + L::kVBase + (tile & 1) * L::kVTile;
 #pragma unroll
-      for (int g = 0; g < 2; ++g)
-        pb[2 * h2 + g] =
-            u32x4{pack_bf16(pv[8 * g + 0], pv[8 * g + 1]), pack_bf16(pv[8 * g + 2], pv[8 * g + 3]),
-                  pack_bf16(pv[8 * g + 4], pv[8 * g + 5]), pack_bf16(pv[8 * g + 6], pv[8 * g + 7])};
-    }
-    l_run += rs;
-    // O^T += V^T P^T (NM independent chains), value fragments read ahead
-    {
-      const uint8_t* vt_l = smem + L::kVBase + (tile & 1) * L::kVTile;
+        for (int ks = 0; ks < 4; ++ks) {
+          const int chunk = 2 * ks + half;
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const int chunk = 2 * ks + half;
-#pragma unroll
-        for (int m = 0; m < NM; ++m) {
-          const int row = 32 * m + l32;
-          const u32x4 a = ld_lds16(vt_l + row * L::kRowV + ((chunk ^ swz_v(row)) << 4));
-          acc[m] = mfma32(a, pb[ks], acc[m]);
+          for (int m = 0; m < NM; ++m) {
+            const int row = 32 * m + l32;
+            const u32x4 a = ld_lds16(vt_l + row * L::kRowV + ((chunk ^ swz_v(row)) << 4));
+            acc[m] = mfma32(a, pb[ks], acc[m]);
+          }
         }
+        pipeline_lds_mfma<4 * NM>();
       }
-      pipeline_lds_mfma<4 * NM>();
+    }
+    if constexpr (kList) {
+      // the key entry of tile + 3, read after this tile's LDS traffic so that
+      // the scalar load never shares the LDS counter with the operand reads
+      __builtin_amdgcn_sched_barrier(0);
+      const int2 en = entry(u0 + tile + 3);
+      ec = ev;
+      ev = ek;
+      ek = en;
     }
     if (++t == tpp) t = 0;
     kbuf = kbuf == 2 ? 0 : kbuf + 1;
@@ -525,7 +592,10 @@ __global__ __launch_bounds__(256, 2) void combine_bf16_kernel(AttnParams p) {
 }
 
 // fp32 inputs: VALU attention, 64 queries per workgroup, 4 lanes per query.
-template <int D>
+// Page mode walks the selected pages and then the current pages; list mode
+// walks the 64-key tiles its query block keeps (one query block per
+// workgroup: query tile qtile / 2, mask bit qtile % 2 of the tile lists).
+template <int D, bool kList>
 __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
   constexpr int T = 32, BM = 64, DP = D / 4;
   __shared__ float ks[T][D + 1];
@@ -535,19 +605,6 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
   const int tid = threadIdx.x, qr = tid >> 2, part = tid & 3;
   const int qtile = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int H = p.H, P = p.P;
-  const int32_t* selrow = p.sel + ((size_t)b * H + h) * p.k_max;
-  int n_sel = 0;
-  while (n_sel < p.k_max) {
-    const int e = selrow[n_sel];
-    if (e < 0 || e >= p.max_pages) break;
-    ++n_sel;
-  }
-  const int n_list = n_sel + p.n_cur;
-  for (int i = tid; i < n_list; i += 256) {
-    const int lp = i < n_sel ? selrow[i] : p.cur_first + (i - n_sel);
-    slots[i] = clampi(p.page_table[(size_t)b * p.max_pages + lp], 0, p.num_slots - 1);
-  }
-  const int n_kv = n_list * P;
   const float* qg = static_cast<const float*>(p.q);
   const float* kg = static_cast<const float*>(p.k);
   const float* vg = static_cast<const float*>(p.v);
@@ -557,30 +614,21 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
     const int qi = min(q0 + r, p.n_q - 1);
     qs[r][dd] = qg[(((size_t)b * p.n_q + qi) * H + h) * D + dd];
   }
-  __syncthreads();
   float acc[DP];
   for (int e = 0; e < DP; ++e) acc[e] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
-  for (int k0 = 0; k0 < n_kv; k0 += T) {
-    const int nk = min(T, n_kv - k0);
+  // keys [off0, off0 + nk) of the page at (slot * H + h) = ph, nk <= T
+  auto step = [&](size_t ph, int off0, int nk) {
     __syncthreads();
+    const float* kp = kg + ph * P * D;
+    const float* vp = vg + ph * D * P;
     for (int x = tid; x < T * D; x += 256) {
       const int key = x / D, dd = x % D;
-      float kv = 0.f;
-      if (key < nk) {
-        const int j = k0 + key, li = j / P, off = j % P;
-        kv = kg[(((size_t)slots[li] * H + h) * P + off) * D + dd];
-      }
-      ks[key][dd] = kv;
+      ks[key][dd] = key < nk ? kp[(size_t)(off0 + key) * D + dd] : 0.f;
     }
     for (int x = tid; x < T * D; x += 256) {
       const int dd = x / T, key = x % T;
-      float vv = 0.f;
-      if (key < nk) {
-        const int j = k0 + key, li = j / P, off = j % P;
-        vv = vg[(((size_t)slots[li] * H + h) * D + dd) * P + off];
-      }
-      vs[key][dd] = vv;
+      vs[key][dd] = key < nk ? vp[(size_t)dd * P + off0 + key] : 0.f;
     }
     __syncthreads();
     float sc[T];
@@ -604,7 +652,35 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
       for (int e = 0; e < DP; ++e) acc[e] = fmaf(pk, vs[key][part * DP + e], acc[e]);
     }
     m_run = m_new;
+  };
+  if constexpr (kList) {
+    const size_t cell = ((size_t)b * H + h) * p.sc.nqt + qtile / 2;
+    const int len = p.blist_len[cell], bit = qtile & 1;
+    const int2* lst = p.blist + cell * p.blist_cap;
+    for (int u = 0; u < len; ++u) {
+      const int2 e = lst[u];
+      if (!((e.y >> bit) & 1)) continue;
+      const int k0 = (e.y >> 2) * 64, k1 = min(P, k0 + 64);
+      for (int off = k0; off < k1; off += T) step((size_t)e.x, off, min(T, k1 - off));
+    }
+  } else {
+    const int32_t* selrow = p.sel + ((size_t)b * H + h) * p.k_max;
+    int n_sel = 0;
+    while (n_sel < p.k_max) {
+      const int e = selrow[n_sel];
+      if (e < 0 || e >= p.max_pages) break;
+      ++n_sel;
+    }
+    const int n_list = n_sel + p.n_cur;
+    for (int i = tid; i < n_list; i += 256) {
+      const int lp = i < n_sel ? selrow[i] : p.cur_first + (i - n_sel);
+      slots[i] = clampi(p.page_table[(size_t)b * p.max_pages + lp], 0, p.num_slots - 1);
+    }
+    __syncthreads();
+    for (int li = 0; li < n_list; ++li)
+      for (int off = 0; off < P; off += T) step((size_t)slots[li] * H + h, off, min(T, P - off));
   }
+  __syncthreads();  // the query rows are complete even if no key was visited
   const int qi = q0 + qr;
   if (qi >= p.n_q) return;
   const float inv_l = l_run > 0.f ? 1.f / l_run : 0.f;
@@ -840,13 +916,23 @@ void plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_
 hipError_t launch_attention(int dtype, int d, int B, const AttnParams& p, hipStream_t s) {
   if (dtype == HSA_DTYPE_BF16) {
     const dim3 grid(8 * std::max(1, p.sc.xcd_items), B);
-    const bool small = p.P < kBN;
+    const bool small = p.P < kBN, list = p.blist != nullptr;
     if (d == 128) {
-      if (small) attn_bf16_kernel<128, true><<<grid, 256, 0, s>>>(p);
-      else attn_bf16_kernel<128, false><<<grid, 256, 0, s>>>(p);
+      if (list) {
+        if (small) attn_bf16_kernel<128, true, true><<<grid, 256, 0, s>>>(p);
+        else attn_bf16_kernel<128, false, true><<<grid, 256, 0, s>>>(p);
+      } else {
+        if (small) attn_bf16_kernel<128, true, false><<<grid, 256, 0, s>>>(p);
+        else attn_bf16_kernel<128, false, false><<<grid, 256, 0, s>>>(p);
+      }
     } else {
-      if (small) attn_bf16_kernel<64, true><<<grid, 256, 0, s>>>(p);
-      else attn_bf16_kernel<64, false><<<grid, 256, 0, s>>>(p);
+      if (list) {
+        if (small) attn_bf16_kernel<64, true, true><<<grid, 256, 0, s>>>(p);
+        else attn_bf16_kernel<64, false, true><<<grid, 256, 0, s>>>(p);
+      } else {
+        if (small) attn_bf16_kernel<64, true, false><<<grid, 256, 0, s>>>(p);
+        else attn_bf16_kernel<64, false, false><<<grid, 256, 0, s>>>(p);
+      }
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.sc.n_chead == 0) return e;
@@ -855,8 +941,13 @@ hipError_t launch_attention(int dtype, int d, int B, const AttnParams& p, hipStr
     else combine_bf16_kernel<64><<<cgrid, 256, 0, s>>>(p);
   } else {
     const dim3 grid((p.n_q + 63) / 64, p.H, B);
-    if (d == 128) attn_f32_kernel<128><<<grid, 256, 0, s>>>(p);
-    else attn_f32_kernel<64><<<grid, 256, 0, s>>>(p);
+    if (p.blist) {
+      if (d == 128) attn_f32_kernel<128, true><<<grid, 256, 0, s>>>(p);
+      else attn_f32_kernel<64, true><<<grid, 256, 0, s>>>(p);
+    } else {
+      if (d == 128) attn_f32_kernel<128, false><<<grid, 256, 0, s>>>(p);
+      else attn_f32_kernel<64, false><<<grid, 256, 0, s>>>(p);
+    }
   }
   return hipGetLastError();
 }

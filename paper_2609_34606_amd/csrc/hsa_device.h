@@ -85,6 +85,12 @@ template <typename T>
 __device__ __forceinline__ T ld_const(const T* p) {
   return *(const __attribute__((address_space(4))) T*)(p);
 }
+// int2 through one 8-byte scalar load (the vector type has no constructor
+// from a constant-address-space lvalue)
+__device__ __forceinline__ int2 ld_const(const int2* p) {
+  const int64_t v = *(const __attribute__((address_space(4))) int64_t*)(p);
+  return make_int2((int)(uint32_t)v, (int)(uint32_t)(v >> 32));
+}
 
 __device__ __forceinline__ int clampi(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
 

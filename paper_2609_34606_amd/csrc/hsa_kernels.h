@@ -60,6 +60,54 @@ struct SelectParams {
 
 hipError_t launch_page_select(int dtype, int d, int B, const QsumParams& qp,
                               const SelectParams& sp, hipStream_t s);
+// The first stage of launch_page_select alone (fp64 column sums of the query
+// rows in splits of qp.rows_per_split).
+hipError_t launch_qsum(int dtype, int B, const QsumParams& qp, hipStream_t s);
+
+// ------------------------------------------------------------ block selection
+// Key blocks: runs of kBlockHist tokens inside each selected history page and
+// of kBlockCur tokens inside each current page (the last block of a page is
+// shorter when the block size does not divide P); query blocks: runs of
+// kBlockQ queries. Both key block sizes are multiples of the attention
+// kernels' 64-key tile, so a block is a whole number of tiles.
+constexpr int kBlockQ = 64, kBlockHist = 128, kBlockCur = 64;
+
+struct BlockSelParams {
+  const void* k;              // pool keys [num_slots, H, P, d]
+  const int32_t* page_table;  // [B, max_pages]
+  const int32_t* sel;         // [B, H, k_max] (not read when k_max == 0)
+  int32_t H, P, n_q, num_slots, max_pages, k_max, cur_first, n_cur;
+  int32_t n_qb;               // query blocks
+  int32_t n_qt;               // attention query tiles (two query blocks each)
+  int32_t n_blk_max;          // key blocks of the longest list (row length of the buffers below)
+  int32_t n_pad;              // n_blk_max rounded up to a power of two, >= 64
+  int32_t rpg;                // query blocks per pooled-rows workgroup (1..4)
+  int32_t qs_split;           // splits of ws_qs (each kBlockQ / 2 rows)
+  double scale;               // pooled-map scale
+  double tau_min, tau_max;
+  const double* ws_qs;        // [B, qs_split, H*d] query column sums
+  double* kbar_t;             // [B, H, d, n_blk_max] block mean keys, d-major
+  double* row_c;              // [B, H, n_qb, n_blk_max] cumulative weight, sorted order
+  int32_t* row_i;             // [B, H, n_qb, n_blk_max] block id, sorted order
+  double* row_g;              // [B, H, n_qb] Gini term of each query block
+  int2* blist;                // [B, H, n_qt, blist_cap] tile lists
+  int32_t* blist_len;         // [B, H, n_qt]
+  int32_t blist_cap;
+  // optional outputs (NULL: not written)
+  double* gini;               // [B, H]
+  double* tau;                // [B, H]
+  int32_t* n_kept;            // [B, H, n_qb]
+  int32_t* kept;              // [B, H, n_qb, kept_len]
+  int32_t kept_len;
+  double* pooled;             // [B, H, n_qb, kept_len]
+};
+
+// Block means, pooled map, per-row order, Gini terms and cumulative weights,
+// then the per-head threshold, the kept prefixes and the tile lists of the
+// attention kernel. ws_qs must already hold the query column sums.
+hipError_t launch_block_select(int dtype, int d, int B, const BlockSelParams& p, hipStream_t s);
+// LDS bytes of one pooled-rows workgroup (at most 64 KB is allowed).
+size_t block_rows_lds_bytes(int d, int n_pad, int rpg);
 
 // ------------------------------------------------------------ attention
 enum AttnMode : int32_t {
@@ -114,6 +162,12 @@ struct AttnParams {
   float* lse;               // [B, H, n_q] nullable
   float* part_o;                         // [B, n_part, nqt, 4 waves, 16*d/32 regs, 64 lanes]
   float* part_lse;                       // [B, n_part, nqt, 4 waves, 64 lanes]
+  // block-sparse mode (blist != NULL): each (b, h, query tile) walks its own
+  // list of 64-key tiles, entry {slot * H + h, (tile index << 2) | mask}; mask
+  // bit w covers query block 2 * qtile + w (waves 2w, 2w + 1)
+  const int2* blist;                     // [B, H, nqt, blist_cap]
+  const int32_t* blist_len;              // [B, H, nqt]
+  int32_t blist_cap;
   AttnSchedule sc;                       // work schedule of the bf16 kernels
 };
 

@@ -217,12 +217,16 @@ __global__ __launch_bounds__(256) void select_kernel(SelectParams p) {
 
 }  // namespace
 
-hipError_t launch_page_select(int dtype, int d, int B, const QsumParams& qp,
-                              const SelectParams& sp, hipStream_t s) {
+hipError_t launch_qsum(int dtype, int B, const QsumParams& qp, hipStream_t s) {
   const dim3 g1(qp.n_split, B);
   if (dtype == HSA_DTYPE_BF16) qsum_kernel<uint16_t><<<g1, 256, 0, s>>>(qp);
   else qsum_kernel<float><<<g1, 256, 0, s>>>(qp);
-  hipError_t e = hipGetLastError();
+  return hipGetLastError();
+}
+
+hipError_t launch_page_select(int dtype, int d, int B, const QsumParams& qp,
+                              const SelectParams& sp, hipStream_t s) {
+  hipError_t e = launch_qsum(dtype, B, qp, s);
   if (e != hipSuccess) return e;
   const dim3 g2(B * sp.H);
   if (d == 128) select_kernel<128><<<g2, 256, 0, s>>>(sp);

@@ -60,10 +60,26 @@ def lib():
     for n, extra in (("hsa_state_update_workspace_size", [c_i32]),
                      ("hsa_page_select_workspace_size", [c_i32]),
                      ("hsa_sparse_attn_workspace_size", [c_i32, c_i32, c_i32]),
-                     ("hsa_forward_workspace_size", [c_i32, c_i32, c_i32])):
+                     ("hsa_forward_workspace_size", [c_i32, c_i32, c_i32]),
+                     ("hsa_adaptive_workspace_size", [c_i32, c_i32, c_i32])):
         f = getattr(L, n)
         f.restype = c_sz
         f.argtypes = [P(HsaConfig)] + extra
+    L.hsa_block_count.restype = c_i32
+    L.hsa_block_count.argtypes = [P(HsaConfig), c_i32, c_i32]
+    c_f64 = ctypes.c_double
+    L.hsa_block_select.restype = ctypes.c_int
+    L.hsa_block_select.argtypes = [P(HsaConfig), c_vp, c_i32, P(HsaKvPool), c_vp, c_i32, c_i32,
+                                   c_i32, c_f64, c_f64, c_vp, c_vp, c_vp, c_vp, c_vp, c_i32, c_vp,
+                                   c_sz, c_vp]
+    L.hsa_sparse_attn_adaptive.restype = ctypes.c_int
+    L.hsa_sparse_attn_adaptive.argtypes = [P(HsaConfig), c_vp, c_i32, P(HsaKvPool), c_vp, c_i32,
+                                           c_vp, c_i32, c_i32, c_f64, c_f64, c_vp, c_vp, c_vp,
+                                           c_sz, c_vp]
+    L.hsa_forward_adaptive.restype = ctypes.c_int
+    L.hsa_forward_adaptive.argtypes = [P(HsaConfig), c_vp, c_i32, P(HsaKvPool), c_i32, c_i32, c_vp,
+                                       c_i32, c_f64, c_f64, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
+                                       c_vp, c_vp, c_sz, c_vp]
     L.hsa_state_update.restype = ctypes.c_int
     L.hsa_state_update.argtypes = [P(HsaConfig), P(HsaKvPool), c_i32, c_i32, c_vp, c_vp, c_vp,
                                    c_vp, c_sz, c_vp]
@@ -149,6 +165,14 @@ def hsa_forward_workspace_size(cfg: HsaConfig, n_q: int, k_max: int, n_cur_pages
     return lib().hsa_forward_workspace_size(ctypes.byref(cfg), n_q, k_max, n_cur_pages)
 
 
+def hsa_adaptive_workspace_size(cfg: HsaConfig, n_q: int, k_max: int, n_cur_pages: int) -> int:
+    return lib().hsa_adaptive_workspace_size(ctypes.byref(cfg), n_q, k_max, n_cur_pages)
+
+
+def hsa_block_count(cfg: HsaConfig, n_hist_pages: int, n_cur_pages: int) -> int:
+    return lib().hsa_block_count(ctypes.byref(cfg), n_hist_pages, n_cur_pages)
+
+
 def hsa_status_string(status: int) -> str:
     return lib().hsa_status_string(status).decode()
 
@@ -217,4 +241,56 @@ def hsa_forward_selected(cfg, q, n_q, pool, sel, k_max, k_h, n_cand, n_cur_pages
                                     0 if ws is None else ws.numel(), _stream(stream))
     if check:
         _check("hsa_forward_selected", st)
+    return st
+
+
+# Paper's setting of the coverage thresholds (tau_max, tau_min) = (1.00, 0.35).
+TAU_MIN, TAU_MAX = 0.35, 1.00
+
+
+def hsa_block_select(cfg, q, n_q, pool, sel, k_max, cur_first_page, n_cur_pages,
+                     tau_min=TAU_MIN, tau_max=TAU_MAX, gini=None, tau=None, n_kept=None,
+                     kept=None, pooled=None, kept_len=0, ws=None, stream=None,
+                     check=True) -> int:
+    if ws is None:
+        ws = _workspace(hsa_adaptive_workspace_size(cfg, n_q, k_max, n_cur_pages), q.device)
+    st = lib().hsa_block_select(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool), _ptr(sel),
+                                k_max, cur_first_page, n_cur_pages, float(tau_min),
+                                float(tau_max), _ptr(gini), _ptr(tau), _ptr(n_kept), _ptr(kept),
+                                _ptr(pooled), kept_len, _ptr(ws),
+                                0 if ws is None else ws.numel(), _stream(stream))
+    if check:
+        _check("hsa_block_select", st)
+    return st
+
+
+def hsa_sparse_attn_adaptive(cfg, q, n_q, pool, sel, k_max, k_h, cur_first_page, n_cur_pages,
+                             o_sp, lse=None, tau_min=TAU_MIN, tau_max=TAU_MAX, ws=None,
+                             stream=None, check=True) -> int:
+    if ws is None:
+        ws = _workspace(hsa_adaptive_workspace_size(cfg, n_q, k_max, n_cur_pages), q.device)
+    _keep, kp = _budgets(k_h)
+    st = lib().hsa_sparse_attn_adaptive(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool),
+                                        _ptr(sel), k_max, kp, cur_first_page, n_cur_pages,
+                                        float(tau_min), float(tau_max), _ptr(o_sp), _ptr(lse),
+                                        _ptr(ws), 0 if ws is None else ws.numel(),
+                                        _stream(stream))
+    if check:
+        _check("hsa_sparse_attn_adaptive", st)
+    return st
+
+
+def hsa_forward_adaptive(cfg, q, n_q, pool, n_cand, n_cur_pages, k_h, k_max, kv_state, k_state,
+                         page_kmean, g_lin, g_sp, o, tau_min=TAU_MIN, tau_max=TAU_MAX,
+                         sel_out=None, ws=None, stream=None, check=True) -> int:
+    if ws is None:
+        ws = _workspace(hsa_adaptive_workspace_size(cfg, n_q, k_max, n_cur_pages), q.device)
+    _keep, kp = _budgets(k_h)
+    st = lib().hsa_forward_adaptive(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool), n_cand,
+                                    n_cur_pages, kp, k_max, float(tau_min), float(tau_max),
+                                    _ptr(kv_state), _ptr(k_state), _ptr(page_kmean), _ptr(g_lin),
+                                    _ptr(g_sp), _ptr(o), _ptr(sel_out), _ptr(ws),
+                                    0 if ws is None else ws.numel(), _stream(stream))
+    if check:
+        _check("hsa_forward_adaptive", st)
     return st

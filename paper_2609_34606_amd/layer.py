@@ -81,3 +81,19 @@ class HsaLayer:
         _h.hsa_forward_selected(self.cfg, q, n_q, self.pool, sel, k_max, k_h, n_cand, n_cur,
                                 self.kv_state, self.k_state, g_lin, g_sp, out, ws=ws, stream=stream)
         return out
+
+    def forward_adaptive(self, q, n_cand: int, n_cur: int, k_h: Sequence[int],
+                         k_max: Optional[int] = None, tau_min: float = _h.TAU_MIN,
+                         tau_max: float = _h.TAU_MAX, g_lin=None, g_sp=None, out=None,
+                         sel_out=None, stream=None):
+        """The forward pass with the head-adaptive block-sparse sparse branch."""
+        B, n_q = q.shape[0], q.shape[1]
+        k_max = max(1, max(k_h)) if k_max is None else k_max
+        if out is None:
+            out = self.torch.empty_like(q)
+        ws = self.workspace("fwd_adaptive", _h.hsa_adaptive_workspace_size(self.cfg, n_q, k_max, n_cur))
+        _h.hsa_forward_adaptive(self.cfg, q, n_q, self.pool, n_cand, n_cur, k_h, k_max,
+                                self.kv_state, self.k_state, self.page_kmean, g_lin, g_sp, out,
+                                tau_min=tau_min, tau_max=tau_max, sel_out=sel_out, ws=ws,
+                                stream=stream)
+        return out

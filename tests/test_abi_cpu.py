@@ -96,3 +96,37 @@ def test_validation_errors_without_launch():
     # negative scale
     neg = P.config(1, 2, 64, 256, "f32", sm_scale=-1.0)
     assert lib.hsa_state_update(by(neg), by(pool), 0, 1, fake, fake, fake, None, 0, None) == 1
+
+
+def test_adaptive_entry_points_validate_before_launch():
+    import numpy as np
+    lib = P.lib()
+    by = ctypes.byref
+    fake = ctypes.c_void_p(0x4000)
+    cfg = P.config(1, 2, 128, 1560, "bf16")
+    pool = _pool(64, 64)
+    # block counts: 13 blocks of <= 128 per history page, 25 of <= 64 per current page
+    assert P.hsa_block_count(cfg, 4, 3) == 4 * 13 + 3 * 25
+    assert P.hsa_block_count(cfg, -1, 3) == -1
+    ws = P.hsa_adaptive_workspace_size(cfg, 4680, 16, 3)
+    assert ws > P.hsa_sparse_attn_workspace_size(cfg, 4680, 16, 3) and ws % 256 == 0
+    kh = np.array([4, 4], np.int32)
+    khp = kh.ctypes.data_as(ctypes.c_void_p)
+    big = 1 << 30
+    # thresholds outside 0 <= tau_min <= tau_max <= 1
+    for tmin, tmax in ((-0.1, 1.0), (0.5, 0.4), (0.3, 1.5), (float("nan"), 1.0)):
+        assert lib.hsa_sparse_attn_adaptive(by(cfg), fake, 64, by(pool), fake, 4, khp, 10, 3,
+                                            tmin, tmax, fake, None, fake, big, None) == 1
+        assert lib.hsa_forward_adaptive(by(cfg), fake, 64, by(pool), 10, 3, khp, 4, tmin, tmax,
+                                        fake, fake, fake, None, None, fake, None, fake, big,
+                                        None) == 1
+    # kept rows shorter than the block count
+    assert lib.hsa_block_select(by(cfg), fake, 64, by(pool), fake, 4, 10, 3, 0.35, 1.0, None, None,
+                                None, fake, None, 4 * 13 + 3 * 25 - 1, fake, big, None) == 1
+    # more key blocks than a head's list may hold
+    long_pool = _pool(4, 1000)
+    assert lib.hsa_sparse_attn_adaptive(by(cfg), fake, 64, by(long_pool), fake, 320, None, 0, 3,
+                                        0.35, 1.0, fake, None, fake, big, None) == 2
+    # workspace too small
+    assert lib.hsa_sparse_attn_adaptive(by(cfg), fake, 64, by(pool), fake, 4, khp, 10, 3, 0.35,
+                                        1.0, fake, None, fake, 1024, None) == 4

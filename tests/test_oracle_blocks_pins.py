@@ -175,3 +175,24 @@ def test_forward_adaptive_full_coverage_matches_hsa_forward():
     b = O.hsa_forward(q, kp, vp, pt, n_cand, n_cur, [2, 3])
     np.testing.assert_array_equal(a["sel"], b["sel"])
     np.testing.assert_allclose(a["O"], b["O"], rtol=1e-10, atol=1e-12)
+
+
+def test_equal_key_blocks_get_equal_weights_and_tie_to_lower_id():
+    rng = np.random.default_rng(21)
+    qb = rng.standard_normal((3, 32))
+    kb = rng.standard_normal((40, 32))
+    kb[[5, 17, 33]] = kb[29]
+    pm = BO.pooled_map(qb, kb, 0.2)
+    assert (pm[:, 5] == pm[:, 29]).all() and (pm[:, 17] == pm[:, 33]).all()
+    for row in pm:
+        order = list(BO.block_order(row))
+        pos = [order.index(j) for j in (5, 17, 29, 33)]
+        assert pos == sorted(pos) and pos[-1] - pos[0] == 3
+
+
+def test_threshold_one_keeps_every_block_even_if_the_sum_rounds_early():
+    # weights whose running sum reaches 1.0 in fp64 before the last block
+    p = np.array([0.5, 0.5 - 2.0 ** -54, 2.0 ** -54, 1e-300])
+    assert np.cumsum(p)[1] == 1.0 or np.cumsum(p)[2] == 1.0
+    assert len(BO.select_blocks(p, 1.0)) == 4
+    assert len(BO.select_blocks(p, 0.75)) == 2
