@@ -71,9 +71,11 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per attention launch from the committed counter summary of
-    this workload, if it was taken on the current kernel sources, else None."""
+def measured_traffic(workload: str, key: str = "hbm_bytes_per_launch"):
+    """HBM bytes per attention launch (page-level kernel; key
+    hbm_bytes_per_launch_tile_list: the block-sparse one) from the committed
+    counter summary of this workload, if it was taken on the current kernel
+    sources, else None."""
     path = os.path.join(ROOT, "profiles", f"attn_{workload}_hbm_traffic.txt")
     if not os.path.exists(path):
         return None
@@ -86,7 +88,7 @@ def measured_traffic(workload: str):
     if kv.get("kernel_source_sha256_16") != kernel_source_hash():
         return None
     try:
-        return int(float(kv["hbm_bytes_per_launch"]))
+        return int(float(kv[key])) or None
     except (KeyError, ValueError):
         return None
 
@@ -181,11 +183,112 @@ def bench_single(args, wl):
                      "kernel": "attn_bf16_kernel (hsa_forward_selected launch)",
                      "flops_per_launch": fa},
     }
+    if not args.no_adaptive:
+        res["adaptive"] = bench_adaptive(args, wl, layer, q, k_h, k_max, sel)
     if not args.no_cpu_baseline:
         heads = list(range(wl.heads)) if wl.heads * wl.n_pages <= 12 * 24 else [0, 1]
         log("timing the oracle on the host ...")
         res["cpu_baseline"] = cpu_baseline(wl, dev, k_h, heads)
     return res
+
+
+def kept_work(wl, sel_row, kept, n_kept, n_q):
+    """Algorithmic attention flops of one head's kept blocks, and the 64-key
+    tiles its 128-query tiles walk (union of the kept sets of their two query
+    blocks) against the tiles all query blocks of the tile keep."""
+    import numpy as np
+    P, d = wl.page_size, wl.head_dim
+    n_sel = int((sel_row >= 0).sum())
+    nbh, nbc = -(-P // 128), -(-P // 64)
+
+    def keys_tiles(j):
+        if j < n_sel * nbh:
+            k0 = (j % nbh) * 128
+            nk = min(128, P - k0)
+        else:
+            k0 = ((j - n_sel * nbh) % nbc) * 64
+            nk = min(64, P - k0)
+        return nk, -(-nk // 64)
+
+    flops, walked, kept_tiles = 0.0, 0, 0
+    n_qb = len(n_kept)
+    for i in range(n_qb):
+        rows = min(64, n_q - 64 * i)
+        for j in kept[i, :n_kept[i]]:
+            nk, nt = keys_tiles(int(j))
+            flops += 4.0 * rows * nk * d
+            kept_tiles += nt
+    for t in range(-(-n_qb // 2)):
+        u = set(kept[2 * t, :n_kept[2 * t]].tolist())
+        if 2 * t + 1 < n_qb:
+            u |= set(kept[2 * t + 1, :n_kept[2 * t + 1]].tolist())
+        walked += 2 * sum(keys_tiles(j)[1] for j in u)   # two query blocks per walk
+    return flops, walked, kept_tiles
+
+
+def bench_adaptive(args, wl, layer, q, k_h, k_max, sel):
+    """The head-adaptive block-sparse path on the same layer and chunk: step
+    (cold fold + hsa_forward_adaptive), the block selection alone, and the
+    sparse branch alone; its attention launch is the sparse-branch call minus
+    the selection it runs first."""
+    import numpy as np
+    import torch
+    from paper_2609_34606_amd import (TAU_MAX, TAU_MIN, hsa_adaptive_workspace_size,
+                                      hsa_block_count, hsa_block_select, hsa_sparse_attn_adaptive)
+    n_q, n_pages = wl.n_q, wl.n_pages
+    out = torch.empty_like(q)
+
+    def step():
+        layer.fold(0, n_pages)
+        layer.forward_adaptive(q, wl.n_cand, wl.n_cur, k_h, k_max=k_max, out=out)
+
+    for _ in range(args.warmup):
+        step()
+    ms = time_loop(step, args.steps, torch)
+    ms_fwd = time_loop(lambda: layer.forward_adaptive(q, wl.n_cand, wl.n_cur, k_h, k_max=k_max,
+                                                      out=out, sel_out=sel), args.steps, torch)
+    ws = layer.workspace("adaptive_parts", hsa_adaptive_workspace_size(layer.cfg, n_q, k_max,
+                                                                       wl.n_cur))
+    ms_bsel = time_loop(lambda: hsa_block_select(layer.cfg, q, n_q, layer.pool, sel, k_max,
+                                                 wl.n_cand, wl.n_cur, ws=ws), args.steps, torch)
+    o_sp = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    ms_sp = time_loop(lambda: hsa_sparse_attn_adaptive(layer.cfg, q, n_q, layer.pool, sel, k_max,
+                                                       k_h, wl.n_cand, wl.n_cur, o_sp, ws=ws),
+                      args.steps, torch)
+    # kept sets of this chunk (untimed) for the algorithmic flops
+    n_qb = -(-n_q // 64)
+    nb = hsa_block_count(layer.cfg, k_max, wl.n_cur)
+    n_kept = torch.zeros((wl.batch, wl.heads, n_qb), dtype=torch.int32, device=q.device)
+    kept = torch.zeros((wl.batch, wl.heads, n_qb, nb), dtype=torch.int32, device=q.device)
+    gini = torch.zeros((wl.batch, wl.heads), dtype=torch.float64, device=q.device)
+    hsa_block_select(layer.cfg, q, n_q, layer.pool, sel, k_max, wl.n_cand, wl.n_cur, gini=gini,
+                     n_kept=n_kept, kept=kept, kept_len=nb, ws=ws)
+    torch.cuda.synchronize()
+    sel_h, nk_h, kp_h = sel.cpu().numpy(), n_kept.cpu().numpy(), kept.cpu().numpy()
+    fa, walked, kept_tiles, frac = 0.0, 0, 0, []
+    for b in range(wl.batch):
+        for h in range(wl.heads):
+            f, w_, k_ = kept_work(wl, sel_h[b, h], kp_h[b, h], nk_h[b, h], n_q)
+            fa, walked, kept_tiles = fa + f, walked + w_, kept_tiles + k_
+            n_blk = hsa_block_count(layer.cfg, int((sel_h[b, h] >= 0).sum()), wl.n_cur)
+            frac.append(float(nk_h[b, h].mean()) / n_blk)
+    ms_attn = ms_sp - ms_bsel
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
+    achieved = fa / (ms_attn * 1e-3) / 1e12
+    return {
+        "tau_min": TAU_MIN, "tau_max": TAU_MAX, "ms_per_step": round(ms, 4),
+        "phases_ms": {"forward_adaptive": round(ms_fwd, 4), "block_select": round(ms_bsel, 4),
+                      "sparse_attn_adaptive": round(ms_sp, 4),
+                      "attention_launch": round(ms_attn, 4)},
+        "kept_block_fraction": round(float(np.mean(frac)), 4),
+        "gini_mean": round(float(gini.cpu().numpy().mean()), 5),
+        "walked_over_kept_tiles": round(walked / max(1, kept_tiles), 3),
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4),
+                     "traffic": measured_traffic(wl.name, "hbm_bytes_per_launch_tile_list"),
+                     "kernel": "attn_bf16_kernel, tile-list mode (sparse-branch launch)",
+                     "flops_per_launch": fa},
+    }
 
 
 def bench_streaming(args, wl):
@@ -288,6 +391,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="c2", help="c1..c5")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-adaptive", action="store_true",
+                    help="skip the head-adaptive block-sparse measurement")
     ap.add_argument("--layers", type=int, default=0, help="c5 only: override the layer count")
     ap.add_argument("--chunks", type=int, default=0, help="c5 only: override the chunk count")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",

@@ -161,6 +161,50 @@ __global__ __launch_bounds__(256) void block_kmean_kernel(BlockSelParams p) {
   }
 }
 
+// One wave sorts n_pad (weight, id) pairs in LDS into the order (weight
+// descending, id ascending) with a bitonic network. In each stage a lane
+// handles pairs lane + 64c; all of its pairs are read before any is written,
+// so the reads of a stage are in flight together (reads after a write to the
+// same array would otherwise wait for it). PPL bounds the pairs per lane and
+// stage held in registers at once.
+template <int PPL>
+__device__ void bitonic_sort_wave(double* rp, int32_t* ri, int n_pad, int lane) {
+  const int half = n_pad >> 1;
+  for (int k = 2; k <= n_pad; k <<= 1) {
+    for (int jj = k >> 1; jj > 0; jj >>= 1) {
+      for (int x0 = 0; x0 < half; x0 += 64 * PPL) {
+        double pa[PPL], pb[PPL];
+        int ia[PPL], ib[PPL], ii[PPL];
+#pragma unroll
+        for (int c = 0; c < PPL; ++c) {
+          const int x = x0 + lane + 64 * c;
+          ii[c] = ((x & ~(jj - 1)) << 1) | (x & (jj - 1));
+          if (x < half) {
+            pa[c] = rp[ii[c]];
+            pb[c] = rp[ii[c] + jj];
+            ia[c] = ri[ii[c]];
+            ib[c] = ri[ii[c] + jj];
+          }
+        }
+#pragma unroll
+        for (int c = 0; c < PPL; ++c) {
+          const int x = x0 + lane + 64 * c;
+          if (x < half) {
+            const bool a_first = pa[c] > pb[c] || (pa[c] == pb[c] && ia[c] < ib[c]);
+            if (a_first != ((ii[c] & k) == 0)) {
+              rp[ii[c]] = pb[c];
+              rp[ii[c] + jj] = pa[c];
+              ri[ii[c]] = ib[c];
+              ri[ii[c] + jj] = ia[c];
+            }
+          }
+        }
+      }
+      wave_sync();
+    }
+  }
+}
+
 // ---------------------------------------------------------------- 2. pooled rows
 // p.rpg query blocks per workgroup (1..4, one per wave; fewer for long lists
 // so that the rows fit in LDS).
@@ -201,6 +245,7 @@ __global__ __launch_bounds__(256) void pooled_rows_kernel(BlockSelParams p) {
   for (int i = 0; i < 4; ++i) qi[i] = (i < rpg ? i : 0) * D;
   for (int j = tid; j < N; j += 256) {
     double a[4] = {0, 0, 0, 0};
+#pragma unroll 16
     for (int dd = 0; dd < D; ++dd) {
       const double kv = kb[(size_t)dd * p.n_blk_max + j];
 #pragma unroll
@@ -247,25 +292,11 @@ __global__ __launch_bounds__(256) void pooled_rows_kernel(BlockSelParams p) {
   if (p.pooled)
     for (int j = lane; j < p.kept_len; j += 64) p.pooled[row * p.kept_len + j] = j < N ? rp[j] : 0.0;
   wave_sync();
-  // bitonic sort, final order: weight descending, block id ascending
-  for (int k = 2; k <= p.n_pad; k <<= 1) {
-    for (int jj = k >> 1; jj > 0; jj >>= 1) {
-      for (int x = lane; x < p.n_pad / 2; x += 64) {
-        const int i = ((x & ~(jj - 1)) << 1) | (x & (jj - 1));
-        const int l = i + jj;
-        const double pa = rp[i], pb = rp[l];
-        const int ia = ri[i], ib = ri[l];
-        const bool a_first = pa > pb || (pa == pb && ia < ib);
-        if (a_first != ((i & k) == 0)) {
-          rp[i] = pb;
-          rp[l] = pa;
-          ri[i] = ib;
-          ri[l] = ia;
-        }
-      }
-      wave_sync();
-    }
-  }
+  // sort: weight descending, block id ascending
+  if (p.n_pad <= 128) bitonic_sort_wave<1>(rp, ri, p.n_pad, lane);
+  else if (p.n_pad == 256) bitonic_sort_wave<2>(rp, ri, p.n_pad, lane);
+  else if (p.n_pad == 512) bitonic_sort_wave<4>(rp, ri, p.n_pad, lane);
+  else bitonic_sort_wave<8>(rp, ri, p.n_pad, lane);
   // Gini term: (1/N) sum over sorted positions m = pos + 1 of (N - 2m + 1) p
   double gs = 0.0;
   for (int pos = lane; pos < N; pos += 64) gs += ((double)(N - 2 * pos - 1) / (double)N) * rp[pos];
