@@ -12,5 +12,6 @@ from .gen import (  # noqa: F401
     f32_to_bf16_bits,
     make_case,
     make_case_torch,
+    make_projections,
     seed_int,
 )

@@ -22,7 +22,7 @@ import numpy as np
 from .configs import Workload
 
 # tensor ids inside a (seed, layer, chunk) stream family
-T_Q, T_K, T_V, T_PERM, T_GLIN, T_GSP, T_CENTROIDS, T_ASSIGN = range(8)
+T_Q, T_K, T_V, T_PERM, T_GLIN, T_GSP, T_CENTROIDS, T_ASSIGN, T_EK, T_EV = range(10)
 
 
 def _ss(wl: Workload, layer: int, chunk: int, tid: int) -> np.random.SeedSequence:
@@ -199,3 +199,35 @@ def make_case_torch(wl: Workload, device, layer: int = 0, chunk: int = 0,
         out["g_lin"] = torch.randn((B, nq, H), generator=gen(T_GLIN), device=device)
         out["g_sp"] = torch.randn((B, nq, H), generator=gen(T_GSP), device=device)
     return out
+
+
+def make_projections(wl: Workload, rank: int, kind: str = "gaussian", layer: int = 0):
+    """Compression weights of a Linformer-style linear branch, per head, in
+    the layout the library reads: e[h][j][t] for rank j and token t of a
+    page ([H, rank, P], the transpose of an L x r projection with L = P).
+
+    The trained weights are not available, so they are drawn:
+      * "gaussian": N(0, 1/P) entries, so that a compressed token of unit
+        variance inputs has unit variance;
+      * "meanpool": row j holds 1/n on its own run of n = P / rank
+        consecutive tokens (P a multiple of rank) and 0 elsewhere.
+    Returns (e_k, e_v) as float32 arrays holding workload-dtype values.
+    """
+    H, P = wl.heads, wl.page_size
+    if kind == "gaussian":
+        s = np.float32(1.0 / np.sqrt(P))
+        e_k = np.random.default_rng(_ss(wl, layer, 0, T_EK)).standard_normal(
+            (H, rank, P), dtype=np.float32) * s
+        e_v = np.random.default_rng(_ss(wl, layer, 0, T_EV)).standard_normal(
+            (H, rank, P), dtype=np.float32) * s
+    elif kind == "meanpool":
+        if P % rank:
+            raise ValueError("meanpool needs P to be a multiple of rank")
+        n = P // rank
+        e_k = np.zeros((H, rank, P), np.float32)
+        for j in range(rank):
+            e_k[:, j, j * n:(j + 1) * n] = np.float32(1.0 / n)
+        e_v = e_k.copy()
+    else:
+        raise ValueError(kind)
+    return _round(wl, e_k), _round(wl, e_v)
