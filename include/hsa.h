@@ -306,6 +306,61 @@ hsa_status_t hsa_forward_adaptive(const hsa_config_t* cfg, const void* q, int32_
                                   const float* g_lin, const float* g_sp, void* o,
                                   int32_t* sel_out, void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * Linformer linear branch (Sec. 3.3 "Linear branch"; App. "Linear Branch"):
+ * per head h, projections E_K^(h), E_V^(h) in R^{L x r} compress keys and
+ * values along the sequence. The sequence is cut into segments of length L
+ * that are projected independently and concatenated; here a segment is one
+ * page (L = P), so each page is compressed once, when it is written.
+ */
+
+/* Workspace of hsa_linformer_compress (0 when none is needed). */
+size_t hsa_linformer_compress_workspace_size(const hsa_config_t* cfg, int32_t rank,
+                                             int32_t n_pages);
+
+/*
+ * hsa_linformer_compress -- for logical pages p in [first_page, first_page +
+ * n_pages) of every batch entry and every head h, with slot = page_table[b][p]:
+ *   ck[slot][h] = E_K^(h)T K[slot][h]              (rank x d)
+ *   cv[slot][h] = (E_V^(h)T V[slot][h])^T           (d x rank, d-major like pool.v)
+ * e_k, e_v: device [H, rank, P] in cfg->dtype, e_k[h][j][t] = E_K^(h)[t][j].
+ * ck: device [num_slots, H, rank, d], cv: device [num_slots, H, d, rank], in
+ * cfg->dtype (bf16: fp32 accumulation, rounded once). rank in {32, 64, 128}
+ * (UNSUPPORTED otherwise). The compressed pages are themselves a KV pool of
+ * page size rank over the same page table: hsa_sparse_attn on it (cfg with
+ * page_size = rank, pool {ck, cv, page_table}) is the Linformer branch over
+ * the listed pages. Errors as hsa_state_update. ws:
+ * hsa_linformer_compress_workspace_size(cfg, rank, n_pages) bytes.
+ */
+hsa_status_t hsa_linformer_compress(const hsa_config_t* cfg, const hsa_kv_pool_t* pool,
+                                    const void* e_k, const void* e_v, int32_t rank,
+                                    int32_t first_page, int32_t n_pages, void* ck, void* cv,
+                                    void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace of hsa_forward_linformer. */
+size_t hsa_linformer_workspace_size(const hsa_config_t* cfg, int32_t n_q, int32_t k_max,
+                                    int32_t n_cur_pages);
+
+/*
+ * hsa_forward_linformer -- the HSA forward pass with the paper's two
+ * branches: page selection as hsa_forward, the head-adaptive block-sparse
+ * sparse branch as hsa_forward_adaptive, and the Linformer linear branch over
+ * the compressed versions of the same pages (selected, then current):
+ *   O_lin = softmax(scale * Q [ck_p1; ck_p2; ...]^T) [cv_p1^T; cv_p2^T; ...],
+ *   o = sigmoid(g_lin) O_lin + sigmoid(g_sp) O_sp   (Sec. 3.3 "Gated fusion").
+ * ck, cv: the compressed pool of hsa_linformer_compress, which must cover
+ * pages [0, n_cand + n_cur_pages); rank as there. Other arguments and errors
+ * as hsa_forward_adaptive (no linear state is read). ws:
+ * hsa_linformer_workspace_size(cfg, n_q, k_max, n_cur_pages) bytes.
+ */
+hsa_status_t hsa_forward_linformer(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                                   const hsa_kv_pool_t* pool, const void* ck, const void* cv,
+                                   int32_t rank, int32_t n_cand, int32_t n_cur_pages,
+                                   const int32_t* k_h, int32_t k_max, double tau_min,
+                                   double tau_max, const double* page_kmean, const float* g_lin,
+                                   const float* g_sp, void* o, int32_t* sel_out, void* ws,
+                                   size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -168,13 +168,16 @@ def hsa_forward_adaptive(q, k_pool, v_pool, page_table, n_cand: int, n_cur: int,
                          g_lin=None, g_sp=None, sm_scale: Optional[float] = None,
                          heads: Optional[Sequence[int]] = None,
                          query_blocks: Optional[Sequence[int]] = None,
-                         state_pages: Optional[Sequence[int]] = None) -> Dict[str, object]:
+                         state_pages: Optional[Sequence[int]] = None,
+                         linear: bool = True) -> Dict[str, object]:
     """HSA forward with the head-adaptive block-sparse sparse branch.
 
     Steps 1-4 (page index, chunk summary, top-k_h pages, page list) and the
     linear branch are those of ``hsa_oracle.hsa_forward``; the sparse branch
     attends, for each query block, to its kept key blocks only. Output rows
-    are those of ``query_blocks`` (all query blocks by default).
+    are those of ``query_blocks`` (all query blocks by default). With
+    ``linear=False`` the kernelised linear branch and the merge are skipped
+    ("O" stays zero) for callers that bring their own linear branch.
     """
     q = np.asarray(q)
     B, n_q, H, d = q.shape
@@ -207,6 +210,8 @@ def hsa_forward_adaptive(q, k_pool, v_pool, page_table, n_cand: int, n_cur: int,
             out["pooled"][(b, h)] = r["pooled"]
             out["O_sp"][b, :, h] = r["O_sp"]
             out["lse"][b, h] = r["lse"]
+            if not linear:
+                continue
             kl, vl = O.gather_pages(k_pool, v_pool, page_table, b, h, state_pages)
             S, z = O.linear_state(kl, vl)
             o_lin = O.linear_branch(np.asarray(q[b, rows, h], np.float64), S, z)

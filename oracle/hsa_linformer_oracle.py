@@ -71,7 +71,8 @@ def hsa_forward_linformer(q, k_pool, v_pool, page_table, e_k, e_v, n_cand: int, 
     qsel = range(len(qb)) if query_blocks is None else list(query_blocks)
     rows = np.concatenate([np.arange(*qb[i]) for i in qsel]) if len(qsel) else np.zeros(0, np.int64)
     sp = BO.hsa_forward_adaptive(q, k_pool, v_pool, page_table, n_cand, n_cur, k_h, tau_min,
-                                 tau_max, sm_scale=sm_scale, heads=heads, query_blocks=qsel)
+                                 tau_max, sm_scale=sm_scale, heads=heads, query_blocks=qsel,
+                                 linear=False)
     out = {"O": np.zeros((B, len(rows), H, d)), "O_lin": np.zeros((B, len(rows), H, d)),
            "lse_lin": np.zeros((B, H, len(rows))), "O_sp": sp["O_sp"], "sel": sp["sel"],
            "kept": sp["kept"], "gini": sp["gini"], "tau": sp["tau"], "rows": rows}

@@ -18,6 +18,10 @@ from .hsa import (  # noqa: F401
     hsa_block_count,
     hsa_block_select,
     hsa_forward_adaptive,
+    hsa_forward_linformer,
+    hsa_linformer_compress,
+    hsa_linformer_compress_workspace_size,
+    hsa_linformer_workspace_size,
     hsa_sparse_attn_adaptive,
     hsa_forward,
     hsa_forward_selected,

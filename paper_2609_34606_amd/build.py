@@ -16,7 +16,8 @@ CSRC = os.path.join(PKG, "csrc")
 LIBDIR = os.path.join(PKG, "lib")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(LIBDIR, "libhsa.so")
-SOURCES = ["hsa_api.hip", "hsa_state.hip", "hsa_select.hip", "hsa_blocks.hip", "hsa_attn.hip"]
+SOURCES = ["hsa_api.hip", "hsa_state.hip", "hsa_select.hip", "hsa_blocks.hip", "hsa_linformer.hip",
+           "hsa_attn.hip"]
 ARCH = "gfx950"
 
 

@@ -317,6 +317,34 @@ hsa_status_t check_adaptive(const hsa_config_t* c, int n_q, int k_max, int n_cur
   return HSA_OK;
 }
 
+// ---------------------------------------------------------------- Linformer branch
+bool valid_rank(int r) { return r == 32 || r == 64 || r == 128; }
+
+struct CompressPlan {
+  int parts, part_len;
+};
+
+// A page is split into parts (each a multiple of 64 tokens) only when there
+// are too few (page, head) pairs to fill the chip; parts add an fp32 partial
+// write and a reduction.
+CompressPlan plan_compress(const hsa_config_t* c, int n_pages) {
+  const int tiles = (c->page_size + 63) / 64;
+  const long items = (long)c->batch * c->num_heads * std::max(n_pages, 1);
+  int parts = 1;
+  if (c->dtype == HSA_DTYPE_BF16 && items < 512) parts = (int)std::min<long>(tiles, (768 + items - 1) / items);
+  const int part_len = (tiles + parts - 1) / parts * 64;
+  return CompressPlan{(c->page_size + part_len - 1) / part_len, part_len};
+}
+
+size_t compress_ws_bytes(const hsa_config_t* c, int rank, int n_pages, const CompressPlan& pl) {
+  if (pl.parts <= 1) return 0;
+  return align_up((size_t)c->batch * c->num_heads * n_pages * pl.parts * 2 * rank * c->head_dim * 4);
+}
+
+size_t o_lin_bytes(const hsa_config_t* c, int n_q) {
+  return align_up((size_t)c->batch * n_q * c->num_heads * c->head_dim * 4);
+}
+
 hsa_status_t run_select(const hsa_config_t* c, const void* q, int n_q, const double* kmean,
                         int max_pages, int n_cand, const int32_t* k_h, int k_max, int32_t* sel,
                         double* sel_score, void* ws, hipStream_t s) {
@@ -589,14 +617,16 @@ hsa_status_t hsa_sparse_attn_adaptive(const hsa_config_t* cfg, const void* q, in
 namespace {
 
 // Checks shared by hsa_forward and hsa_forward_selected.
+// need_state: the kernelised linear branch reads kv_state / k_state.
 hsa_status_t check_forward(const hsa_config_t* cfg, const void* q, int32_t n_q,
                            const hsa_kv_pool_t* pool, int32_t n_cand, int32_t n_cur_pages,
                            const int32_t* k_h, int32_t k_max, const float* kv_state,
-                           const float* k_state, const void* o) {
+                           const float* k_state, const void* o, bool need_state = true) {
   hsa_status_t st = check_cfg(cfg);
   if (st != HSA_OK) return st;
   if ((st = check_pool(pool)) != HSA_OK) return st;
-  if (!q || !k_h || !kv_state || !k_state || !o) return HSA_ERR_INVALID_ARG;
+  if (!q || !k_h || !o) return HSA_ERR_INVALID_ARG;
+  if (need_state && (!kv_state || !k_state)) return HSA_ERR_INVALID_ARG;
   if (n_q < 1 || n_cand < 0 || n_cur_pages < 0 || k_max < 1) return HSA_ERR_INVALID_ARG;
   if ((long)n_cand + n_cur_pages > pool->max_pages) return HSA_ERR_OUT_OF_RANGE;
   if (n_cand > HSA_MAX_CAND) return HSA_ERR_UNSUPPORTED;
@@ -613,8 +643,10 @@ hsa_status_t run_attend(const hsa_config_t* cfg, const void* q, int32_t n_q,
                         const int32_t* k_h, int32_t n_cand, int32_t n_cur_pages,
                         const float* kv_state, const float* k_state, const float* g_lin,
                         const float* g_sp, void* o, void* partials, hipStream_t s,
-                        const AdaptiveWs* w = nullptr, uint8_t* wbase = nullptr) {
+                        const AdaptiveWs* w = nullptr, uint8_t* wbase = nullptr,
+                        const float* o_lin = nullptr) {
   AttnParams p{};
+  p.o_lin = o_lin;
   p.q = q;
   p.k = pool->k;
   p.v = pool->v;
@@ -718,6 +750,93 @@ hsa_status_t hsa_forward_adaptive(const hsa_config_t* cfg, const void* q, int32_
   if (st != HSA_OK) return st;
   return run_attend(cfg, q, n_q, pool, sel, k_max, k_h, n_cand, n_cur_pages, kv_state, k_state,
                     g_lin, g_sp, o, base + w.part_off, s, &w, base);
+}
+
+size_t hsa_linformer_compress_workspace_size(const hsa_config_t* cfg, int32_t rank,
+                                             int32_t n_pages) {
+  if (check_cfg(cfg) != HSA_OK || !valid_rank(rank) || n_pages < 0) return 0;
+  return compress_ws_bytes(cfg, rank, n_pages, plan_compress(cfg, n_pages));
+}
+
+hsa_status_t hsa_linformer_compress(const hsa_config_t* cfg, const hsa_kv_pool_t* pool,
+                                    const void* e_k, const void* e_v, int32_t rank,
+                                    int32_t first_page, int32_t n_pages, void* ck, void* cv,
+                                    void* ws, size_t ws_bytes, void* stream) {
+  hsa_status_t st = check_cfg(cfg);
+  if (st != HSA_OK) return st;
+  if ((st = check_pool(pool)) != HSA_OK) return st;
+  if (!e_k || !e_v || !ck || !cv) return HSA_ERR_INVALID_ARG;
+  if (!valid_rank(rank)) return HSA_ERR_UNSUPPORTED;
+  if (first_page < 0 || n_pages < 0) return HSA_ERR_INVALID_ARG;
+  if ((long)first_page + n_pages > pool->max_pages) return HSA_ERR_OUT_OF_RANGE;
+  if (n_pages == 0) return HSA_OK;
+  const CompressPlan pl = plan_compress(cfg, n_pages);
+  if ((st = check_ws(ws, ws_bytes, compress_ws_bytes(cfg, rank, n_pages, pl))) != HSA_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = validate_pages(cfg, pool, first_page, n_pages, s)) != HSA_OK) return st;
+  CompressParams p{};
+  p.k = pool->k;
+  p.v = pool->v;
+  p.page_table = pool->page_table;
+  p.e_k = e_k;
+  p.e_v = e_v;
+  p.ck = ck;
+  p.cv = cv;
+  p.partial = static_cast<float*>(ws);
+  p.H = cfg->num_heads;
+  p.P = cfg->page_size;
+  p.R = rank;
+  p.D = cfg->head_dim;
+  p.num_slots = pool->num_slots;
+  p.max_pages = pool->max_pages;
+  p.first_page = first_page;
+  p.n_pages = n_pages;
+  p.parts = pl.parts;
+  p.part_len = pl.part_len;
+  return from_hip(launch_compress(cfg->dtype, cfg->batch, p, s));
+}
+
+size_t hsa_linformer_workspace_size(const hsa_config_t* cfg, int32_t n_q, int32_t k_max,
+                                    int32_t n_cur_pages) {
+  const size_t a = hsa_adaptive_workspace_size(cfg, n_q, k_max, n_cur_pages);
+  return a ? a + o_lin_bytes(cfg, n_q) : 0;
+}
+
+hsa_status_t hsa_forward_linformer(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                                   const hsa_kv_pool_t* pool, const void* ck, const void* cv,
+                                   int32_t rank, int32_t n_cand, int32_t n_cur_pages,
+                                   const int32_t* k_h, int32_t k_max, double tau_min,
+                                   double tau_max, const double* page_kmean, const float* g_lin,
+                                   const float* g_sp, void* o, int32_t* sel_out, void* ws,
+                                   size_t ws_bytes, void* stream) {
+  hsa_status_t st = check_forward(cfg, q, n_q, pool, n_cand, n_cur_pages, k_h, k_max, nullptr,
+                                  nullptr, o, false);
+  if (st != HSA_OK) return st;
+  if (!page_kmean || !ck || !cv) return HSA_ERR_INVALID_ARG;
+  if (!valid_rank(rank)) return HSA_ERR_UNSUPPORTED;
+  if ((st = check_adaptive(cfg, n_q, k_max, n_cur_pages, tau_min, tau_max)) != HSA_OK) return st;
+  const AdaptiveWs w = adaptive_ws(cfg, n_q, k_max, n_cur_pages);
+  if ((st = check_ws(ws, ws_bytes, w.total + o_lin_bytes(cfg, n_q))) != HSA_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = validate_pages(cfg, pool, 0, n_cand + n_cur_pages, s)) != HSA_OK) return st;
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  float* o_lin = reinterpret_cast<float*>(base + w.total);
+  int32_t* sel = sel_out ? sel_out : reinterpret_cast<int32_t*>(base + w.sel_off);
+  st = run_select(cfg, q, n_q, page_kmean, pool->max_pages, n_cand, k_h, k_max, sel, nullptr, ws, s);
+  if (st != HSA_OK) return st;
+  st = run_block_select(cfg, q, n_q, pool, sel, k_max, n_cand, n_cur_pages, tau_min, tau_max, w,
+                        base, true, BlockSelOut(), s);
+  if (st != HSA_OK) return st;
+  // linear branch: attention over the compressed pages of the same list (a
+  // pool of page size rank through the same page table)
+  hsa_config_t cr = *cfg;
+  cr.page_size = rank;
+  const hsa_kv_pool_t cpool{ck, cv, pool->page_table, pool->num_slots, pool->max_pages};
+  st = run_sparse(&cr, q, n_q, &cpool, sel, k_max, k_h, n_cand, n_cur_pages, o_lin, nullptr,
+                  base + w.part_off, nullptr, s);
+  if (st != HSA_OK) return st;
+  return run_attend(cfg, q, n_q, pool, sel, k_max, k_h, n_cand, n_cur_pages, nullptr, nullptr,
+                    g_lin, g_sp, o, base + w.part_off, s, &w, base, o_lin);
 }
 
 }  // extern "C"

@@ -119,6 +119,29 @@ __device__ __forceinline__ void finish(const AttnParams& p, uint8_t* smem, int b
     }
     return;
   }
+  if (p.o_lin) {
+    // linear branch from another launch (Linformer): gated sum only
+    if (q_ok) {
+      const size_t gi = ((size_t)b * p.n_q + q_idx) * H + h;
+      const float wl = p.g_lin ? 1.f / (1.f + __expf(-p.g_lin[gi])) : 0.5f;
+      const float wsp = p.g_sp ? 1.f / (1.f + __expf(-p.g_sp[gi])) : 0.5f;
+      const float a_sp = wsp * inv_l;
+      const float* lrow = p.o_lin + gi * D;
+      uint16_t* orow = static_cast<uint16_t*>(p.o) + gi * D;
+#pragma unroll
+      for (int m = 0; m < NM; ++m)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int d0 = 32 * m + 8 * g + 4 * half;
+          const f32x4 l = *reinterpret_cast<const f32x4*>(lrow + d0);
+          float v[4];
+#pragma unroll
+          for (int q2 = 0; q2 < 4; ++q2) v[q2] = wl * l[q2] + a_sp * acc[m][4 * g + q2];
+          *reinterpret_cast<u32x2*>(orow + d0) = u32x2{pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
+        }
+    }
+    return;
+  }
   __syncthreads();  // all waves are done with the shared memory
   constexpr int RH = D / 2;  // state rows per half
   uint8_t* sh = smem;
@@ -691,14 +714,20 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
       p.lse[((size_t)b * H + h) * p.n_q + qi] = l_run > 0.f ? m_run + logf(l_run) : -INFINITY;
     return;
   }
-  const float* st = p.kv_state + ((size_t)b * H + h) * D * D;
-  const float* zz = p.k_state + ((size_t)b * H + h) * D;
-  float den = 0.f;
-  for (int i = 0; i < D; ++i) den = fmaf(phi(qs[qr][i]), zz[i], den);
   const size_t gi = ((size_t)b * p.n_q + qi) * H + h;
   const float wl = p.g_lin ? 1.f / (1.f + expf(-p.g_lin[gi])) : 0.5f;
   const float wsp = p.g_sp ? 1.f / (1.f + expf(-p.g_sp[gi])) : 0.5f;
   float* orow = static_cast<float*>(p.o) + gi * D + part * DP;
+  if (p.o_lin) {
+    // linear branch from another launch (Linformer): gated sum only
+    const float* lrow = p.o_lin + gi * D + part * DP;
+    for (int e = 0; e < DP; ++e) orow[e] = wl * lrow[e] + wsp * acc[e] * inv_l;
+    return;
+  }
+  const float* st = p.kv_state + ((size_t)b * H + h) * D * D;
+  const float* zz = p.k_state + ((size_t)b * H + h) * D;
+  float den = 0.f;
+  for (int i = 0; i < D; ++i) den = fmaf(phi(qs[qr][i]), zz[i], den);
   for (int e = 0; e < DP; ++e) {
     const int j = part * DP + e;
     float num = 0.f;

@@ -109,6 +109,25 @@ hipError_t launch_block_select(int dtype, int d, int B, const BlockSelParams& p,
 // LDS bytes of one pooled-rows workgroup (at most 64 KB is allowed).
 size_t block_rows_lds_bytes(int d, int n_pad, int rpg);
 
+// ------------------------------------------------------------ Linformer compression
+struct CompressParams {
+  const void* k;              // pool keys [num_slots, H, P, d]
+  const void* v;              // pool values [num_slots, H, d, P]
+  const int32_t* page_table;  // [B, max_pages]
+  const void* e_k;            // [H, R, P]: e_k[h][j][t] = E_K^(h)[t][j]
+  const void* e_v;            // [H, R, P]
+  void* ck;                   // [num_slots, H, R, d]
+  void* cv;                   // [num_slots, H, d, R]
+  float* partial;             // [B, H, n_pages, parts, 2, R*d] (parts > 1)
+  int32_t H, P, R, D, num_slots, max_pages, first_page, n_pages;
+  int32_t parts;              // parts per page
+  int32_t part_len;           // tokens per part (multiple of 64)
+};
+
+// Compresses logical pages [first_page, first_page + n_pages) of every batch
+// entry (bf16: R in {32, 64, 128}; fp32: any R).
+hipError_t launch_compress(int dtype, int B, const CompressParams& p, hipStream_t s);
+
 // ------------------------------------------------------------ attention
 enum AttnMode : int32_t {
   ATTN_FINAL = 0,   // fused linear branch + gated merge, write o (dtype)
@@ -157,6 +176,8 @@ struct AttnParams {
   const float* g_lin;       // [B, n_q, H] nullable
   const float* g_sp;
   void* o;                  // [B, n_q, H, d] dtype
+  const float* o_lin;       // [B, n_q, H, d] fp32 linear-branch output of another
+                            // launch; NULL: the kernelised branch from the state
   // sparse mode
   float* o_sp;              // [B, n_q, H, d]
   float* lse;               // [B, H, n_q] nullable

@@ -65,6 +65,19 @@ def lib():
         f = getattr(L, n)
         f.restype = c_sz
         f.argtypes = [P(HsaConfig)] + extra
+    for n, extra in (("hsa_linformer_compress_workspace_size", [c_i32, c_i32]),
+                     ("hsa_linformer_workspace_size", [c_i32, c_i32, c_i32])):
+        f = getattr(L, n)
+        f.restype = c_sz
+        f.argtypes = [P(HsaConfig)] + extra
+    L.hsa_linformer_compress.restype = ctypes.c_int
+    L.hsa_linformer_compress.argtypes = [P(HsaConfig), P(HsaKvPool), c_vp, c_vp, c_i32, c_i32,
+                                         c_i32, c_vp, c_vp, c_vp, c_sz, c_vp]
+    L.hsa_forward_linformer.restype = ctypes.c_int
+    L.hsa_forward_linformer.argtypes = [P(HsaConfig), c_vp, c_i32, P(HsaKvPool), c_vp, c_vp, c_i32,
+                                        c_i32, c_i32, c_vp, c_i32, ctypes.c_double,
+                                        ctypes.c_double, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz,
+                                        c_vp]
     L.hsa_block_count.restype = c_i32
     L.hsa_block_count.argtypes = [P(HsaConfig), c_i32, c_i32]
     c_f64 = ctypes.c_double
@@ -293,4 +306,40 @@ def hsa_forward_adaptive(cfg, q, n_q, pool, n_cand, n_cur_pages, k_h, k_max, kv_
                                     0 if ws is None else ws.numel(), _stream(stream))
     if check:
         _check("hsa_forward_adaptive", st)
+    return st
+
+
+def hsa_linformer_compress_workspace_size(cfg: HsaConfig, rank: int, n_pages: int) -> int:
+    return lib().hsa_linformer_compress_workspace_size(ctypes.byref(cfg), rank, n_pages)
+
+
+def hsa_linformer_workspace_size(cfg: HsaConfig, n_q: int, k_max: int, n_cur_pages: int) -> int:
+    return lib().hsa_linformer_workspace_size(ctypes.byref(cfg), n_q, k_max, n_cur_pages)
+
+
+def hsa_linformer_compress(cfg, pool, e_k, e_v, rank, first_page, n_pages, ck, cv, ws=None,
+                           stream=None, check=True) -> int:
+    if ws is None:
+        ws = _workspace(hsa_linformer_compress_workspace_size(cfg, rank, n_pages), ck.device)
+    st = lib().hsa_linformer_compress(ctypes.byref(cfg), ctypes.byref(pool), _ptr(e_k), _ptr(e_v),
+                                      rank, first_page, n_pages, _ptr(ck), _ptr(cv), _ptr(ws),
+                                      0 if ws is None else ws.numel(), _stream(stream))
+    if check:
+        _check("hsa_linformer_compress", st)
+    return st
+
+
+def hsa_forward_linformer(cfg, q, n_q, pool, ck, cv, rank, n_cand, n_cur_pages, k_h, k_max,
+                          page_kmean, g_lin, g_sp, o, tau_min=TAU_MIN, tau_max=TAU_MAX,
+                          sel_out=None, ws=None, stream=None, check=True) -> int:
+    if ws is None:
+        ws = _workspace(hsa_linformer_workspace_size(cfg, n_q, k_max, n_cur_pages), q.device)
+    _keep, kp = _budgets(k_h)
+    st = lib().hsa_forward_linformer(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool), _ptr(ck),
+                                     _ptr(cv), rank, n_cand, n_cur_pages, kp, k_max,
+                                     float(tau_min), float(tau_max), _ptr(page_kmean), _ptr(g_lin),
+                                     _ptr(g_sp), _ptr(o), _ptr(sel_out), _ptr(ws),
+                                     0 if ws is None else ws.numel(), _stream(stream))
+    if check:
+        _check("hsa_forward_linformer", st)
     return st

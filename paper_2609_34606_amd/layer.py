@@ -48,6 +48,24 @@ class HsaLayer:
             self._ws[key] = w
         return w
 
+    def set_projections(self, e_k, e_v):
+        """Linformer projections ([H, rank, P] each, e[h][j][t] = E^(h)[t][j])
+        and a compressed pool for every slot of the layer's pool."""
+        torch = self.torch
+        H, rank = e_k.shape[0], e_k.shape[1]
+        self.e_k, self.e_v, self.rank = e_k, e_v, rank
+        slots = self.k_pool.shape[0]
+        d = self.k_pool.shape[-1]
+        self.ck = torch.empty((slots, H, rank, d), dtype=self.k_pool.dtype, device=self.device)
+        self.cv = torch.empty((slots, H, d, rank), dtype=self.k_pool.dtype, device=self.device)
+
+    def compress(self, first_page: int, n_pages: int, stream=None):
+        """Compress logical pages [first, first+n) with the Linformer projections."""
+        ws = self.workspace("compress", _h.hsa_linformer_compress_workspace_size(
+            self.cfg, self.rank, n_pages))
+        _h.hsa_linformer_compress(self.cfg, self.pool, self.e_k, self.e_v, self.rank, first_page,
+                                  n_pages, self.ck, self.cv, ws=ws, stream=stream)
+
     def reset_state(self):
         self.kv_state.zero_()
         self.k_state.zero_()
@@ -96,4 +114,21 @@ class HsaLayer:
                                 self.kv_state, self.k_state, self.page_kmean, g_lin, g_sp, out,
                                 tau_min=tau_min, tau_max=tau_max, sel_out=sel_out, ws=ws,
                                 stream=stream)
+        return out
+
+    def forward_linformer(self, q, n_cand: int, n_cur: int, k_h: Sequence[int],
+                          k_max: Optional[int] = None, tau_min: float = _h.TAU_MIN,
+                          tau_max: float = _h.TAU_MAX, g_lin=None, g_sp=None, out=None,
+                          sel_out=None, stream=None):
+        """The forward pass with the Linformer linear branch over the compressed
+        pages and the head-adaptive block-sparse sparse branch."""
+        B, n_q = q.shape[0], q.shape[1]
+        k_max = max(1, max(k_h)) if k_max is None else k_max
+        if out is None:
+            out = self.torch.empty_like(q)
+        ws = self.workspace("fwd_linformer", _h.hsa_linformer_workspace_size(self.cfg, n_q, k_max, n_cur))
+        _h.hsa_forward_linformer(self.cfg, q, n_q, self.pool, self.ck, self.cv, self.rank, n_cand,
+                                 n_cur, k_h, k_max, self.page_kmean, g_lin, g_sp, out,
+                                 tau_min=tau_min, tau_max=tau_max, sel_out=sel_out, ws=ws,
+                                 stream=stream)
         return out
