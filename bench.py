@@ -185,6 +185,8 @@ def bench_single(args, wl):
     }
     if not args.no_adaptive:
         res["adaptive"] = bench_adaptive(args, wl, layer, q, k_h, k_max, sel)
+        if wl.dtype == "bf16":
+            res["linformer"] = bench_linformer(args, wl, layer, q, k_h, k_max, sel)
     if not args.no_cpu_baseline:
         heads = list(range(wl.heads)) if wl.heads * wl.n_pages <= 12 * 24 else [0, 1]
         log("timing the oracle on the host ...")
@@ -288,6 +290,62 @@ def bench_adaptive(args, wl, layer, q, k_h, k_max, sel):
                      "traffic": measured_traffic(wl.name, "hbm_bytes_per_launch_tile_list"),
                      "kernel": "attn_bf16_kernel, tile-list mode (sparse-branch launch)",
                      "flops_per_launch": fa},
+    }
+
+
+def bench_linformer(args, wl, layer, q, k_h, k_max, sel, rank=64):
+    """The paper's two branches on the same layer and chunk: page selection,
+    head-adaptive block-sparse sparse branch and the Linformer linear branch
+    over the compressed pages (rank 64, seeded projections). The step is the
+    cold page index (hsa_state_update) + the compression of every page +
+    hsa_forward_linformer; the branch launch is the attention over the
+    compressed pool for the step's selection."""
+    import torch
+    from paper_2609_34606_amd import config as mkcfg
+    from paper_2609_34606_amd import hsa_sparse_attn, hsa_sparse_attn_workspace_size, kv_pool
+    from synth_inputs import make_projections
+    n_q, n_pages = wl.n_q, wl.n_pages
+    e_k, e_v = make_projections(wl, rank)
+    to = lambda a: torch.from_numpy(a).to(q.device).to(q.dtype)
+    layer.set_projections(to(e_k), to(e_v))
+    out = torch.empty_like(q)
+
+    def step():
+        layer.fold(0, n_pages)
+        layer.compress(0, n_pages)
+        layer.forward_linformer(q, wl.n_cand, wl.n_cur, k_h, k_max=k_max, out=out)
+
+    for _ in range(args.warmup):
+        step()
+    ms = time_loop(step, args.steps, torch)
+    ms_cold = time_loop(lambda: layer.compress(0, n_pages), args.steps, torch)
+    ms_warm = time_loop(lambda: layer.compress(wl.n_cand, wl.n_cur), args.steps, torch)
+    ms_fwd = time_loop(lambda: layer.forward_linformer(q, wl.n_cand, wl.n_cur, k_h, k_max=k_max,
+                                                       out=out, sel_out=sel), args.steps, torch)
+    crank = mkcfg(wl.batch, wl.heads, wl.head_dim, rank, q.dtype)
+    cpool = kv_pool(layer.ck, layer.cv, layer.page_table)
+    o_lin = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    ws = layer.workspace("lin_attn", hsa_sparse_attn_workspace_size(crank, n_q, k_max, wl.n_cur))
+    ms_br = time_loop(lambda: hsa_sparse_attn(crank, q, n_q, cpool, sel, k_max, k_h, wl.n_cand,
+                                              wl.n_cur, o_lin, ws=ws), args.steps, torch)
+    k_eff = [min(k, wl.n_cand) for k in k_h]
+    fb = sum(4.0 * n_q * (k + wl.n_cur) * rank * wl.head_dim for k in k_eff) * wl.batch
+    esz = 2
+    cbytes = n_pages * wl.heads * wl.batch * (2 * wl.page_size * wl.head_dim * esz +
+                                             2 * rank * wl.head_dim * esz)
+    peak = PEAK_BF16_TFLOPS
+    return {
+        "rank": rank, "projections": "seeded N(0, 1/P)", "ms_per_step": round(ms, 4),
+        "phases_ms": {"compress_cold_all_pages": round(ms_cold, 4),
+                      "compress_current_pages": round(ms_warm, 4),
+                      "forward_linformer": round(ms_fwd, 4),
+                      "linformer_branch_launch": round(ms_br, 4)},
+        "compress_hbm_gbs": round(cbytes / (ms_cold * 1e-3) / 1e9, 1),
+        "compress_hbm_frac": round(cbytes / (ms_cold * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "branch_roofline": {"bound": "mfma", "achieved": round(fb / (ms_br * 1e-3) / 1e12, 2),
+                            "peak": peak, "unit": "TFLOP/s",
+                            "frac": round(fb / (ms_br * 1e-3) / 1e12 / peak, 4),
+                            "flops_per_launch": fb},
     }
 
 

@@ -325,13 +325,13 @@ struct CompressPlan {
 };
 
 // A page is split into parts (each a multiple of 64 tokens) only when there
-// are too few (page, head) pairs to fill the chip; parts add an fp32 partial
-// write and a reduction.
+// are too few (page, head) pairs to give every CU a workgroup; parts add an
+// fp32 partial write and a reduction (64 KB per part at rank 64, d = 128).
 CompressPlan plan_compress(const hsa_config_t* c, int n_pages) {
   const int tiles = (c->page_size + 63) / 64;
   const long items = (long)c->batch * c->num_heads * std::max(n_pages, 1);
   int parts = 1;
-  if (c->dtype == HSA_DTYPE_BF16 && items < 512) parts = (int)std::min<long>(tiles, (768 + items - 1) / items);
+  if (c->dtype == HSA_DTYPE_BF16 && items < 256) parts = (int)std::min<long>(tiles, (256 + items - 1) / items);
   const int part_len = (tiles + parts - 1) / parts * 64;
   return CompressPlan{(c->page_size + part_len - 1) / part_len, part_len};
 }

@@ -180,24 +180,24 @@ __global__ __launch_bounds__(256) void compress_bf16_kernel(CompressParams p) {
   }
 }
 
-// Sum of a page's parts in part order, rounded once to the pool's type.
-template <typename T>
+// Sum of a page's parts in part order, rounded once to bf16. One workgroup
+// per (1024 outputs, page, head), four consecutive outputs per thread.
+constexpr int kReduceChunk = 1024;
+
 __global__ __launch_bounds__(256) void compress_reduce_kernel(CompressParams p) {
-  const int pi = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int RD = p.R * p.D;
+  const int chunks = 2 * RD / kReduceChunk;
+  const int pi = blockIdx.x / chunks, c = blockIdx.x % chunks, h = blockIdx.y, b = blockIdx.z;
   const int page = p.first_page + pi;
   const int slot = clampi(p.page_table[(size_t)b * p.max_pages + page], 0, p.num_slots - 1);
   const size_t hb = (size_t)slot * p.H + h;
-  const int RD = p.R * p.D;
   const float* src = p.partial + (((size_t)b * p.H + h) * p.n_pages + pi) * p.parts * (2 * RD);
-  T* ck = static_cast<T*>(p.ck) + hb * RD;
-  T* cv = static_cast<T*>(p.cv) + hb * RD;
-  for (int e = threadIdx.x; e < 2 * RD; e += 256) {
-    float s = 0.f;
-    for (int k = 0; k < p.parts; ++k) s += src[(size_t)k * 2 * RD + e];
-    T* dst = e < RD ? ck + e : cv + (e - RD);
-    if constexpr (sizeof(T) == 2) *dst = (T)(pack_bf16(s, 0.f) & 0xffffu);
-    else *dst = s;
-  }
+  const int e = c * kReduceChunk + 4 * threadIdx.x;
+  f32x4 s = *reinterpret_cast<const f32x4*>(src + e);
+  for (int k = 1; k < p.parts; ++k) s += *reinterpret_cast<const f32x4*>(src + (size_t)k * 2 * RD + e);
+  uint16_t* dst = (e < RD ? static_cast<uint16_t*>(p.ck) + hb * RD + e
+                          : static_cast<uint16_t*>(p.cv) + hb * RD + (e - RD));
+  *reinterpret_cast<u32x2*>(dst) = u32x2{pack_bf16(s.x, s.y), pack_bf16(s.z, s.w)};
 }
 
 // fp32 inputs: plain VALU products, fp32 accumulation in token order (small
@@ -253,7 +253,8 @@ hipError_t launch_compress(int dtype, int B, const CompressParams& p, hipStream_
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.parts == 1) return e;
-  compress_reduce_kernel<uint16_t><<<dim3(p.n_pages, p.H, B), 256, 0, s>>>(p);
+  // 2 R d is a multiple of kReduceChunk for every supported (R, d)
+  compress_reduce_kernel<<<dim3(p.n_pages * (2 * p.R * p.D / kReduceChunk), p.H, B), 256, 0, s>>>(p);
   return hipGetLastError();
 }
 
