@@ -307,6 +307,49 @@ hsa_status_t hsa_forward_adaptive(const hsa_config_t* cfg, const void* q, int32_
                                   int32_t* sel_out, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * Two-stage retrieval of the hierarchical KV cache (Sec. 3.2). The KV bank is
+ * a sequence of chunks in generation order, chunk m holding the history pages
+ * [chunk_first[b][m], chunk_first[b][m+1]) (chunk_first[b][n_chunks] =
+ * n_cand), with one prompt embedding per chunk (the chunk index).
+ *
+ * hsa_chunk_select -- Stage 1, prompt-level retrieval: per batch entry,
+ *   cos_m = (p . c_m) / (|p| |c_m|)  (0 when a norm is 0), fp64,
+ * and the top-1 chunk m* by (cos desc, m asc). Writes chunk_out[b] = m*
+ * (nullable), chunk_score[b] = cos_m* (nullable, fp64) and cand_range[b] =
+ * {chunk_first[b][m*], chunk_first[b][m*+1]} clamped to [0, n_cand] (device
+ * int32 [B, 2], the Stage-2 candidates). prompt_emb: device fp32 [B, E];
+ * chunk_emb: device fp32 [B, n_chunks, E]; chunk_first: device int32
+ * [B, n_chunks + 1].
+ */
+hsa_status_t hsa_chunk_select(const hsa_config_t* cfg, const float* prompt_emb,
+                              const float* chunk_emb, int32_t emb_dim, int32_t n_chunks,
+                              const int32_t* chunk_first, int32_t n_cand, int32_t* chunk_out,
+                              double* chunk_score, int32_t* cand_range, void* stream);
+
+/* Workspace of hsa_forward_retrieval. */
+size_t hsa_retrieval_workspace_size(const hsa_config_t* cfg, int32_t n_q, int32_t k_max,
+                                    int32_t n_cur_pages);
+
+/*
+ * hsa_forward_retrieval -- hsa_forward with Stage 1 in front: the chunk of
+ * hsa_chunk_select, then Stage-2 page selection among that chunk's pages only
+ * (sel holds logical page indices; a head keeps min(k_h[h], pages of the
+ * chunk) pages), the sparse branch over them plus the current pages
+ * [n_cand, n_cand + n_cur_pages), the linear branch over the state and the
+ * gated fusion. chunk_out: device int32 [B] or NULL. Other arguments and
+ * errors as hsa_forward. ws: hsa_retrieval_workspace_size(...) bytes.
+ */
+hsa_status_t hsa_forward_retrieval(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                                   const hsa_kv_pool_t* pool, const float* prompt_emb,
+                                   const float* chunk_emb, int32_t emb_dim, int32_t n_chunks,
+                                   const int32_t* chunk_first, int32_t n_cand,
+                                   int32_t n_cur_pages, const int32_t* k_h, int32_t k_max,
+                                   const float* kv_state, const float* k_state,
+                                   const double* page_kmean, const float* g_lin,
+                                   const float* g_sp, void* o, int32_t* chunk_out,
+                                   int32_t* sel_out, void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Linformer linear branch (Sec. 3.3 "Linear branch"; App. "Linear Branch"):
  * per head h, projections E_K^(h), E_V^(h) in R^{L x r} compress keys and
  * values along the sequence. The sequence is cut into segments of length L

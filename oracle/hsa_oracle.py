@@ -169,7 +169,8 @@ def hsa_forward(q, k_pool, v_pool, page_table, n_cand: int, n_cur: int,
                 sm_scale: Optional[float] = None, k_max: Optional[int] = None,
                 heads: Optional[Sequence[int]] = None,
                 query_rows: Optional[Sequence[int]] = None,
-                state_pages: Optional[Sequence[int]] = None) -> Dict[str, np.ndarray]:
+                state_pages: Optional[Sequence[int]] = None,
+                cand_range: Optional[Sequence[Sequence[int]]] = None) -> Dict[str, np.ndarray]:
     """HSA forward for one chunk.
 
     q [B,n_q,H,d]; history (candidate) pages are logical pages [0, n_cand);
@@ -184,6 +185,9 @@ def hsa_forward(q, k_pool, v_pool, page_table, n_cand: int, n_cur: int,
       7. gated merge.
     ``query_rows`` restricts steps 5-7 to some queries (step 2 always uses
     all of them); ``heads`` restricts everything to some heads.
+    ``cand_range[b] = (lo, hi)`` restricts the candidates of batch entry b
+    to logical pages [lo, hi) within the history (Stage-1 retrieval picks
+    one chunk); ``alpha`` then holds scores at those positions only.
     """
     q = np.asarray(q)
     B, n_q, H, d = q.shape
@@ -210,8 +214,10 @@ def hsa_forward(q, k_pool, v_pool, page_table, n_cand: int, n_cur: int,
             kbar = np.stack([page_key_mean(k_pool[int(page_table[b, p]), h])
                              for p in range(n_cand + n_cur)]) if n_cand + n_cur else np.zeros((0, d))
             qbar = query_mean(q[b, :, h, :])
-            alpha = page_scores(qbar, kbar[:n_cand])
-            sel = select_top_pages(alpha, k_h[h])
+            lo, hi = (0, n_cand) if cand_range is None else (int(cand_range[b][0]), int(cand_range[b][1]))
+            alpha = np.zeros(n_cand)
+            alpha[lo:hi] = page_scores(qbar, kbar[lo:hi])
+            sel = lo + select_top_pages(alpha[lo:hi], k_h[h])
             out["kbar"][b, h] = kbar
             out["qbar"][b, h] = qbar
             out["alpha"][b, h] = alpha

@@ -17,7 +17,10 @@ from .hsa import (  # noqa: F401
     hsa_adaptive_workspace_size,
     hsa_block_count,
     hsa_block_select,
+    hsa_chunk_select,
     hsa_forward_adaptive,
+    hsa_forward_retrieval,
+    hsa_retrieval_workspace_size,
     hsa_forward_linformer,
     hsa_linformer_compress,
     hsa_linformer_compress_workspace_size,

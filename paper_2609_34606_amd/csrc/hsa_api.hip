@@ -347,7 +347,8 @@ size_t o_lin_bytes(const hsa_config_t* c, int n_q) {
 
 hsa_status_t run_select(const hsa_config_t* c, const void* q, int n_q, const double* kmean,
                         int max_pages, int n_cand, const int32_t* k_h, int k_max, int32_t* sel,
-                        double* sel_score, void* ws, hipStream_t s) {
+                        double* sel_score, void* ws, hipStream_t s,
+                        const int32_t* cand_range = nullptr) {
   QsumParams qp{};
   qp.q = q;
   qp.n_q = n_q;
@@ -367,6 +368,7 @@ hsa_status_t run_select(const hsa_config_t* c, const void* q, int n_q, const dou
   for (int h = 0; h < c->num_heads; ++h) sp.k_h[h] = k_h[h];
   sp.sel = sel;
   sp.sel_score = sel_score;
+  sp.cand_range = cand_range;
   return from_hip(launch_page_select(c->dtype, c->head_dim, c->batch, qp, sp, s));
 }
 
@@ -750,6 +752,65 @@ hsa_status_t hsa_forward_adaptive(const hsa_config_t* cfg, const void* q, int32_
   if (st != HSA_OK) return st;
   return run_attend(cfg, q, n_q, pool, sel, k_max, k_h, n_cand, n_cur_pages, kv_state, k_state,
                     g_lin, g_sp, o, base + w.part_off, s, &w, base);
+}
+
+hsa_status_t hsa_chunk_select(const hsa_config_t* cfg, const float* prompt_emb,
+                              const float* chunk_emb, int32_t emb_dim, int32_t n_chunks,
+                              const int32_t* chunk_first, int32_t n_cand, int32_t* chunk_out,
+                              double* chunk_score, int32_t* cand_range, void* stream) {
+  hsa_status_t st = check_cfg(cfg);
+  if (st != HSA_OK) return st;
+  if (!prompt_emb || !chunk_emb || !chunk_first || !cand_range) return HSA_ERR_INVALID_ARG;
+  if (emb_dim < 1 || n_chunks < 1 || n_cand < 0) return HSA_ERR_INVALID_ARG;
+  ChunkSelectParams p{};
+  p.prompt = prompt_emb;
+  p.chunks = chunk_emb;
+  p.chunk_first = chunk_first;
+  p.E = emb_dim;
+  p.M = n_chunks;
+  p.n_cand = n_cand;
+  p.chunk_out = chunk_out;
+  p.chunk_score = chunk_score;
+  p.cand_range = cand_range;
+  return from_hip(launch_chunk_select(cfg->batch, p, static_cast<hipStream_t>(stream)));
+}
+
+size_t hsa_retrieval_workspace_size(const hsa_config_t* cfg, int32_t n_q, int32_t k_max,
+                                    int32_t n_cur_pages) {
+  const size_t f = hsa_forward_workspace_size(cfg, n_q, k_max, n_cur_pages);
+  return f ? f + align_up((size_t)cfg->batch * 2 * 4) : 0;
+}
+
+hsa_status_t hsa_forward_retrieval(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                                   const hsa_kv_pool_t* pool, const float* prompt_emb,
+                                   const float* chunk_emb, int32_t emb_dim, int32_t n_chunks,
+                                   const int32_t* chunk_first, int32_t n_cand,
+                                   int32_t n_cur_pages, const int32_t* k_h, int32_t k_max,
+                                   const float* kv_state, const float* k_state,
+                                   const double* page_kmean, const float* g_lin,
+                                   const float* g_sp, void* o, int32_t* chunk_out,
+                                   int32_t* sel_out, void* ws, size_t ws_bytes, void* stream) {
+  hsa_status_t st = check_forward(cfg, q, n_q, pool, n_cand, n_cur_pages, k_h, k_max, kv_state,
+                                  k_state, o);
+  if (st != HSA_OK) return st;
+  if (!page_kmean || !prompt_emb || !chunk_emb || !chunk_first) return HSA_ERR_INVALID_ARG;
+  if (emb_dim < 1 || n_chunks < 1) return HSA_ERR_INVALID_ARG;
+  const size_t fwd = hsa_forward_workspace_size(cfg, n_q, k_max, n_cur_pages);
+  if ((st = check_ws(ws, ws_bytes, fwd + align_up((size_t)cfg->batch * 2 * 4))) != HSA_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = validate_pages(cfg, pool, 0, n_cand + n_cur_pages, s)) != HSA_OK) return st;
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  int32_t* range = reinterpret_cast<int32_t*>(base + fwd);
+  st = hsa_chunk_select(cfg, prompt_emb, chunk_emb, emb_dim, n_chunks, chunk_first, n_cand,
+                        chunk_out, nullptr, range, stream);
+  if (st != HSA_OK) return st;
+  int32_t* sel = sel_out ? sel_out : reinterpret_cast<int32_t*>(base + select_ws_bytes(cfg, n_q));
+  void* partials = base + select_ws_bytes(cfg, n_q) + sel_ws_bytes(cfg, k_max);
+  st = run_select(cfg, q, n_q, page_kmean, pool->max_pages, n_cand, k_h, k_max, sel, nullptr, ws, s,
+                  range);
+  if (st != HSA_OK) return st;
+  return run_attend(cfg, q, n_q, pool, sel, k_max, k_h, n_cand, n_cur_pages, kv_state, k_state,
+                    g_lin, g_sp, o, partials, s);
 }
 
 size_t hsa_linformer_compress_workspace_size(const hsa_config_t* cfg, int32_t rank,

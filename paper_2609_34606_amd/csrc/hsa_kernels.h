@@ -56,7 +56,22 @@ struct SelectParams {
   int32_t k_h[HSA_MAX_HEADS];
   int32_t* sel;             // [B, H, k_max]
   double* sel_score;        // nullable
+  const int32_t* cand_range;  // [B, 2] candidate pages [lo, hi) of each batch
+                              // entry (Stage-1 chunk), nullable: [0, n_cand)
 };
+
+// Stage-1 prompt-level retrieval: top-1 chunk by cosine similarity.
+struct ChunkSelectParams {
+  const float* prompt;      // [B, E]
+  const float* chunks;      // [B, M, E]
+  const int32_t* chunk_first;  // [B, M + 1] first logical page of each chunk
+  int32_t E, M, n_cand;
+  int32_t* chunk_out;       // [B] nullable
+  double* chunk_score;      // [B] nullable
+  int32_t* cand_range;      // [B, 2] pages of the chosen chunk, clamped to [0, n_cand]
+};
+
+hipError_t launch_chunk_select(int B, const ChunkSelectParams& p, hipStream_t s);
 
 hipError_t launch_page_select(int dtype, int d, int B, const QsumParams& qp,
                               const SelectParams& sp, hipStream_t s);

@@ -123,21 +123,24 @@ __global__ __launch_bounds__(256) void select_kernel(SelectParams p) {
     __syncthreads();
   }
 
+  // candidates: logical pages [lo, lo + n_c)
+  const int lo = p.cand_range ? clampi(p.cand_range[2 * b], 0, p.n_cand) : 0;
+  const int n_c = p.cand_range ? clampi(p.cand_range[2 * b + 1], lo, p.n_cand) - lo : p.n_cand;
   // scores: 16 lanes per candidate, DS consecutive dims each, reduced in a
   // fixed butterfly order
-  const double* km = p.page_kmean + (size_t)bh * p.max_pages * D;
+  const double* km = p.page_kmean + ((size_t)bh * p.max_pages + lo) * D;
   const int sub = tid & 15;
   double qv[DS];
 #pragma unroll
   for (int e = 0; e < DS; ++e) qv[e] = qbar[sub * DS + e];
   const double rsd = sqrt((double)D);
-  for (int c0 = 0; c0 < p.n_cand; c0 += 16 * 2) {
+  for (int c0 = 0; c0 < n_c; c0 += 16 * 2) {
     double part[2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int c = c0 + u * 16 + (tid >> 4);
       part[u] = 0.0;
-      if (c < p.n_cand) {
+      if (c < n_c) {
         const double* kr = km + (size_t)c * D + sub * DS;
 #pragma unroll
         for (int e = 0; e < DS; ++e) part[u] = fma(qv[e], kr[e], part[u]);
@@ -151,7 +154,7 @@ __global__ __launch_bounds__(256) void select_kernel(SelectParams p) {
       v += __shfl_xor(v, 2);
       v += __shfl_xor(v, 1);
       const int c = c0 + u * 16 + (tid >> 4);
-      if (sub == 0 && c < p.n_cand) {
+      if (sub == 0 && c < n_c) {
         score[c] = v / rsd;
         taken[c] = 0;
       }
@@ -159,7 +162,7 @@ __global__ __launch_bounds__(256) void select_kernel(SelectParams p) {
   }
   __syncthreads();
 
-  const int k_eff = min(p.k_h[h], p.n_cand);
+  const int k_eff = min(p.k_h[h], n_c);
   int32_t* sel = p.sel + (size_t)bh * p.k_max;
   double* sc = p.sel_score ? p.sel_score + (size_t)bh * p.k_max : nullptr;
   for (int r = k_eff + tid; r < p.k_max; r += 256) {
@@ -167,18 +170,18 @@ __global__ __launch_bounds__(256) void select_kernel(SelectParams p) {
     if (sc) sc[r] = 0.0;
   }
   if (k_eff == 0) return;
-  if (p.n_cand <= 2048) {
+  if (n_c <= 2048) {
     // rank of each candidate in the (score desc, index asc) order; ranks are
     // a permutation for comparable scores (rows start at -1 in case a NaN
     // score breaks that)
     for (int r = tid; r < k_eff; r += 256) sel[r] = -1;
     __syncthreads();
-    for (int c = tid; c < p.n_cand; c += 256) {
+    for (int c = tid; c < n_c; c += 256) {
       const Best me{score[c], c};
       int rank = 0;
-      for (int o = 0; o < p.n_cand; ++o) rank += before(Best{score[o], o}, me) ? 1 : 0;
+      for (int o = 0; o < n_c; ++o) rank += before(Best{score[o], o}, me) ? 1 : 0;
       if (rank < k_eff) {
-        sel[rank] = c;
+        sel[rank] = lo + c;
         if (sc) sc[rank] = me.s;
       }
     }
@@ -188,7 +191,7 @@ __global__ __launch_bounds__(256) void select_kernel(SelectParams p) {
   for (int r = 0; r < k_eff; ++r) {
     Best best{-DBL_MAX, INT32_MAX};
     bool have = false;
-    for (int c = tid; c < p.n_cand; c += 256) {
+    for (int c = tid; c < n_c; c += 256) {
       if (taken[c]) continue;
       const Best cand{score[c], c};
       if (!have || before(cand, best)) { best = cand; have = true; }
@@ -204,18 +207,70 @@ __global__ __launch_bounds__(256) void select_kernel(SelectParams p) {
     if (tid == 0) {
       Best bb = wbest[0];
       for (int w = 1; w < 4; ++w)
-        if (wbest[w].i < p.n_cand && (bb.i >= p.n_cand || before(wbest[w], bb))) bb = wbest[w];
+        if (wbest[w].i < n_c && (bb.i >= n_c || before(wbest[w], bb))) bb = wbest[w];
       // a NaN score can leave no comparable candidate: pad instead of indexing
-      const bool ok = bb.i >= 0 && bb.i < p.n_cand;
+      const bool ok = bb.i >= 0 && bb.i < n_c;
       if (ok) taken[bb.i] = 1;
-      sel[r] = ok ? bb.i : -1;
+      sel[r] = ok ? lo + bb.i : -1;
       if (sc) sc[r] = ok ? bb.s : 0.0;
     }
     __syncthreads();
   }
 }
 
+// Stage-1 prompt-level retrieval (Sec. 3.2): one workgroup per batch entry.
+// Each wave takes every fourth chunk: fp64 dot product and norm over the
+// embedding dimension (lanes stride it, a fixed butterfly reduces), cosine
+// = dot / (|p| |c|), 0 for a zero norm; then the top-1 by (cosine desc,
+// index asc) over the whole workgroup.
+__global__ __launch_bounds__(256) void chunk_select_kernel(ChunkSelectParams p) {
+  __shared__ Best wbest[4];
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const float* pr = p.prompt + (size_t)b * p.E;
+  double pn = 0.0;
+  for (int e = lane; e < p.E; e += 64) pn = fma((double)pr[e], (double)pr[e], pn);
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) pn += __shfl_xor(pn, m);
+  Best best{-DBL_MAX, INT32_MAX};
+  for (int c = wave; c < p.M; c += 4) {
+    const float* cr = p.chunks + ((size_t)b * p.M + c) * p.E;
+    double dot = 0.0, cn = 0.0;
+    for (int e = lane; e < p.E; e += 64) {
+      const double x = (double)cr[e];
+      dot = fma(x, (double)pr[e], dot);
+      cn = fma(x, x, cn);
+    }
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+      dot += __shfl_xor(dot, m);
+      cn += __shfl_xor(cn, m);
+    }
+    const double den = sqrt(cn) * sqrt(pn);
+    const Best cand{den > 0.0 ? dot / den : 0.0, c};
+    if (best.i == INT32_MAX || before(cand, best)) best = cand;
+  }
+  if (lane == 0) wbest[wave] = best;
+  __syncthreads();
+  if (tid == 0) {
+    Best bb = wbest[0];
+    for (int w = 1; w < 4; ++w)
+      if (wbest[w].i < p.M && (bb.i >= p.M || before(wbest[w], bb))) bb = wbest[w];
+    const int m = bb.i < p.M ? bb.i : 0;
+    const int32_t* cf = p.chunk_first + (size_t)b * (p.M + 1);
+    const int lo = clampi(cf[m], 0, p.n_cand);
+    p.cand_range[2 * b] = lo;
+    p.cand_range[2 * b + 1] = clampi(cf[m + 1], lo, p.n_cand);
+    if (p.chunk_out) p.chunk_out[b] = m;
+    if (p.chunk_score) p.chunk_score[b] = bb.i < p.M ? bb.s : 0.0;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_chunk_select(int B, const ChunkSelectParams& p, hipStream_t s) {
+  chunk_select_kernel<<<B, 256, 0, s>>>(p);
+  return hipGetLastError();
+}
 
 hipError_t launch_qsum(int dtype, int B, const QsumParams& qp, hipStream_t s) {
   const dim3 g1(qp.n_split, B);

@@ -78,6 +78,15 @@ def lib():
                                         c_i32, c_i32, c_vp, c_i32, ctypes.c_double,
                                         ctypes.c_double, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz,
                                         c_vp]
+    L.hsa_retrieval_workspace_size.restype = c_sz
+    L.hsa_retrieval_workspace_size.argtypes = [P(HsaConfig), c_i32, c_i32, c_i32]
+    L.hsa_chunk_select.restype = ctypes.c_int
+    L.hsa_chunk_select.argtypes = [P(HsaConfig), c_vp, c_vp, c_i32, c_i32, c_vp, c_i32, c_vp, c_vp,
+                                   c_vp, c_vp]
+    L.hsa_forward_retrieval.restype = ctypes.c_int
+    L.hsa_forward_retrieval.argtypes = [P(HsaConfig), c_vp, c_i32, P(HsaKvPool), c_vp, c_vp, c_i32,
+                                        c_i32, c_vp, c_i32, c_i32, c_vp, c_i32, c_vp, c_vp, c_vp,
+                                        c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]
     L.hsa_block_count.restype = c_i32
     L.hsa_block_count.argtypes = [P(HsaConfig), c_i32, c_i32]
     c_f64 = ctypes.c_double
@@ -342,4 +351,37 @@ def hsa_forward_linformer(cfg, q, n_q, pool, ck, cv, rank, n_cand, n_cur_pages, 
                                      0 if ws is None else ws.numel(), _stream(stream))
     if check:
         _check("hsa_forward_linformer", st)
+    return st
+
+
+def hsa_retrieval_workspace_size(cfg: HsaConfig, n_q: int, k_max: int, n_cur_pages: int) -> int:
+    return lib().hsa_retrieval_workspace_size(ctypes.byref(cfg), n_q, k_max, n_cur_pages)
+
+
+def hsa_chunk_select(cfg, prompt_emb, chunk_emb, emb_dim, n_chunks, chunk_first, n_cand,
+                     cand_range, chunk_out=None, chunk_score=None, stream=None,
+                     check=True) -> int:
+    st = lib().hsa_chunk_select(ctypes.byref(cfg), _ptr(prompt_emb), _ptr(chunk_emb), emb_dim,
+                                n_chunks, _ptr(chunk_first), n_cand, _ptr(chunk_out),
+                                _ptr(chunk_score), _ptr(cand_range), _stream(stream))
+    if check:
+        _check("hsa_chunk_select", st)
+    return st
+
+
+def hsa_forward_retrieval(cfg, q, n_q, pool, prompt_emb, chunk_emb, emb_dim, n_chunks,
+                          chunk_first, n_cand, n_cur_pages, k_h, k_max, kv_state, k_state,
+                          page_kmean, g_lin, g_sp, o, chunk_out=None, sel_out=None, ws=None,
+                          stream=None, check=True) -> int:
+    if ws is None:
+        ws = _workspace(hsa_retrieval_workspace_size(cfg, n_q, k_max, n_cur_pages), q.device)
+    _keep, kp = _budgets(k_h)
+    st = lib().hsa_forward_retrieval(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool),
+                                     _ptr(prompt_emb), _ptr(chunk_emb), emb_dim, n_chunks,
+                                     _ptr(chunk_first), n_cand, n_cur_pages, kp, k_max,
+                                     _ptr(kv_state), _ptr(k_state), _ptr(page_kmean), _ptr(g_lin),
+                                     _ptr(g_sp), _ptr(o), _ptr(chunk_out), _ptr(sel_out), _ptr(ws),
+                                     0 if ws is None else ws.numel(), _stream(stream))
+    if check:
+        _check("hsa_forward_retrieval", st)
     return st

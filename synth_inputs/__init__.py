@@ -13,5 +13,6 @@ from .gen import (  # noqa: F401
     make_case,
     make_case_torch,
     make_projections,
+    make_prompts,
     seed_int,
 )

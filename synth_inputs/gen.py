@@ -22,7 +22,7 @@ import numpy as np
 from .configs import Workload
 
 # tensor ids inside a (seed, layer, chunk) stream family
-T_Q, T_K, T_V, T_PERM, T_GLIN, T_GSP, T_CENTROIDS, T_ASSIGN, T_EK, T_EV = range(10)
+T_Q, T_K, T_V, T_PERM, T_GLIN, T_GSP, T_CENTROIDS, T_ASSIGN, T_EK, T_EV, T_PROMPT = range(11)
 
 
 def _ss(wl: Workload, layer: int, chunk: int, tid: int) -> np.random.SeedSequence:
@@ -231,3 +231,41 @@ def make_projections(wl: Workload, rank: int, kind: str = "gaussian", layer: int
     else:
         raise ValueError(kind)
     return _round(wl, e_k), _round(wl, e_v)
+
+
+def make_prompts(wl: Workload, emb_dim: int = 4096, layer: int = 0, chunk: int = 0):
+    """Prompt embeddings of the KV bank's chunks and of the current chunk.
+
+    Chunks are runs of consecutive history pages: the clustered workload's
+    runs of 10 pages (one prompt per run), otherwise generation chunks of
+    n_cur pages. Each cluster (or chunk) gets a seeded N(0,1) direction; a
+    chunk's embedding is its direction plus N(0, 0.3^2) noise, and the
+    current prompt is the direction of the current chunk's cluster (the
+    clustered workload) or of a random chunk, plus noise.
+    Returns (prompt_emb [B, E], chunk_emb [B, M, E], chunk_first [B, M+1]
+    int32) as float32 / int32 arrays.
+    """
+    B = wl.batch
+    rng = np.random.default_rng(_ss(wl, layer, chunk, T_PROMPT))
+    if wl.structure == "clusters":
+        run = 10
+        _, c_star, page_cluster = _cluster_layout(wl, layer, chunk)
+        first = list(range(0, wl.n_cand, run)) + [wl.n_cand]
+        labels = [int(page_cluster[f]) for f in first[:-1]]
+        target = c_star
+        n_dir = 32
+    else:
+        run = max(1, wl.n_cur)
+        first = list(range(0, wl.n_cand, run)) + [wl.n_cand]
+        labels = list(range(len(first) - 1))
+        n_dir = max(1, len(labels))
+        target = int(rng.integers(n_dir))
+    dirs = rng.standard_normal((n_dir, emb_dim)).astype(np.float32)
+    M = len(labels)
+    chunk_emb = np.empty((B, M, emb_dim), np.float32)
+    prompt = np.empty((B, emb_dim), np.float32)
+    for b in range(B):
+        chunk_emb[b] = dirs[labels] + np.float32(0.3) * rng.standard_normal((M, emb_dim), dtype=np.float32)
+        prompt[b] = dirs[target] + np.float32(0.3) * rng.standard_normal(emb_dim, dtype=np.float32)
+    chunk_first = np.tile(np.asarray(first, np.int32), (B, 1))
+    return prompt, chunk_emb, chunk_first
