@@ -350,6 +350,52 @@ hsa_status_t hsa_forward_retrieval(const hsa_config_t* cfg, const void* q, int32
                                    int32_t* sel_out, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * Host-managed tier of the KV cache (Sec. 3.2 "Cache hierarchy and
+ * dataflow": L1 = the device pool, L2 = pinned host memory). A tier owns the
+ * placement of logical pages: each page (b, p) lives in one of the pool's
+ * num_slots slots or in one of l2_slots host slots, and the tier keeps the
+ * device page table's entries of pages in the pool up to date. Pages leave
+ * the pool least recently used first, only when a slot is needed; the pages
+ * a fetch lists are brought back before anything that follows on the same
+ * stream. Kernels only touch pages in the pool, so a forward pass over
+ * fetched pages gives the same result as one with every page resident. The
+ * page index and the linear state cover a page from the moment it is folded
+ * (hsa_state_update right after writing it), whatever its tier later.
+ * A tier is not thread-safe; its calls run in order on the given stream.
+ */
+typedef struct hsa_tier hsa_tier_t;
+
+/* Creates a tier for pool (device k, v, page_table; num_slots L1 slots,
+ * max_pages logical pages per batch entry). host_k, host_v: pinned host
+ * memory of l2_slots slots in the pool layout ([l2_slots, H, P, d] and
+ * [l2_slots, H, d, P], cfg->dtype), owned by the caller. pool->k == NULL
+ * makes a plan-only tier that issues no copy (policy inspection). */
+hsa_status_t hsa_tier_create(const hsa_config_t* cfg, const hsa_kv_pool_t* pool, void* host_k,
+                             void* host_v, int32_t l2_slots, hsa_tier_t** tier);
+void hsa_tier_destroy(hsa_tier_t* tier);
+
+/* A pool slot for new logical page `page` of batch entry b (written next by
+ * the caller); if none is free, the least recently used page moves to L2.
+ * A tier holds at most num_slots + l2_slots - 1 pages (num_slots without L2):
+ * one host slot stays free so that a fetch can always swap. UNSUPPORTED
+ * beyond that. Sets the page-table entry. */
+hsa_status_t hsa_tier_place(hsa_tier_t* tier, int32_t b, int32_t page, int32_t* slot,
+                            void* stream);
+
+/* Brings every listed page into the pool: pages host int32 [B, n_per_batch]
+ * logical pages (entries < 0 ignored, e.g. a copy of sel plus the current
+ * pages); they become the most recently used. UNSUPPORTED if they do not fit
+ * in the pool at once. */
+hsa_status_t hsa_tier_fetch(hsa_tier_t* tier, const int32_t* pages, int32_t n_per_batch,
+                            void* stream);
+
+/* Where a page lives: its pool slot (>= 0), -(l2 slot + 2) in L2, -1 never placed. */
+int32_t hsa_tier_locate(const hsa_tier_t* tier, int32_t b, int32_t page);
+
+/* Pages moved to L2 and brought back so far. */
+void hsa_tier_counters(const hsa_tier_t* tier, int64_t* evictions, int64_t* fetches);
+
+/*
  * Linformer linear branch (Sec. 3.3 "Linear branch"; App. "Linear Branch"):
  * per head h, projections E_K^(h), E_V^(h) in R^{L x r} compress keys and
  * values along the sequence. The sequence is cut into segments of length L

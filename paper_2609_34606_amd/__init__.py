@@ -10,6 +10,7 @@ from .hsa import (  # noqa: F401
     HsaConfig,
     HsaError,
     HsaKvPool,
+    HsaTier,
     LibraryNotBuilt,
     TAU_MAX,
     TAU_MIN,

@@ -87,6 +87,18 @@ def lib():
     L.hsa_forward_retrieval.argtypes = [P(HsaConfig), c_vp, c_i32, P(HsaKvPool), c_vp, c_vp, c_i32,
                                         c_i32, c_vp, c_i32, c_i32, c_vp, c_i32, c_vp, c_vp, c_vp,
                                         c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]
+    L.hsa_tier_create.restype = ctypes.c_int
+    L.hsa_tier_create.argtypes = [P(HsaConfig), P(HsaKvPool), c_vp, c_vp, c_i32, P(c_vp)]
+    L.hsa_tier_destroy.restype = None
+    L.hsa_tier_destroy.argtypes = [c_vp]
+    L.hsa_tier_place.restype = ctypes.c_int
+    L.hsa_tier_place.argtypes = [c_vp, c_i32, c_i32, P(c_i32), c_vp]
+    L.hsa_tier_fetch.restype = ctypes.c_int
+    L.hsa_tier_fetch.argtypes = [c_vp, c_vp, c_i32, c_vp]
+    L.hsa_tier_locate.restype = c_i32
+    L.hsa_tier_locate.argtypes = [c_vp, c_i32, c_i32]
+    L.hsa_tier_counters.restype = None
+    L.hsa_tier_counters.argtypes = [c_vp, P(ctypes.c_int64), P(ctypes.c_int64)]
     L.hsa_block_count.restype = c_i32
     L.hsa_block_count.argtypes = [P(HsaConfig), c_i32, c_i32]
     c_f64 = ctypes.c_double
@@ -385,3 +397,57 @@ def hsa_forward_retrieval(cfg, q, n_q, pool, prompt_emb, chunk_emb, emb_dim, n_c
     if check:
         _check("hsa_forward_retrieval", st)
     return st
+
+
+class HsaTier:
+    """Host-managed tier of a layer's KV pool (include/hsa.h, hsa_tier_*):
+    logical pages live in the pool's slots or in pinned host slots.
+    ``pool`` None makes a plan-only tier (bookkeeping without copies)."""
+
+    def __init__(self, cfg: HsaConfig, pool: Optional[HsaKvPool], l2_slots: int, host_k=None,
+                 host_v=None, num_slots: int = 0, max_pages: int = 0):
+        if pool is None:
+            pool = HsaKvPool(None, None, None, num_slots, max_pages)
+        self._keep = (cfg, pool, host_k, host_v)
+        h = c_vp()
+        _check("hsa_tier_create", lib().hsa_tier_create(ctypes.byref(cfg), ctypes.byref(pool),
+                                                         _ptr(host_k), _ptr(host_v), l2_slots,
+                                                         ctypes.byref(h)))
+        self._h = h
+
+    def close(self):
+        if self._h:
+            lib().hsa_tier_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def place(self, b: int, page: int, stream=None, check=True):
+        slot = c_i32(-1)
+        st = lib().hsa_tier_place(self._h, b, page, ctypes.byref(slot),
+                                  None if self._keep[1].k is None else _stream(stream))
+        if check:
+            _check("hsa_tier_place", st)
+            return slot.value
+        return st, slot.value
+
+    def fetch(self, pages, stream=None, check=True) -> int:
+        arr = np.ascontiguousarray(np.asarray(pages, dtype=np.int32))
+        n = arr.shape[-1] if arr.ndim else 0
+        st = lib().hsa_tier_fetch(self._h, arr.ctypes.data_as(c_vp), n,
+                                  None if self._keep[1].k is None else _stream(stream))
+        if check:
+            _check("hsa_tier_fetch", st)
+        return st
+
+    def locate(self, b: int, page: int) -> int:
+        return lib().hsa_tier_locate(self._h, b, page)
+
+    def counters(self):
+        e, f = ctypes.c_int64(0), ctypes.c_int64(0)
+        lib().hsa_tier_counters(self._h, ctypes.byref(e), ctypes.byref(f))
+        return e.value, f.value

@@ -130,3 +130,31 @@ def test_adaptive_entry_points_validate_before_launch():
     # workspace too small
     assert lib.hsa_sparse_attn_adaptive(by(cfg), fake, 64, by(pool), fake, 4, khp, 10, 3, 0.35,
                                         1.0, fake, None, fake, 1024, None) == 4
+
+
+def test_tier_policy_plan_only():
+    # 4 pool slots, 6 host slots, 10 logical pages: pages leave the pool least
+    # recently used first; a fetch brings listed pages back and pins them
+    cfg = P.config(1, 2, 64, 256, "bf16")
+    t = P.HsaTier(cfg, None, 6, num_slots=4, max_pages=10)
+    slots = [t.place(0, p) for p in range(4)]
+    assert sorted(slots) == [0, 1, 2, 3] and t.counters() == (0, 0)
+    assert t.place(0, 4) == slots[0] and t.locate(0, 0) == -2     # page 0 -> host slot 0
+    assert t.place(0, 5) == slots[1] and t.locate(0, 1) == -3
+    t.fetch([[0, 2]])                  # 0 comes back into the LRU slot (page 3's); 2 is pinned
+    assert t.locate(0, 0) >= 0 and t.locate(0, 2) >= 0 and t.locate(0, 3) < -1
+    assert t.counters() == (3, 1)
+    t.place(0, 6)                      # LRU among 4, 5, 0, 2: page 4
+    assert t.locate(0, 4) < -1
+    # more pages listed than the pool holds
+    assert t.fetch([[0, 1, 2, 3, 5]], check=False) == 2
+    # a page never placed, a page out of range
+    assert t.fetch([[9]], check=False) == 1 and t.fetch([[10]], check=False) == 3
+    assert t.place(0, 6, check=False)[0] == 1                       # placed twice
+    # capacity: pool + host slots - 1 (one host slot stays free for swaps)
+    t2 = P.HsaTier(cfg, None, 2, num_slots=2, max_pages=10)
+    t2.place(0, 0), t2.place(0, 1), t2.place(0, 2)
+    assert t2.place(0, 3, check=False)[0] == 2
+    t2.fetch([[0, 1]])                 # both back in the pool through the spare slot
+    assert t2.locate(0, 0) >= 0 and t2.locate(0, 1) >= 0 and t2.locate(0, 2) < -1
+    t.close(), t2.close()
