@@ -187,6 +187,8 @@ def bench_single(args, wl):
         res["adaptive"] = bench_adaptive(args, wl, layer, q, k_h, k_max, sel)
         if wl.dtype == "bf16":
             res["linformer"] = bench_linformer(args, wl, layer, q, k_h, k_max, sel)
+        res["retrieval"] = bench_retrieval(args, wl, layer, q, k_h, k_max)
+        res["tier"] = bench_tier(args, wl, dev)
     if not args.no_cpu_baseline:
         heads = list(range(wl.heads)) if wl.heads * wl.n_pages <= 12 * 24 else [0, 1]
         log("timing the oracle on the host ...")
@@ -347,6 +349,74 @@ def bench_linformer(args, wl, layer, q, k_h, k_max, sel, rank=64):
                             "frac": round(fb / (ms_br * 1e-3) / 1e12 / peak, 4),
                             "flops_per_launch": fb},
     }
+
+
+def bench_retrieval(args, wl, layer, q, k_h, k_max):
+    """Stage-1 prompt-level retrieval (cosine top-1 over the chunks' prompt
+    embeddings, 4096-dim) alone and in front of the forward pass."""
+    import torch
+    from paper_2609_34606_amd import hsa_chunk_select, hsa_forward_retrieval
+    from paper_2609_34606_amd import hsa_retrieval_workspace_size
+    from synth_inputs import make_prompts
+    pe, ce, cf = make_prompts(wl)
+    t = lambda a: torch.from_numpy(a).to(q.device)
+    pe, ce, cf = t(pe), t(ce), t(cf)
+    M, E = ce.shape[1], ce.shape[2]
+    rng = torch.empty((wl.batch, 2), dtype=torch.int32, device=q.device)
+    ms_s1 = time_loop(lambda: hsa_chunk_select(layer.cfg, pe, ce, E, M, cf, wl.n_cand, rng),
+                      args.steps, torch)
+    out = torch.empty_like(q)
+    ws = layer.workspace("retrieval", hsa_retrieval_workspace_size(layer.cfg, wl.n_q, k_max, wl.n_cur))
+    ms_fwd = time_loop(lambda: hsa_forward_retrieval(
+        layer.cfg, q, wl.n_q, layer.pool, pe, ce, E, M, cf, wl.n_cand, wl.n_cur, k_h, k_max,
+        layer.kv_state, layer.k_state, layer.page_kmean, None, None, out, ws=ws), args.steps, torch)
+    return {"chunks": M, "emb_dim": E, "pages_per_chunk": int(cf[0, 1] - cf[0, 0]),
+            "phases_ms": {"stage1_chunk_select": round(ms_s1, 4),
+                          "forward_retrieval": round(ms_fwd, 4)}}
+
+
+def bench_tier(args, wl, dev, n_slots=8, n_set=6):
+    """Host-managed tier: a pool of n_slots slots over the workload's pages
+    (the rest in pinned host memory); each timed fetch brings n_set pages
+    back from host memory and moves as many out, alternating two disjoint
+    sets. Reports the host<->device traffic per fetch and its rate."""
+    import numpy as np
+    import torch
+    from paper_2609_34606_amd import HsaLayer, HsaTier
+    H, d, P = wl.heads, wl.head_dim, wl.page_size
+    npg = min(wl.n_pages, 2 * n_set + n_slots)
+    dt = dev["q"].dtype
+    pool_k = torch.empty((n_slots, H, P, d), dtype=dt, device=dev["q"].device)
+    pool_v = torch.empty((n_slots, H, d, P), dtype=dt, device=dev["q"].device)
+    table = torch.full((wl.batch, npg), -1, dtype=torch.int32, device=dev["q"].device)
+    l2 = npg - n_slots + 1
+    host_k = torch.empty((l2, H, P, d), dtype=dt, pin_memory=True)
+    host_v = torch.empty((l2, H, d, P), dtype=dt, pin_memory=True)
+    layer = HsaLayer(wl.batch, H, d, P, dt, dev["q"].device, k_pool=pool_k, v_pool=pool_v,
+                     page_table=table)
+    tier = HsaTier(layer.cfg, layer.pool, l2, host_k, host_v)
+    for p in range(npg):
+        slot = tier.place(0, p)
+        pool_k[slot] = dev["k_pool"][int(dev["page_table"][0, p])]
+        pool_v[slot] = dev["v_pool"][int(dev["page_table"][0, p])]
+    sets = [np.arange(0, n_set, dtype=np.int32)[None], np.arange(n_set, 2 * n_set, dtype=np.int32)[None]]
+    tier.fetch(sets[1])
+    torch.cuda.synchronize()
+    e0, f0 = tier.counters()
+    iters = max(4, args.steps // 2)
+    t0 = time.perf_counter()
+    for i in range(iters):
+        tier.fetch(sets[i % 2])
+        torch.cuda.synchronize()
+    dt_s = (time.perf_counter() - t0) / iters
+    e1, f1 = tier.counters()
+    moved = ((e1 - e0) + (f1 - f0)) / iters
+    page_bytes = 2 * H * P * d * (2 if wl.dtype == "bf16" else 4)
+    tier.close()
+    return {"pool_slots": n_slots, "host_slots": l2, "pages_per_fetch": n_set,
+            "pages_moved_per_fetch": moved, "ms_per_fetch": round(dt_s * 1e3, 3),
+            "host_device_gbs": round(moved * page_bytes / dt_s / 1e9, 1),
+            "note": "each page moved is one key block and one value block of every head"}
 
 
 def bench_streaming(args, wl):

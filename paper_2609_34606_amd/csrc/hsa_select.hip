@@ -218,42 +218,54 @@ __global__ __launch_bounds__(256) void select_kernel(SelectParams p) {
   }
 }
 
-// Stage-1 prompt-level retrieval (Sec. 3.2): one workgroup per batch entry.
-// Each wave takes every fourth chunk: fp64 dot product and norm over the
-// embedding dimension (lanes stride it, a fixed butterfly reduces), cosine
-// = dot / (|p| |c|), 0 for a zero norm; then the top-1 by (cosine desc,
-// index asc) over the whole workgroup.
-__global__ __launch_bounds__(256) void chunk_select_kernel(ChunkSelectParams p) {
-  __shared__ Best wbest[4];
+// Stage-1 prompt-level retrieval (Sec. 3.2): one workgroup of 16 waves per
+// batch entry. Each wave takes every sixteenth chunk: fp64 dot product and
+// norm over the embedding dimension (each lane keeps four partial sums over
+// its strided elements, added in a fixed order, then a fixed butterfly
+// across the wave), cosine = dot / (|p| |c|), 0 for a zero norm; then the
+// top-1 by (cosine desc, index asc) over the workgroup.
+constexpr int kChunkWaves = 16;
+
+__global__ __launch_bounds__(64 * kChunkWaves) void chunk_select_kernel(ChunkSelectParams p) {
+  __shared__ Best wbest[kChunkWaves];
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float* pr = p.prompt + (size_t)b * p.E;
-  double pn = 0.0;
-  for (int e = lane; e < p.E; e += 64) pn = fma((double)pr[e], (double)pr[e], pn);
+  auto wave_sum = [](double v) {
 #pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) pn += __shfl_xor(pn, m);
+    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
+    return v;
+  };
+  double pa[4] = {0, 0, 0, 0};
+  for (int e = lane; e < p.E; e += 256)
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (e + 64 * u < p.E) pa[u] = fma((double)pr[e + 64 * u], (double)pr[e + 64 * u], pa[u]);
+  const double pn = wave_sum((pa[0] + pa[1]) + (pa[2] + pa[3]));
   Best best{-DBL_MAX, INT32_MAX};
-  for (int c = wave; c < p.M; c += 4) {
+  for (int c = wave; c < p.M; c += kChunkWaves) {
     const float* cr = p.chunks + ((size_t)b * p.M + c) * p.E;
-    double dot = 0.0, cn = 0.0;
-    for (int e = lane; e < p.E; e += 64) {
-      const double x = (double)cr[e];
-      dot = fma(x, (double)pr[e], dot);
-      cn = fma(x, x, cn);
-    }
+    double dot[4] = {0, 0, 0, 0}, cn[4] = {0, 0, 0, 0};
+    for (int e = lane; e < p.E; e += 256)
 #pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-      dot += __shfl_xor(dot, m);
-      cn += __shfl_xor(cn, m);
-    }
-    const double den = sqrt(cn) * sqrt(pn);
-    const Best cand{den > 0.0 ? dot / den : 0.0, c};
+      for (int u = 0; u < 4; ++u) {
+        const int i = e + 64 * u;
+        if (i < p.E) {
+          const double x = (double)cr[i];
+          dot[u] = fma(x, (double)pr[i], dot[u]);
+          cn[u] = fma(x, x, cn[u]);
+        }
+      }
+    const double dt = wave_sum((dot[0] + dot[1]) + (dot[2] + dot[3]));
+    const double cc = wave_sum((cn[0] + cn[1]) + (cn[2] + cn[3]));
+    const double den = sqrt(cc) * sqrt(pn);
+    const Best cand{den > 0.0 ? dt / den : 0.0, c};
     if (best.i == INT32_MAX || before(cand, best)) best = cand;
   }
   if (lane == 0) wbest[wave] = best;
   __syncthreads();
   if (tid == 0) {
     Best bb = wbest[0];
-    for (int w = 1; w < 4; ++w)
+    for (int w = 1; w < kChunkWaves; ++w)
       if (wbest[w].i < p.M && (bb.i >= p.M || before(wbest[w], bb))) bb = wbest[w];
     const int m = bb.i < p.M ? bb.i : 0;
     const int32_t* cf = p.chunk_first + (size_t)b * (p.M + 1);
@@ -268,7 +280,7 @@ __global__ __launch_bounds__(256) void chunk_select_kernel(ChunkSelectParams p) 
 }  // namespace
 
 hipError_t launch_chunk_select(int B, const ChunkSelectParams& p, hipStream_t s) {
-  chunk_select_kernel<<<B, 256, 0, s>>>(p);
+  chunk_select_kernel<<<B, 64 * kChunkWaves, 0, s>>>(p);
   return hipGetLastError();
 }
 
