@@ -188,7 +188,7 @@ def bench_single(args, wl):
         if wl.dtype == "bf16":
             res["linformer"] = bench_linformer(args, wl, layer, q, k_h, k_max, sel)
         res["retrieval"] = bench_retrieval(args, wl, layer, q, k_h, k_max)
-        res["tier"] = bench_tier(args, wl, dev)
+        res["tier"] = bench_tier(args, wl, dev, layer, q, k_h, k_max, sel)
     if not args.no_cpu_baseline:
         heads = list(range(wl.heads)) if wl.heads * wl.n_pages <= 12 * 24 else [0, 1]
         log("timing the oracle on the host ...")
@@ -375,48 +375,110 @@ def bench_retrieval(args, wl, layer, q, k_h, k_max):
                           "forward_retrieval": round(ms_fwd, 4)}}
 
 
-def bench_tier(args, wl, dev, n_slots=8, n_set=6):
-    """Host-managed tier: a pool of n_slots slots over the workload's pages
-    (the rest in pinned host memory); each timed fetch brings n_set pages
-    back from host memory and moves as many out, alternating two disjoint
-    sets. Reports the host<->device traffic per fetch and its rate."""
+def bench_tier(args, wl, dev, main_layer, q, k_h, k_max, sel, n_slots=8, n_set=6):
+    """Host-managed tiers on a second pool of n_slots slots over the
+    workload's pages (the rest in pinned host memory, or two host slots and a
+    file under the system's temporary directory). Each timed fetch brings
+    n_set pages back into the pool and moves as many out, alternating two
+    disjoint sets. Reports the pages moved per fetch, the time and the
+    host<->device rate; and, for the prefetch, the time of a prefetch of
+    n_set pages on a side stream alone, of the main layer's attention
+    launches alone, and of the two issued together (the overlap of copies
+    with compute, as when one layer's pages move while another computes)."""
+    import tempfile
+
     import numpy as np
     import torch
     from paper_2609_34606_amd import HsaLayer, HsaTier
     H, d, P = wl.heads, wl.head_dim, wl.page_size
     npg = min(wl.n_pages, 2 * n_set + n_slots)
     dt = dev["q"].dtype
-    pool_k = torch.empty((n_slots, H, P, d), dtype=dt, device=dev["q"].device)
-    pool_v = torch.empty((n_slots, H, d, P), dtype=dt, device=dev["q"].device)
-    table = torch.full((wl.batch, npg), -1, dtype=torch.int32, device=dev["q"].device)
-    l2 = npg - n_slots + 1
-    host_k = torch.empty((l2, H, P, d), dtype=dt, pin_memory=True)
-    host_v = torch.empty((l2, H, d, P), dtype=dt, pin_memory=True)
-    layer = HsaLayer(wl.batch, H, d, P, dt, dev["q"].device, k_pool=pool_k, v_pool=pool_v,
-                     page_table=table)
-    tier = HsaTier(layer.cfg, layer.pool, l2, host_k, host_v)
-    for p in range(npg):
-        slot = tier.place(0, p)
-        pool_k[slot] = dev["k_pool"][int(dev["page_table"][0, p])]
-        pool_v[slot] = dev["v_pool"][int(dev["page_table"][0, p])]
-    sets = [np.arange(0, n_set, dtype=np.int32)[None], np.arange(n_set, 2 * n_set, dtype=np.int32)[None]]
-    tier.fetch(sets[1])
-    torch.cuda.synchronize()
-    e0, f0 = tier.counters()
-    iters = max(4, args.steps // 2)
-    t0 = time.perf_counter()
-    for i in range(iters):
-        tier.fetch(sets[i % 2])
-        torch.cuda.synchronize()
-    dt_s = (time.perf_counter() - t0) / iters
-    e1, f1 = tier.counters()
-    moved = ((e1 - e0) + (f1 - f0)) / iters
+    cuda = dev["q"].device
     page_bytes = 2 * H * P * d * (2 if wl.dtype == "bf16" else 4)
-    tier.close()
-    return {"pool_slots": n_slots, "host_slots": l2, "pages_per_fetch": n_set,
-            "pages_moved_per_fetch": moved, "ms_per_fetch": round(dt_s * 1e3, 3),
-            "host_device_gbs": round(moved * page_bytes / dt_s / 1e9, 1),
-            "note": "each page moved is one key block and one value block of every head"}
+    pool_k = torch.empty((n_slots, H, P, d), dtype=dt, device=cuda)
+    pool_v = torch.empty((n_slots, H, d, P), dtype=dt, device=cuda)
+    table = torch.full((wl.batch, npg), -1, dtype=torch.int32, device=cuda)
+    layer = HsaLayer(wl.batch, H, d, P, dt, cuda, k_pool=pool_k, v_pool=pool_v, page_table=table)
+    sets = [np.arange(0, n_set, dtype=np.int32)[None], np.arange(n_set, 2 * n_set, dtype=np.int32)[None]]
+    iters = max(10, args.steps)
+
+    def make(l2, l3, tmp):
+        host_k = torch.empty((l2, H, P, d), dtype=dt, pin_memory=True)
+        host_v = torch.empty((l2, H, d, P), dtype=dt, pin_memory=True)
+        tier = HsaTier(layer.cfg, layer.pool, l2, host_k, host_v, l3_dir=tmp if l3 else None,
+                       l3_slots=l3)
+        for p in range(npg):
+            slot = tier.place(0, p)
+            pool_k[slot] = dev["k_pool"][int(dev["page_table"][0, p])]
+            pool_v[slot] = dev["v_pool"][int(dev["page_table"][0, p])]
+        tier.fetch(sets[1])
+        torch.cuda.synchronize()
+        return tier, (host_k, host_v)
+
+    def cycle(tier):
+        s0 = tier.stats()
+        t0 = time.perf_counter()
+        for i in range(iters):
+            tier.fetch(sets[i % 2])
+            torch.cuda.synchronize()
+        dt_s = (time.perf_counter() - t0) / iters
+        s1 = tier.stats()
+        moved = {k: (s1[k] - s0[k]) / iters for k in s1}
+        per = moved["evictions"] + moved["fetches"]
+        return {"pages_moved_per_fetch": per, "pages_to_file_per_fetch": moved["spills"],
+                "pages_from_file_per_fetch": moved["reloads"], "ms_per_fetch": round(dt_s * 1e3, 3),
+                "host_device_gbs": round(per * page_bytes / dt_s / 1e9, 1)}
+
+    res = {"pool_slots": n_slots, "pages": npg, "pages_per_fetch": n_set,
+           "page_bytes": page_bytes,
+           "note": "a page moved is one key block and one value block of every head"}
+    # the link itself: one pinned copy of n_set pages' bytes each way
+    hbuf = torch.empty(n_set * page_bytes, dtype=torch.uint8, pin_memory=True)
+    dbuf = torch.empty(n_set * page_bytes, dtype=torch.uint8, device=cuda)
+    ms_h2d = time_loop(lambda: dbuf.copy_(hbuf, non_blocking=True), iters, torch)
+    ms_d2h = time_loop(lambda: hbuf.copy_(dbuf, non_blocking=True), iters, torch)
+    res["link_gbs"] = {"h2d": round(n_set * page_bytes / ms_h2d / 1e6, 1),
+                       "d2h": round(n_set * page_bytes / ms_d2h / 1e6, 1)}
+    del hbuf, dbuf
+    with tempfile.TemporaryDirectory() as tmp:
+        tier, keep = make(npg - n_slots + 1, 0, tmp)
+        res["host_tier"] = dict(host_slots=npg - n_slots + 1, **cycle(tier))
+        # prefetch beside the attention: forwards on the compute stream, the
+        # prefetch of the other set on a side stream (an empty fetch first, so
+        # that no page is held)
+        side = torch.cuda.Stream()
+        n_fwd = 6
+        out = torch.empty_like(q)
+
+        def forwards():
+            for _ in range(n_fwd):
+                main_layer.forward_selected(q, sel, wl.n_cand, wl.n_cur, k_h, k_max=k_max, out=out)
+
+        def timed(fn):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for i in range(iters):
+                fn(i)
+                torch.cuda.synchronize()
+            return (time.perf_counter() - t0) / iters * 1e3
+
+        empty = np.zeros((1, 0), np.int32)
+        ms_f = timed(lambda i: forwards())
+        ms_p = timed(lambda i: (tier.fetch(empty), tier.prefetch(sets[i % 2], stream=side)))
+        ms_b = timed(lambda i: (tier.fetch(empty), forwards(), tier.prefetch(sets[i % 2], stream=side)))
+        res["prefetch_overlap"] = {
+            "attention_launches": n_fwd, "ms_attention": round(ms_f, 3),
+            "ms_prefetch": round(ms_p, 3), "ms_together": round(ms_b, 3),
+            "together_over_longer": round(ms_b / max(ms_f, ms_p), 3),
+            "together_over_sum": round(ms_b / (ms_f + ms_p), 3)}
+        tier.close()
+        del keep
+        n_l2 = 2
+        tier, keep = make(n_l2, npg - n_slots - n_l2 + 1, tmp)
+        res["file_tier"] = dict(host_slots=n_l2, file_slots=npg - n_slots - n_l2 + 1,
+                                file_dir=tmp.rsplit("/", 1)[0], **cycle(tier))
+        tier.close()
+    return res
 
 
 def bench_streaming(args, wl):

@@ -74,7 +74,8 @@ typedef enum hsa_status {
   HSA_ERR_UNSUPPORTED = 2, /* valid but not implemented: d, P, H, sizes  */
   HSA_ERR_OUT_OF_RANGE = 3, /* page outside the pool / page table         */
   HSA_ERR_WORKSPACE = 4,   /* workspace NULL or smaller than required    */
-  HSA_ERR_DEVICE = 5       /* a HIP call failed                          */
+  HSA_ERR_DEVICE = 5,      /* a HIP call failed                          */
+  HSA_ERR_IO = 6           /* a file read or write of the host tier failed */
 } hsa_status_t;
 
 typedef enum hsa_dtype { HSA_DTYPE_BF16 = 0, HSA_DTYPE_F32 = 1 } hsa_dtype_t;
@@ -350,50 +351,89 @@ hsa_status_t hsa_forward_retrieval(const hsa_config_t* cfg, const void* q, int32
                                    int32_t* sel_out, void* ws, size_t ws_bytes, void* stream);
 
 /*
- * Host-managed tier of the KV cache (Sec. 3.2 "Cache hierarchy and
- * dataflow": L1 = the device pool, L2 = pinned host memory). A tier owns the
- * placement of logical pages: each page (b, p) lives in one of the pool's
- * num_slots slots or in one of l2_slots host slots, and the tier keeps the
- * device page table's entries of pages in the pool up to date. Pages leave
- * the pool least recently used first, only when a slot is needed; the pages
- * a fetch lists are brought back before anything that follows on the same
- * stream. Kernels only touch pages in the pool, so a forward pass over
- * fetched pages gives the same result as one with every page resident. The
- * page index and the linear state cover a page from the moment it is folded
- * (hsa_state_update right after writing it), whatever its tier later.
- * A tier is not thread-safe; its calls run in order on the given stream.
+ * Host-managed tiers of the KV cache (Sec. 3.2 "Cache hierarchy and
+ * dataflow"): L1 = the device pool, L2 = pinned host memory, L3 = a file on
+ * a local drive. A tier owns the placement of logical pages: each page
+ * (b, p) lives in one of the pool's num_slots slots, one of l2_slots host
+ * slots or one of l3_slots file slots, and the tier keeps the device page
+ * table's entries of pages in the pool up to date. A slot holds every head
+ * of a page. Pages leave the pool least recently used first, only when a slot
+ * is needed, and L2 spills to L3 the same way; the pages a fetch lists are in
+ * the pool before anything that follows on the same stream. Kernels only
+ * touch pages in the pool, so a forward pass over fetched pages gives the
+ * same result as one with every page resident. The page index and the linear
+ * state cover a page from the moment it is folded (hsa_state_update right
+ * after writing it), whatever its tier later.
+ *
+ * Streams: place, fetch and the kernels that read the pool go on one
+ * "compute" stream; a prefetch may go on another stream and then overlaps
+ * them. Host-to-device copies run on the calling stream, device-to-host
+ * copies on a stream of the tier's own (so the two directions overlap); the
+ * tier orders them with events and makes the calling stream wait for its
+ * own copies before returning. A move from L2 to L3 or from L3 waits on the
+ * host for the copies it depends on (so that call blocks). A tier is not
+ * thread-safe.
  */
 typedef struct hsa_tier hsa_tier_t;
 
+typedef struct hsa_tier_stats {
+  int64_t evictions;  /* pages moved L1 -> L2 */
+  int64_t fetches;    /* pages moved into L1 from L2 or L3 (prefetched ones included) */
+  int64_t spills;     /* pages moved L2 -> L3 */
+  int64_t reloads;    /* pages moved L3 -> L1 */
+  int64_t prefetched; /* pages moved into L1 by hsa_tier_prefetch */
+} hsa_tier_stats_t;
+
 /* Creates a tier for pool (device k, v, page_table; num_slots L1 slots,
- * max_pages logical pages per batch entry). host_k, host_v: pinned host
- * memory of l2_slots slots in the pool layout ([l2_slots, H, P, d] and
- * [l2_slots, H, d, P], cfg->dtype), owned by the caller. pool->k == NULL
- * makes a plan-only tier that issues no copy (policy inspection). */
+ * max_pages logical pages per batch entry) on the current device.
+ * host_k, host_v: pinned host memory of l2_slots slots in the pool layout
+ * ([l2_slots, H, P, d] and [l2_slots, H, d, P], cfg->dtype), owned by the
+ * caller. l3_dir: a directory on the drive where the tier keeps an unnamed
+ * file of l3_slots slots (gone when the tier is destroyed); l3_slots > 0
+ * needs l2_slots >= 1. The tier allocates two pinned staging pages for L3
+ * reads, an internal stream and its events. pool->k == NULL makes a
+ * plan-only tier that issues no copy and touches no file (policy
+ * inspection). HSA_ERR_IO if the file cannot be created. */
 hsa_status_t hsa_tier_create(const hsa_config_t* cfg, const hsa_kv_pool_t* pool, void* host_k,
-                             void* host_v, int32_t l2_slots, hsa_tier_t** tier);
+                             void* host_v, int32_t l2_slots, const char* l3_dir,
+                             int32_t l3_slots, hsa_tier_t** tier);
+
+/* Waits for the tier's own copies, then frees it. Call it once the kernels
+ * that read its pages have finished. */
 void hsa_tier_destroy(hsa_tier_t* tier);
 
 /* A pool slot for new logical page `page` of batch entry b (written next by
- * the caller); if none is free, the least recently used page moves to L2.
- * A tier holds at most num_slots + l2_slots - 1 pages (num_slots without L2):
- * one host slot stays free so that a fetch can always swap. UNSUPPORTED
- * beyond that. Sets the page-table entry. */
+ * the caller on the same stream); if none is free, the least recently used
+ * page moves down a tier. A tier holds at most
+ * num_slots + l2_slots + l3_slots - 1 pages (num_slots without lower tiers):
+ * one lower-tier slot stays free so that a fetch can always swap.
+ * UNSUPPORTED beyond that. Sets the page-table entry. */
 hsa_status_t hsa_tier_place(hsa_tier_t* tier, int32_t b, int32_t page, int32_t* slot,
                             void* stream);
 
 /* Brings every listed page into the pool: pages host int32 [B, n_per_batch]
  * logical pages (entries < 0 ignored, e.g. a copy of sel plus the current
- * pages); they become the most recently used. UNSUPPORTED if they do not fit
- * in the pool at once. */
+ * pages); they become the most recently used and are the pages a later
+ * prefetch leaves in place. Waits for the last prefetch first.
+ * UNSUPPORTED if they do not fit in the pool at once. */
 hsa_status_t hsa_tier_fetch(hsa_tier_t* tier, const int32_t* pages, int32_t n_per_batch,
                             void* stream);
 
-/* Where a page lives: its pool slot (>= 0), -(l2 slot + 2) in L2, -1 never placed. */
+/* As hsa_tier_fetch, on a side stream, for pages a later fetch is expected
+ * to list (e.g. the chunk Stage 1 will choose): the copies start once the
+ * compute stream has passed the last fetch and overlap the kernels that
+ * follow it there; no page the last fetch listed or placed since then
+ * moves. The next fetch waits for the prefetch. UNSUPPORTED if those pages
+ * and the listed ones do not fit in the pool together. */
+hsa_status_t hsa_tier_prefetch(hsa_tier_t* tier, const int32_t* pages, int32_t n_per_batch,
+                               void* stream);
+
+/* Where a page lives: its pool slot (>= 0), -(i + 2) in L2 slot i,
+ * -(l2_slots + i + 2) in L3 slot i, -1 never placed. */
 int32_t hsa_tier_locate(const hsa_tier_t* tier, int32_t b, int32_t page);
 
-/* Pages moved to L2 and brought back so far. */
-void hsa_tier_counters(const hsa_tier_t* tier, int64_t* evictions, int64_t* fetches);
+/* Pages moved between tiers so far. */
+void hsa_tier_stats(const hsa_tier_t* tier, hsa_tier_stats_t* stats);
 
 /*
  * Linformer linear branch (Sec. 3.3 "Linear branch"; App. "Linear Branch"):

@@ -436,6 +436,7 @@ const char* hsa_status_string(hsa_status_t s) {
     case HSA_ERR_OUT_OF_RANGE: return "HSA_ERR_OUT_OF_RANGE";
     case HSA_ERR_WORKSPACE: return "HSA_ERR_WORKSPACE";
     case HSA_ERR_DEVICE: return "HSA_ERR_DEVICE";
+    case HSA_ERR_IO: return "HSA_ERR_IO";
   }
   return "HSA_ERR_UNKNOWN";
 }

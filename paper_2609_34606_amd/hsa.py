@@ -18,7 +18,8 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib", "libh
 HSA_DTYPE_BF16 = 0
 HSA_DTYPE_F32 = 1
 STATUS = {0: "HSA_OK", 1: "HSA_ERR_INVALID_ARG", 2: "HSA_ERR_UNSUPPORTED",
-          3: "HSA_ERR_OUT_OF_RANGE", 4: "HSA_ERR_WORKSPACE", 5: "HSA_ERR_DEVICE"}
+          3: "HSA_ERR_OUT_OF_RANGE", 4: "HSA_ERR_WORKSPACE", 5: "HSA_ERR_DEVICE",
+          6: "HSA_ERR_IO"}
 
 c_i32, c_vp, c_sz = ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t
 
@@ -26,6 +27,12 @@ c_i32, c_vp, c_sz = ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t
 class HsaConfig(ctypes.Structure):
     _fields_ = [("batch", c_i32), ("num_heads", c_i32), ("head_dim", c_i32),
                 ("page_size", c_i32), ("dtype", c_i32), ("sm_scale", ctypes.c_float)]
+
+
+class HsaTierStats(ctypes.Structure):
+    _fields_ = [("evictions", ctypes.c_int64), ("fetches", ctypes.c_int64),
+                ("spills", ctypes.c_int64), ("reloads", ctypes.c_int64),
+                ("prefetched", ctypes.c_int64)]
 
 
 class HsaKvPool(ctypes.Structure):
@@ -88,17 +95,20 @@ def lib():
                                         c_i32, c_vp, c_i32, c_i32, c_vp, c_i32, c_vp, c_vp, c_vp,
                                         c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]
     L.hsa_tier_create.restype = ctypes.c_int
-    L.hsa_tier_create.argtypes = [P(HsaConfig), P(HsaKvPool), c_vp, c_vp, c_i32, P(c_vp)]
+    L.hsa_tier_create.argtypes = [P(HsaConfig), P(HsaKvPool), c_vp, c_vp, c_i32, ctypes.c_char_p,
+                                  c_i32, P(c_vp)]
     L.hsa_tier_destroy.restype = None
     L.hsa_tier_destroy.argtypes = [c_vp]
     L.hsa_tier_place.restype = ctypes.c_int
     L.hsa_tier_place.argtypes = [c_vp, c_i32, c_i32, P(c_i32), c_vp]
     L.hsa_tier_fetch.restype = ctypes.c_int
     L.hsa_tier_fetch.argtypes = [c_vp, c_vp, c_i32, c_vp]
+    L.hsa_tier_prefetch.restype = ctypes.c_int
+    L.hsa_tier_prefetch.argtypes = [c_vp, c_vp, c_i32, c_vp]
     L.hsa_tier_locate.restype = c_i32
     L.hsa_tier_locate.argtypes = [c_vp, c_i32, c_i32]
-    L.hsa_tier_counters.restype = None
-    L.hsa_tier_counters.argtypes = [c_vp, P(ctypes.c_int64), P(ctypes.c_int64)]
+    L.hsa_tier_stats.restype = None
+    L.hsa_tier_stats.argtypes = [c_vp, P(HsaTierStats)]
     L.hsa_block_count.restype = c_i32
     L.hsa_block_count.argtypes = [P(HsaConfig), c_i32, c_i32]
     c_f64 = ctypes.c_double
@@ -145,8 +155,10 @@ def _ptr(t) -> Optional[int]:
 
 
 def _stream(stream) -> Optional[int]:
+    """A HIP stream handle: an int, a torch stream, or None for torch's
+    current stream."""
     if stream is not None:
-        return int(stream)
+        return int(getattr(stream, "cuda_stream", stream))
     import torch
     return torch.cuda.current_stream().cuda_stream
 
@@ -400,19 +412,21 @@ def hsa_forward_retrieval(cfg, q, n_q, pool, prompt_emb, chunk_emb, emb_dim, n_c
 
 
 class HsaTier:
-    """Host-managed tier of a layer's KV pool (include/hsa.h, hsa_tier_*):
-    logical pages live in the pool's slots or in pinned host slots.
-    ``pool`` None makes a plan-only tier (bookkeeping without copies)."""
+    """Host-managed tiers of a layer's KV pool (include/hsa.h, hsa_tier_*):
+    logical pages live in the pool's slots (L1), in pinned host slots (L2) or
+    in slots of an unnamed file under ``l3_dir`` (L3). ``pool`` None makes a
+    plan-only tier (bookkeeping without copies)."""
 
     def __init__(self, cfg: HsaConfig, pool: Optional[HsaKvPool], l2_slots: int, host_k=None,
-                 host_v=None, num_slots: int = 0, max_pages: int = 0):
+                 host_v=None, num_slots: int = 0, max_pages: int = 0, l3_dir: Optional[str] = None,
+                 l3_slots: int = 0):
         if pool is None:
             pool = HsaKvPool(None, None, None, num_slots, max_pages)
         self._keep = (cfg, pool, host_k, host_v)
         h = c_vp()
-        _check("hsa_tier_create", lib().hsa_tier_create(ctypes.byref(cfg), ctypes.byref(pool),
-                                                         _ptr(host_k), _ptr(host_v), l2_slots,
-                                                         ctypes.byref(h)))
+        _check("hsa_tier_create", lib().hsa_tier_create(
+            ctypes.byref(cfg), ctypes.byref(pool), _ptr(host_k), _ptr(host_v), l2_slots,
+            None if l3_dir is None else str(l3_dir).encode(), l3_slots, ctypes.byref(h)))
         self._h = h
 
     def close(self):
@@ -426,28 +440,40 @@ class HsaTier:
         except Exception:
             pass
 
+    def _stream(self, stream):
+        return None if self._keep[1].k is None else _stream(stream)
+
     def place(self, b: int, page: int, stream=None, check=True):
         slot = c_i32(-1)
-        st = lib().hsa_tier_place(self._h, b, page, ctypes.byref(slot),
-                                  None if self._keep[1].k is None else _stream(stream))
+        st = lib().hsa_tier_place(self._h, b, page, ctypes.byref(slot), self._stream(stream))
         if check:
             _check("hsa_tier_place", st)
             return slot.value
         return st, slot.value
 
-    def fetch(self, pages, stream=None, check=True) -> int:
+    def _move(self, fn, pages, stream, check):
         arr = np.ascontiguousarray(np.asarray(pages, dtype=np.int32))
         n = arr.shape[-1] if arr.ndim else 0
-        st = lib().hsa_tier_fetch(self._h, arr.ctypes.data_as(c_vp), n,
-                                  None if self._keep[1].k is None else _stream(stream))
+        st = getattr(lib(), fn)(self._h, arr.ctypes.data_as(c_vp), n, self._stream(stream))
         if check:
-            _check("hsa_tier_fetch", st)
+            _check(fn, st)
         return st
+
+    def fetch(self, pages, stream=None, check=True) -> int:
+        return self._move("hsa_tier_fetch", pages, stream, check)
+
+    def prefetch(self, pages, stream=None, check=True) -> int:
+        return self._move("hsa_tier_prefetch", pages, stream, check)
 
     def locate(self, b: int, page: int) -> int:
         return lib().hsa_tier_locate(self._h, b, page)
 
+    def stats(self) -> dict:
+        s = HsaTierStats()
+        lib().hsa_tier_stats(self._h, ctypes.byref(s))
+        return {k: getattr(s, k) for k, _ in HsaTierStats._fields_}
+
     def counters(self):
-        e, f = ctypes.c_int64(0), ctypes.c_int64(0)
-        lib().hsa_tier_counters(self._h, ctypes.byref(e), ctypes.byref(f))
-        return e.value, f.value
+        """(pages moved out of the pool, pages brought into it)."""
+        s = self.stats()
+        return s["evictions"], s["fetches"]

@@ -158,3 +158,38 @@ def test_tier_policy_plan_only():
     t2.fetch([[0, 1]])                 # both back in the pool through the spare slot
     assert t2.locate(0, 0) >= 0 and t2.locate(0, 1) >= 0 and t2.locate(0, 2) < -1
     t.close(), t2.close()
+
+
+def test_tier_three_levels_and_prefetch_plan_only():
+    # 2 pool slots, 2 host slots, 3 file slots (capacity 2 + 2 + 3 - 1 = 6):
+    # L1 evicts its least recently used page to L2, a full L2 spills its own
+    # to L3, a page read back from L3 frees its slot for the spill it causes
+    cfg = P.config(1, 2, 64, 256, "bf16")
+    with pytest.raises(P.HsaError):
+        P.HsaTier(cfg, None, 0, num_slots=2, max_pages=10, l3_slots=3)   # L3 needs L2
+    t = P.HsaTier(cfg, None, 2, num_slots=2, max_pages=10, l3_slots=3)
+    L2 = lambda i: -(i + 2)
+    L3 = lambda i: -(2 + 2 + i)
+    for p in range(6):
+        t.place(0, p)
+    assert t.place(0, 6, check=False)[0] == 2
+    assert [t.locate(0, p) for p in range(6)] == [L3(0), L3(1), L2(0), L2(1), 0, 1]
+    assert t.stats() == dict(evictions=4, fetches=0, spills=2, reloads=0, prefetched=0)
+    t.fetch([[0]])                 # p0: L3 -> L1; p4 -> L2; p2 -> L3 (the freed slot)
+    assert [t.locate(0, p) for p in range(6)] == [0, L3(1), L3(0), L2(1), L2(0), 1]
+    # a prefetch leaves the fetched page where it is and moves the other
+    t.prefetch([[1]])
+    assert [t.locate(0, p) for p in range(6)] == [0, 1, L3(0), L3(1), L2(0), L2(1)]
+    assert t.stats() == dict(evictions=6, fetches=2, spills=4, reloads=2, prefetched=1)
+    # the fetched page plus two more do not fit in two slots
+    assert t.prefetch([[2, 3]], check=False) == 2
+    # a fetch may move anything it does not list
+    t.fetch([[2, 3]])
+    assert [t.locate(0, p) for p in range(6)] == [L2(0), L2(1), 0, 1, L3(0), L3(1)]
+    assert t.stats() == dict(evictions=8, fetches=4, spills=6, reloads=4, prefetched=1)
+    # both listed pages wait in L2, so no L2 page can make room: the pool's
+    # least recently used page goes straight to the free file slot
+    t.fetch([[0, 1]])
+    assert [t.locate(0, p) for p in range(6)] == [0, 1, L3(2), L2(0), L3(0), L3(1)]
+    assert t.stats() == dict(evictions=10, fetches=6, spills=7, reloads=4, prefetched=1)
+    t.close()

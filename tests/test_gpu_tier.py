@@ -1,10 +1,12 @@
-"""GPU check of the host-managed KV tier: a pool with fewer slots than
+"""GPU check of the host-managed KV tiers: a pool with fewer slots than
 logical pages, pages placed in generation order (moving the least recently
-used ones to pinned host memory), Stage-2 selection on the page index, a
-fetch of the selected and current pages, and the forward pass. Because the
-kernels only read pages that are in the pool, the result must equal, bit for
-bit, the forward with every page resident (same pages folded in the same
-order); it is also checked against the oracle."""
+used ones to pinned host memory and from there to a file), Stage-2 selection
+on the page index, a fetch of the selected and current pages, the forward
+pass, and a prefetch on a side stream issued while that forward runs (it
+moves pages the forward does not read). Because the kernels only read pages
+that are in the pool, the result must equal, bit for bit, the forward with
+every page resident (same pages folded in the same order); it is also
+checked against the oracle."""
 import numpy as np
 import pytest
 
@@ -17,7 +19,8 @@ from oracle import hsa_oracle as O
 pytestmark = pytest.mark.gpu
 
 
-def test_forward_over_fetched_pages_is_bit_exact():
+@pytest.mark.parametrize("l2,l3", [(9, 0), (3, 6), (1, 8)])
+def test_forward_over_fetched_pages_is_bit_exact(l2, l3, tmp_path):
     import torch
     from paper_2609_34606_amd import HsaLayer, HsaTier, hsa_page_select
     wl = Workload("tier", batch=1, heads=3, head_dim=128, n_q=300, page_size=200, n_cand=15,
@@ -29,7 +32,7 @@ def test_forward_over_fetched_pages_is_bit_exact():
     k_h, k_max = list(wl.k_h), max(wl.k_h)
     # two chunks: the first sees 12 history pages, the second 15
     chunks = [(12, 3), (15, 3)]
-    n_slots, l2 = 10, 9          # 18 pages fit: 10 + 9 - 1
+    n_slots = 10                 # 18 pages fit: 10 + l2 + l3 - 1
     pool_k = torch.empty((n_slots, H, P, d), dtype=torch.bfloat16, device=cuda)
     pool_v = torch.empty((n_slots, H, d, P), dtype=torch.bfloat16, device=cuda)
     table = torch.full((1, npg + 3), -1, dtype=torch.int32, device=cuda)
@@ -37,12 +40,14 @@ def test_forward_over_fetched_pages_is_bit_exact():
     host_v = torch.empty((l2, H, d, P), dtype=torch.bfloat16, pin_memory=True)
     layer = HsaLayer(1, H, d, P, torch.bfloat16, cuda, k_pool=pool_k, v_pool=pool_v,
                      page_table=table)
-    tier = HsaTier(layer.cfg, layer.pool, l2, host_k, host_v)
+    tier = HsaTier(layer.cfg, layer.pool, l2, host_k, host_v, l3_dir=tmp_path if l3 else None,
+                   l3_slots=l3)
+    side = torch.cuda.Stream()
     # the second chunk's queries are a fresh draw
     qs = [dev["q"], torch.from_numpy(make_case(wl, chunk=1).q).to(cuda).to(torch.bfloat16)]
     placed = 0
     for ci, (n_cand, n_cur) in enumerate(chunks):
-        say(f"[case] tier chunk {ci}: {n_cand} history pages, pool of {n_slots}, host tier of {l2}")
+        say(f"[case] tier chunk {ci}: {n_cand} history pages, pool of {n_slots}, host {l2}, file {l3}")
         # pages arrive in generation order; each is written into the slot the
         # tier gives it and folded at once (state and page index)
         for p in range(placed, n_cand + n_cur):
@@ -61,6 +66,15 @@ def test_forward_over_fetched_pages_is_bit_exact():
                                 np.arange(n_cand, n_cand + n_cur, dtype=np.int32)[None]], 1)
         tier.fetch(pages)
         o = layer.forward_selected(q, sel, n_cand, n_cur, k_h, g_lin=dev["g_lin"], g_sp=dev["g_sp"])
+        # while the forward runs: bring back up to two pages from the lowest
+        # tier holding any (the file first), moving pages the forward does not
+        # read (the pool holds those and the prefetched ones together)
+        room = n_slots - len(set(pages[pages >= 0].tolist()))
+        lows = sorted(range(placed), key=lambda p: tier.locate(0, p))[:min(2, room)]
+        lows = [p for p in lows if tier.locate(0, p) < -1]
+        if lows:
+            tier.prefetch([lows], stream=side)
+            assert all(tier.locate(0, p) >= 0 for p in pages.ravel() if p >= 0)
         torch.cuda.synchronize()
         # the resident reference: the same pages folded in the same order
         if ci == 0:
@@ -76,8 +90,7 @@ def test_forward_over_fetched_pages_is_bit_exact():
         o_r = ref.forward(q, n_cand, n_cur, k_h, k_max=k_max, g_lin=dev["g_lin"], g_sp=dev["g_sp"],
                           sel_out=sel_r)
         torch.cuda.synchronize()
-        ev, fe = tier.counters()
-        say(f"  evictions {ev}, fetches {fe}; selected {to_host(sel).tolist()}")
+        say(f"  {tier.stats()}; selected {to_host(sel).tolist()}")
         assert torch.equal(sel, sel_r)
         assert torch.equal(layer.kv_state, ref.kv_state) and torch.equal(layer.page_kmean[:, :, :placed],
                                                                           ref.page_kmean[:, :, :placed])
@@ -88,5 +101,8 @@ def test_forward_over_fetched_pages_is_bit_exact():
                              case.g_lin, case.g_sp, k_max=k_max)
         np.testing.assert_array_equal(to_host(sel), oref["sel"])
         assert_close(f"O chunk {ci}", to_host(o), oref["O"], **BF16_TOL)
-    assert tier.counters()[0] > 0 and tier.counters()[1] > 0
+    st = tier.stats()
+    assert st["evictions"] > 0 and st["fetches"] > 0 and st["prefetched"] > 0
+    if l3:
+        assert st["spills"] > 0 and st["reloads"] > 0
     tier.close()
