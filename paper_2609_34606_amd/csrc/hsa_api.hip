@@ -18,6 +18,7 @@ constexpr size_t kAlign = 256;
 constexpr int kStateTargetGroups = 512;  // ~2 workgroups per CU on 256 CUs
 constexpr int kQsumRows = 32;
 constexpr int kPartPerHead = 4;  // partial slots per head for split key lists
+constexpr int kPageWaves = 8;    // attention workgroup width for the page walk
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -160,10 +161,10 @@ size_t partial_ws_bytes(const hsa_config_t* c, int n_q) {
 }
 
 void set_partials(AttnParams& p, const hsa_config_t* c, int n_q, void* base) {
-  const size_t cells = (size_t)c->batch * kPartPerHead * c->num_heads * ((n_q + 127) / 128);
   p.part_o = static_cast<float*>(base);
-  p.part_lse = reinterpret_cast<float*>(static_cast<uint8_t*>(base) +
-                                        align_up(cells * 128 * c->head_dim * 4));
+  p.part_lse = reinterpret_cast<float*>(
+      static_cast<uint8_t*>(base) +
+      attention_partial_o_bytes(c->batch, c->head_dim, n_q, kPartPerHead * c->num_heads));
 }
 
 hsa_status_t from_hip(hipError_t e) { return e == hipSuccess ? HSA_OK : HSA_ERR_DEVICE; }
@@ -418,7 +419,7 @@ hsa_status_t run_sparse(const hsa_config_t* cfg, const void* q, int32_t n_q,
   for (int h = 0; h < cfg->num_heads; ++h)
     list_len[h] = std::min(k_h ? k_h[h] : k_max, pool->max_pages) + n_cur_pages;
   plan_attention(p, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
-                 kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16);
+                 kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16, w ? 4 : kPageWaves);
   if (cfg->dtype == HSA_DTYPE_BF16) set_partials(p, cfg, n_q, partials);
   if (w) set_block_lists(p, *w, static_cast<uint8_t*>(partials) - w->part_off);
   return from_hip(launch_attention(cfg->dtype, cfg->head_dim, cfg->batch, p, s));
@@ -674,7 +675,7 @@ hsa_status_t run_attend(const hsa_config_t* cfg, const void* q, int32_t n_q,
   int list_len[HSA_MAX_HEADS];
   for (int h = 0; h < cfg->num_heads; ++h) list_len[h] = std::min(k_h[h], n_cand) + n_cur_pages;
   plan_attention(p, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
-                 kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16);
+                 kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16, w ? 4 : kPageWaves);
   if (cfg->dtype == HSA_DTYPE_BF16) set_partials(p, cfg, n_q, partials);
   if (w) set_block_lists(p, *w, wbase);
   return from_hip(launch_attention(cfg->dtype, cfg->head_dim, cfg->batch, p, s));

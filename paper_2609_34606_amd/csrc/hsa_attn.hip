@@ -33,27 +33,30 @@
 namespace hsa {
 namespace {
 
-constexpr int kBM = 128;   // queries per workgroup (4 waves x 32)
+constexpr int kWaveQ = 32;    // queries per wave
+constexpr int kMaxWaves = 8;  // waves of the widest workgroup
 constexpr int kBN = 64;    // keys per tile
 
-template <int D>
+template <int D, int kW = 4>
 struct AttnLayout {
   static constexpr int kRowK = 2 * D;                  // bytes per key row
   static constexpr int kChunksK = D / 8;               // 16-byte chunks per key row
   static constexpr int kKTile = kBN * kRowK;           // key tile bytes
   static constexpr int kRowV = kBN * 2;                // bytes per value row (64 keys)
   static constexpr int kVTile = D * kRowV;             // value tile bytes
-  static constexpr int kKStages = 3;                   // key tiles in the ring
-  static constexpr int kVStages = 2;                   // value tiles in the ring
+  // key and value tiles in the rings (keys run one tile further ahead): 3 + 2
+  // (80 KB at d = 128) for two workgroups per CU, 4 + 3 (112 KB) for one
+  static constexpr int kKStages = kW == 8 ? 4 : 3;
+  static constexpr int kVStages = kKStages - 1;
   static constexpr int kVBase = kKStages * kKTile;
-  static constexpr int kKV = kVBase + kVStages * kVTile;  // 80 KB at d = 128
+  static constexpr int kKV = kVBase + kVStages * kVTile;
   static constexpr int kLinHalf = (D / 2) * D * 2 * 2; // half the state rows, hi + lo
   static constexpr int kLin = kLinHalf + D * 4;        // + normaliser
   static constexpr int kBytes = kKV > kLin ? kKV : kLin;
   static constexpr int kRowsPerInstK = 1024 / kRowK;   // key rows per 1-KB load
   static constexpr int kRowsPerInstV = 1024 / kRowV;   // value rows per 1-KB load
-  static constexpr int kInstK = kKTile / 1024 / 4;     // key loads per wave
-  static constexpr int kInstV = kVTile / 1024 / 4;     // value loads per wave
+  static constexpr int kInstK = kKTile / 1024 / kW;    // key loads per wave
+  static constexpr int kInstV = kVTile / 1024 / kW;    // value loads per wave
 };
 
 // Swizzles of 16-byte chunks within LDS rows: 16 consecutive rows read at one
@@ -94,7 +97,7 @@ __device__ __forceinline__ int key_perm(int m) {
 //   parts (~16 bits kept) and staged through LDS in two halves of its rows;
 //   o = sigmoid(g_lin) O_lin + sigmoid(g_sp) O_sp, rounded to bf16.
 // Every thread of the workgroup must call it (it synchronises).
-template <int D>
+template <int D, int NT>
 __device__ __forceinline__ void finish(const AttnParams& p, uint8_t* smem, int b, int h, int q_idx,
                                        const u32x4 (&qf)[D / 16], const f32x16 (&acc)[D / 32],
                                        float inv_l, float lse) {
@@ -150,7 +153,7 @@ __device__ __forceinline__ void finish(const AttnParams& p, uint8_t* smem, int b
   if (tid < D) zs[tid] = p.k_state[((size_t)b * H + h) * D + tid];
   const float* st = p.kv_state + ((size_t)b * H + h) * D * D;
   auto stage_state = [&](int hf) {
-    for (int e = 4 * tid; e < RH * D; e += 1024) {
+    for (int e = 4 * tid; e < RH * D; e += 4 * NT) {
       const f32x4 x = *reinterpret_cast<const f32x4*>(st + (size_t)hf * RH * D + e);
       const int j = e / D, i = e % D;
       const int off = j * (2 * D) + (((i >> 3) ^ swz_k<D>(j)) << 4) + (i & 7) * 2;
@@ -225,9 +228,11 @@ __device__ __forceinline__ void finish(const AttnParams& p, uint8_t* smem, int b
   }
 }
 
-template <int D, bool kSmallP, bool kList>
-__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
-  using L = AttnLayout<D>;
+template <int D, bool kSmallP, bool kList, int kW>
+__global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p) {
+  static_assert(!kList || kW == 4, "tile lists mark two 64-query blocks per workgroup");
+  using L = AttnLayout<D, kW>;
+  constexpr int kBM = kWaveQ * kW;
   constexpr int KK = D / 16;   // 16-wide d slices
   constexpr int NM = D / 32;   // 32-wide d blocks of the output
   __shared__ __attribute__((aligned(1024))) uint8_t smem[L::kBytes];
@@ -312,7 +317,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
 
   // ---- Q fragment: lane holds query (l%32) of this wave, d = 16kk + 8*half + 0..7
   const uint16_t* qb = static_cast<const uint16_t*>(p.q);
-  const int q_idx = qtile * kBM + wave * 32 + l32;
+  const int q_idx = qtile * kBM + wave * kWaveQ + l32;
   const int q_ld = min(q_idx, p.n_q - 1);
   u32x4 qf[KK];
   {
@@ -413,9 +418,12 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
   const float c2 = p.scale_log2;
   const int krow = key_perm(l32);
 
-  // prologue: K(0), V(0), K(1). List mode keeps the entries of the tile
-  // being computed (ec), of the next value issue (ev) and of the next key
-  // issue (ek) in scalar registers, read one iteration ahead.
+  // prologue: K(0), V(0), ..., K(S-2), V(S-2), K(S-1) for S = kVStages.
+  // List mode (S = 2) keeps the entries of the tile being computed (ec), of
+  // the next value issue (ev) and of the next key issue (ek) in scalar
+  // registers, read one iteration ahead.
+  constexpr int SK = L::kKStages, SV = L::kVStages;
+  static_assert(!kList || SV == 2, "the tile-list walk keeps three entries");
   int2 ec = make_int2(0, 0), ev = ec, ek = ec;
   if (ntiles > 0) {
     if constexpr (kList) {
@@ -426,23 +434,30 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
       issue_k_at(1, ev);
       ek = entry(u0 + 2);
     } else {
-      issue_k(0);
-      issue_v(0);
-      issue_k(1);
+#pragma unroll
+      for (int i = 0; i < SV - 1; ++i) {
+        issue_k(i);
+        issue_v(i);
+      }
+      issue_k(SV - 1);
     }
   }
-  int t = 0, kbuf = 0;
+  // ring slots: kbuf / vbuf of the tile being computed, and of the tiles
+  // issued in this iteration (tile + SK - 1 and tile + SV - 1)
+  int t = 0, kbuf = 0, vbuf = 0;
+  int kbuf_in = SK - 1, vbuf_in = SV - 1;
   for (int tile = 0; tile < ntiles; ++tile) {
-    // K(tile) and V(tile) have landed once at most the next key tile's
-    // loads are outstanding
-    wait_vmcnt<L::kInstK>();
+    // K(tile) and V(tile) have landed once at most the loads issued after
+    // V(tile) are outstanding: K(tile+1), and one V and one K per later
+    // iteration
+    wait_vmcnt<L::kInstK + (SV - 2) * (L::kInstK + L::kInstV)>();
     lds_barrier();
     if constexpr (kList) {
-      issue_v_at((tile + 1) & 1, ev);
-      issue_k_at(kbuf == 0 ? 2 : kbuf - 1, ek);   // ring slot (tile+2) % 3
+      issue_v_at(vbuf_in, ev);
+      issue_k_at(kbuf_in, ek);
     } else {
-      issue_v((tile + 1) & 1);
-      issue_k(kbuf == 0 ? 2 : kbuf - 1);
+      issue_v(vbuf_in);
+      issue_k(kbuf_in);
     }
     // list mode: waves of a query block that does not keep this tile skip it
     const int tc = kList ? (ec.y >> 2) : t;
@@ -454,17 +469,37 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
       f32x16 s[2];
       {
         const uint8_t* kt_l = smem + kbuf * L::kKTile;
-        s[0] = f32x16{0};
-        s[1] = f32x16{0};
+        if constexpr (D == 128 && kW == 8) {
+          // registers to spare: four chains, even and odd d slices
+          // accumulated apart and added at the end, so that dependent MFMAs
+          // sit four issues apart
+          f32x16 s4[2][2];
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk)
+          for (int h2 = 0; h2 < 2; ++h2) s4[h2][0] = s4[h2][1] = f32x16{0};
 #pragma unroll
-          for (int h2 = 0; h2 < 2; ++h2) {
-            const int row = 32 * h2 + krow;
-            const int chunk = 2 * kk + half;
-            const u32x4 a = ld_lds16(kt_l + row * L::kRowK + ((chunk ^ swz_k<D>(row)) << 4));
-            s[h2] = mfma32(a, qf[kk], s[h2]);
-          }
+          for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+            for (int h2 = 0; h2 < 2; ++h2) {
+              const int row = 32 * h2 + krow;
+              const int chunk = 2 * kk + half;
+              const u32x4 a = ld_lds16(kt_l + row * L::kRowK + ((chunk ^ swz_k<D>(row)) << 4));
+              s4[h2][kk & 1] = mfma32(a, qf[kk], s4[h2][kk & 1]);
+            }
+          s[0] = s4[0][0] + s4[0][1];
+          s[1] = s4[1][0] + s4[1][1];
+        } else {
+          s[0] = f32x16{0};
+          s[1] = f32x16{0};
+#pragma unroll
+          for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+            for (int h2 = 0; h2 < 2; ++h2) {
+              const int row = 32 * h2 + krow;
+              const int chunk = 2 * kk + half;
+              const u32x4 a = ld_lds16(kt_l + row * L::kRowK + ((chunk ^ swz_k<D>(row)) << 4));
+              s[h2] = mfma32(a, qf[kk], s[h2]);
+            }
+        }
         pipeline_lds_mfma<2 * KK>();
       }
       // The last tile of a page: window rows holding keys outside the tile
@@ -523,7 +558,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
       l_run += rs;
       // O^T += V^T P^T (NM independent chains), value fragments read ahead
       {
-        const uint8_t* vt_l = smem + L::kVBase + (tile & 1) * L::kVTile;
+        const uint8_t* vt_l = smem + L::kVBase + vbuf * L::kVTile;
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
           const int chunk = 2 * ks + half;
@@ -547,7 +582,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
       ek = en;
     }
     if (++t == tpp) t = 0;
-    kbuf = kbuf == 2 ? 0 : kbuf + 1;
+    kbuf = kbuf == SK - 1 ? 0 : kbuf + 1;
+    vbuf = vbuf == SV - 1 ? 0 : vbuf + 1;
+    kbuf_in = kbuf_in == SK - 1 ? 0 : kbuf_in + 1;
+    vbuf_in = vbuf_in == SV - 1 ? 0 : vbuf_in + 1;
   }
   wait_vmcnt<0>();  // the trailing re-reads
 
@@ -557,7 +595,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
   if (ns > 1) {
     // partial result of this split: normalised output and log-sum-exp, in the
     // accumulator register layout (register-major, lane fastest: coalesced)
-    const size_t cell = (((size_t)b * p.sc.n_part + p.sc.part_base[h] + split) * nqt + qtile) * 4 + wave;
+    const size_t cell = ((size_t)b * p.sc.n_part + p.sc.part_base[h] + split) * p.sc.nq32 + qtile * kW + wave;
     float* po = p.part_o + cell * (NM * 16 * 64) + lane;
 #pragma unroll
     for (int m = 0; m < NM; ++m)
@@ -566,11 +604,13 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnParams p) {
     p.part_lse[cell * 64 + lane] = lse;
     return;
   }
-  finish<D>(p, smem, b, h, qtile * kBM + wave * 32 + l32, qf, acc, inv_l, lse);
+  finish<D, 64 * kW>(p, smem, b, h, q_idx, qf, acc, inv_l, lse);
 }
 
-// Merge of the splits of one (head, query tile): weights exp(lse_s - max),
+// Merge of the splits of one (head, 128 queries): weights exp(lse_s - max),
 // summed over the splits in order, then the same finish as an unsplit item.
+// Partials are kept per 32-query wave slot, so this works for attention
+// workgroups of any width.
 template <int D>
 __global__ __launch_bounds__(256, 2) void combine_bf16_kernel(AttnParams p) {
   using L = AttnLayout<D>;
@@ -579,11 +619,11 @@ __global__ __launch_bounds__(256, 2) void combine_bf16_kernel(AttnParams p) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, half = lane >> 5;
-  const int b = blockIdx.y, nqt = p.sc.nqt;
-  const int ch = blockIdx.x / nqt, qtile = blockIdx.x % nqt;
+  const int b = blockIdx.y, nq32 = p.sc.nq32, cq = nq32 / 4;
+  const int ch = blockIdx.x / cq, q32 = (blockIdx.x % cq) * 4 + wave;
   const int h = p.sc.c_head[ch], ns = p.sc.n_split[h];
-  const size_t cell0 = (((size_t)b * p.sc.n_part + p.sc.part_base[h]) * nqt + qtile) * 4 + wave;
-  const size_t cstride = (size_t)nqt * 4;  // cells between consecutive splits
+  const size_t cell0 = ((size_t)b * p.sc.n_part + p.sc.part_base[h]) * nq32 + q32;
+  const size_t cstride = (size_t)nq32;  // cells between consecutive splits
   float lmax = -INFINITY;
   for (int s = 0; s < ns; ++s) lmax = fmaxf(lmax, p.part_lse[(cell0 + s * cstride) * 64 + lane]);
   f32x16 acc[NM];
@@ -603,7 +643,7 @@ __global__ __launch_bounds__(256, 2) void combine_bf16_kernel(AttnParams p) {
   }
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
   const float lse = wsum > 0.f ? lmax + __logf(wsum) : -INFINITY;
-  const int q_idx = qtile * kBM + wave * 32 + l32;
+  const int q_idx = q32 * kWaveQ + l32;
   u32x4 qf[KK];
   {
     const int q_ld = min(q_idx, p.n_q - 1);
@@ -611,7 +651,7 @@ __global__ __launch_bounds__(256, 2) void combine_bf16_kernel(AttnParams p) {
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) qf[kk] = ld_global16(qrow + 16 * kk);
   }
-  finish<D>(p, smem, b, h, q_idx, qf, acc, inv, lse);
+  finish<D, 256>(p, smem, b, h, q_idx, qf, acc, inv, lse);
 }
 
 // fp32 inputs: VALU attention, 64 queries per workgroup, 4 lanes per query.
@@ -738,11 +778,20 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
 
 }  // namespace
 
+// Partials are kept per 32-query wave slot; the widest workgroup pads the
+// query count the most.
+static size_t partial_cells(int B, int n_q, int max_part) {
+  const size_t nq32 = (size_t)((n_q + kWaveQ * kMaxWaves - 1) / (kWaveQ * kMaxWaves)) * kMaxWaves;
+  return (size_t)B * max_part * nq32;
+}
+
+size_t attention_partial_o_bytes(int B, int d, int n_q, int max_part) {
+  return (partial_cells(B, n_q, max_part) * kWaveQ * d * 4 + 255) / 256 * 256;
+}
+
 size_t attention_partial_bytes(int B, int d, int n_q, int max_part) {
-  const size_t nqt = (n_q + kBM - 1) / kBM;
-  const size_t cells = (size_t)B * max_part * nqt;
-  const size_t o = cells * kBM * d * 4, l = cells * 4 * 64 * 4;
-  return ((o + 255) / 256 + (l + 255) / 256) * 256;
+  return attention_partial_o_bytes(B, d, n_q, max_part) +
+         (partial_cells(B, n_q, max_part) * 64 * 4 + 255) / 256 * 256;
 }
 
 namespace {
@@ -755,12 +804,13 @@ struct Chunk {
 };
 
 // Workgroup w of a launch runs on XCD w % 8, and each XCD hands its
-// workgroups, in order, to whichever of its 64 slots (32 CUs x 2) frees
-// first. Simulates that for the chunks given XCD by XCD (list scheduling):
-// chunks are taken largest item first, each goes to the XCD where its items
-// can all start earliest. Returns the simulated makespan; fills xcd_of.
-double deal_chunks(const std::vector<Chunk>& chunks, std::vector<int>& xcd_of) {
-  constexpr int kXcd = 8, kSlotsPerXcd = 64;
+// workgroups, in order, to whichever of its slots (32 CUs x the workgroups a
+// CU holds) frees first. Simulates that for the chunks given XCD by XCD
+// (list scheduling): chunks are taken largest item first, each goes to the
+// XCD where its items can all start earliest. Returns the simulated
+// makespan; fills xcd_of.
+double deal_chunks(const std::vector<Chunk>& chunks, int kSlotsPerXcd, std::vector<int>& xcd_of) {
+  constexpr int kXcd = 8;
   // slot finish times of each XCD, kept sorted ascending
   std::vector<double> slot(kXcd * kSlotsPerXcd, 0.0);
   xcd_of.assign(chunks.size(), 0);
@@ -787,27 +837,27 @@ double deal_chunks(const std::vector<Chunk>& chunks, std::vector<int>& xcd_of) {
 
 // Inputs of a schedule, the key of the schedule cache.
 struct PlanKey {
-  int H, d, n_q, P, max_part, split;
+  int H, d, n_q, P, max_part, split, waves;
   int list_len[HSA_MAX_HEADS];
   bool operator==(const PlanKey& o) const {
     return H == o.H && d == o.d && n_q == o.n_q && P == o.P && max_part == o.max_part &&
-           split == o.split && std::equal(list_len, list_len + H, o.list_len);
+           split == o.split && waves == o.waves && std::equal(list_len, list_len + H, o.list_len);
   }
 };
 
 void plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_len, int max_part,
-                   bool split);
+                   bool split, int waves);
 
 }  // namespace
 
 void plan_attention(AttnParams& p, int H, int d, int n_q, int P, const int* list_len, int max_part,
-                    bool split) {
+                    bool split, int waves) {
   constexpr int kCache = 8;
   static std::mutex mu;
   static PlanKey keys[kCache];
   static AttnSchedule scheds[kCache];
   static int n_cached = 0, next = 0;
-  PlanKey key{H, d, n_q, P, max_part, split ? 1 : 0, {}};
+  PlanKey key{H, d, n_q, P, max_part, split ? 1 : 0, waves, {}};
   std::copy(list_len, list_len + H, key.list_len);
   {
     std::lock_guard<std::mutex> lock(mu);
@@ -817,7 +867,7 @@ void plan_attention(AttnParams& p, int H, int d, int n_q, int P, const int* list
         return;
       }
   }
-  plan_schedule(p, H, d, n_q, P, list_len, max_part, split);
+  plan_schedule(p, H, d, n_q, P, list_len, max_part, split, waves);
   std::lock_guard<std::mutex> lock(mu);
   keys[next] = key;
   scheds[next] = p.sc;
@@ -828,11 +878,14 @@ void plan_attention(AttnParams& p, int H, int d, int n_q, int P, const int* list
 namespace {
 
 void plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_len, int max_part,
-                   bool split) {
+                   bool split, int waves) {
+  const int kBM = kWaveQ * waves;
   const int nqt = (n_q + kBM - 1) / kBM;
+  const int slots_per_xcd = 32 * (8 / waves);
   const int tpp = (P + kBN - 1) / kBN;
-  // Cost model (unit: one 64-key tile of one item with two workgroups on a
-  // CU): an item costs its tiles plus a fixed prologue/epilogue; splitting a
+  // Cost model (unit: one 64-key tile of one item with a full CU, i.e. two
+  // 4-wave or one 8-wave workgroup): an item costs its tiles plus a fixed
+  // prologue/epilogue; splitting a
   // head adds a combine pass whose time is dominated by writing and reading
   // the partial outputs.
   constexpr double kOverheadTiles = 3.0, kTileUs = 2.25;
@@ -874,7 +927,7 @@ void plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_
       if (ns[h] > 1) n_part += ns[h];
     if (n_part > max_part) return 1e30;
     build(ns, per_group, order, chunks);
-    double us = deal_chunks(chunks, xcd_of) * kTileUs;
+    double us = deal_chunks(chunks, slots_per_xcd, xcd_of) * kTileUs * (waves / 4.0);
     if (n_part > 0) us += kCombineUsFixed + 2.0 * n_part * nqt * (double)kBM * d * 4 / kPartialBytesPerUs;
     return us;
   };
@@ -899,6 +952,8 @@ void plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_
   }
   evaluate(best_ns, best_g);  // rebuild order, chunks and xcd_of of the choice
   p.sc.nqt = nqt;
+  p.sc.nq32 = nqt * waves;
+  p.sc.waves = waves;
   p.sc.n_order = H;
   int items = 0, n_part = 0, n_chead = 0;
   for (int i = 0; i < H; ++i) {
@@ -946,26 +1001,35 @@ hipError_t launch_attention(int dtype, int d, int B, const AttnParams& p, hipStr
   if (dtype == HSA_DTYPE_BF16) {
     const dim3 grid(8 * std::max(1, p.sc.xcd_items), B);
     const bool small = p.P < kBN, list = p.blist != nullptr;
+    // tile lists (block-sparse mode) are built per 128-query tile
+    if (list && p.sc.waves != 4) return hipErrorInvalidValue;
+    const int nt = 64 * p.sc.waves;
     if (d == 128) {
       if (list) {
-        if (small) attn_bf16_kernel<128, true, true><<<grid, 256, 0, s>>>(p);
-        else attn_bf16_kernel<128, false, true><<<grid, 256, 0, s>>>(p);
+        if (small) attn_bf16_kernel<128, true, true, 4><<<grid, 256, 0, s>>>(p);
+        else attn_bf16_kernel<128, false, true, 4><<<grid, 256, 0, s>>>(p);
+      } else if (p.sc.waves == 8) {
+        if (small) attn_bf16_kernel<128, true, false, 8><<<grid, nt, 0, s>>>(p);
+        else attn_bf16_kernel<128, false, false, 8><<<grid, nt, 0, s>>>(p);
       } else {
-        if (small) attn_bf16_kernel<128, true, false><<<grid, 256, 0, s>>>(p);
-        else attn_bf16_kernel<128, false, false><<<grid, 256, 0, s>>>(p);
+        if (small) attn_bf16_kernel<128, true, false, 4><<<grid, nt, 0, s>>>(p);
+        else attn_bf16_kernel<128, false, false, 4><<<grid, nt, 0, s>>>(p);
       }
     } else {
       if (list) {
-        if (small) attn_bf16_kernel<64, true, true><<<grid, 256, 0, s>>>(p);
-        else attn_bf16_kernel<64, false, true><<<grid, 256, 0, s>>>(p);
+        if (small) attn_bf16_kernel<64, true, true, 4><<<grid, 256, 0, s>>>(p);
+        else attn_bf16_kernel<64, false, true, 4><<<grid, 256, 0, s>>>(p);
+      } else if (p.sc.waves == 8) {
+        if (small) attn_bf16_kernel<64, true, false, 8><<<grid, nt, 0, s>>>(p);
+        else attn_bf16_kernel<64, false, false, 8><<<grid, nt, 0, s>>>(p);
       } else {
-        if (small) attn_bf16_kernel<64, true, false><<<grid, 256, 0, s>>>(p);
-        else attn_bf16_kernel<64, false, false><<<grid, 256, 0, s>>>(p);
+        if (small) attn_bf16_kernel<64, true, false, 4><<<grid, nt, 0, s>>>(p);
+        else attn_bf16_kernel<64, false, false, 4><<<grid, nt, 0, s>>>(p);
       }
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.sc.n_chead == 0) return e;
-    const dim3 cgrid(p.sc.n_chead * p.sc.nqt, B);
+    const dim3 cgrid(p.sc.n_chead * (p.sc.nq32 / 4), B);
     if (d == 128) combine_bf16_kernel<128><<<cgrid, 256, 0, s>>>(p);
     else combine_bf16_kernel<64><<<cgrid, 256, 0, s>>>(p);
   } else {

@@ -153,7 +153,9 @@ enum AttnMode : int32_t {
 struct AttnSchedule {
   // Attention items of one batch entry are numbered head by head in head_order, each head
   // contributing n_split[h] * nqt items (split-major, query tile fastest).
-  int32_t nqt;                           // query tiles of kBM queries
+  int32_t nqt;                           // query tiles of 32 * waves queries
+  int32_t waves;                         // waves per workgroup (4 or 8)
+  int32_t nq32;                          // 32-query wave slots per (head, split): nqt * waves
   int32_t n_items;                       // attention items per batch entry
   int32_t n_order;                       // heads listed in head_order
   int32_t head_order[HSA_MAX_HEADS];
@@ -196,8 +198,8 @@ struct AttnParams {
   // sparse mode
   float* o_sp;              // [B, n_q, H, d]
   float* lse;               // [B, H, n_q] nullable
-  float* part_o;                         // [B, n_part, nqt, 4 waves, 16*d/32 regs, 64 lanes]
-  float* part_lse;                       // [B, n_part, nqt, 4 waves, 64 lanes]
+  float* part_o;                         // [B, n_part, nq32, 16*d/32 regs, 64 lanes]
+  float* part_lse;                       // [B, n_part, nq32, 64 lanes]
   // block-sparse mode (blist != NULL): each (b, h, query tile) walks its own
   // list of 64-key tiles, entry {slot * H + h, (tile index << 2) | mask}; mask
   // bit w covers query block 2 * qtile + w (waves 2w, 2w + 1)
@@ -210,12 +212,16 @@ struct AttnParams {
 // Chooses the split of each head's page list and the item order for
 // list_len[h] pages per head (H heads, head dim d, n_q queries, page size P);
 // at most max_part partial slots. split = false keeps every head whole.
-// Fills p.sc; the last few schedules are cached (thread-safe), so a call
-// with the inputs of a recent one costs a table lookup.
+// waves: 8 (256-query workgroups, one per CU) for the page walk, 4 (128
+// queries, two per CU) for tile lists. Fills p.sc; the last few schedules
+// are cached (thread-safe), so a call with the inputs of a recent one costs
+// a table lookup.
 void plan_attention(AttnParams& p, int H, int d, int n_q, int P, const int* list_len,
-                    int max_part, bool split);
-// Workspace bytes for max_part partial slots.
+                    int max_part, bool split, int waves);
+// Workspace bytes for max_part partial slots (any workgroup width), and
+// the offset of the LSE partials in it.
 size_t attention_partial_bytes(int B, int d, int n_q, int max_part);
+size_t attention_partial_o_bytes(int B, int d, int n_q, int max_part);
 
 hipError_t launch_attention(int dtype, int d, int B, const AttnParams& p,
                             hipStream_t s);
