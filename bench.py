@@ -187,8 +187,8 @@ def bench_single(args, wl):
         res["adaptive"] = bench_adaptive(args, wl, layer, q, k_h, k_max, sel)
         if wl.dtype == "bf16":
             res["linformer"] = bench_linformer(args, wl, layer, q, k_h, k_max, sel)
-        res["retrieval"] = bench_retrieval(args, wl, layer, q, k_h, k_max)
-        res["tier"] = bench_tier(args, wl, dev, layer, q, k_h, k_max, sel)
+            res["retrieval"] = bench_retrieval(args, wl, layer, q, k_h, k_max)
+            res["tier"] = bench_tier(args, wl, dev, layer, q, k_h, k_max, sel)
     if not args.no_cpu_baseline:
         heads = list(range(wl.heads)) if wl.heads * wl.n_pages <= 12 * 24 else [0, 1]
         log("timing the oracle on the host ...")
