@@ -8,17 +8,19 @@
 // fetched straight from its page through the page table into LDS, so the
 // concatenation costs no extra HBM pass.
 //
-// Work decomposition (bf16, d = 128 shown): a workgroup owns 128 queries of
-// one head, four waves of 32 queries each, and walks the head's key list in
-// tiles of 64 keys: key tiles in a 3-slot LDS ring (two in flight while one
-// is computed), value tiles in a 2-slot ring. Each wave computes the transposed score tile S^T = K Q^T with
-// 32x32x16 bf16 MFMAs so that a lane holds 32 scores of a single query: the
-// running max needs one cross-lane exchange per tile and the accumulator
-// rescale is one multiply per register. The value product is O^T += V^T P^T,
-// reading the d-major value pages directly. Key rows are fed to the score
-// MFMA in a permuted order so that the score registers of a lane already form
-// the bf16 operand of the value MFMA. Two workgroups (80 KB of LDS each)
-// share a CU.
+// Two bf16 walks share the tile layout and the epilogue. Both compute the
+// transposed score tile S^T = K Q^T with 32x32x16 bf16 MFMAs, so that a lane
+// holds 32 scores of a single query (the running max needs one cross-lane
+// exchange per tile, the accumulator rescale one multiply per register), and
+// the value product O^T += V^T P^T straight from the d-major value pages. Key
+// rows are fed to the score MFMA in a permuted order so that the score
+// registers of a lane already form the bf16 operand of the value MFMA.
+//  * attn_pp_kernel, the page walk: 256 queries of one head per workgroup
+//    (8 waves, one workgroup per CU), 64-key tiles in 4 + 4 LDS rings, the
+//    score and value halves of the two waves of each SIMD in alternation.
+//  * attn_bf16_kernel, the tile-list walk of the block-sparse mode: 128
+//    queries (4 waves, two workgroups per CU), a 3-slot key and a 2-slot
+//    value ring, all waves in step.
 #include <float.h>
 
 #include <algorithm>
@@ -44,10 +46,11 @@ struct AttnLayout {
   static constexpr int kKTile = kBN * kRowK;           // key tile bytes
   static constexpr int kRowV = kBN * 2;                // bytes per value row (64 keys)
   static constexpr int kVTile = D * kRowV;             // value tile bytes
-  // key and value tiles in the rings (keys run one tile further ahead): 3 + 2
-  // (80 KB at d = 128) for two workgroups per CU, 4 + 3 (112 KB) for one
+  // key and value tiles in the rings: 3 + 2 (80 KB at d = 128, keys one
+  // tile further ahead) for the 4-wave tile-list walk, two workgroups per
+  // CU; 4 + 4 (128 KB) for the 8-wave page walk, one per CU
   static constexpr int kKStages = kW == 8 ? 4 : 3;
-  static constexpr int kVStages = kKStages - 1;
+  static constexpr int kVStages = kW == 8 ? 4 : 2;
   static constexpr int kVBase = kKStages * kKTile;
   static constexpr int kKV = kVBase + kVStages * kVTile;
   static constexpr int kLinHalf = (D / 2) * D * 2 * 2; // half the state rows, hi + lo
@@ -230,7 +233,7 @@ __device__ __forceinline__ void finish(const AttnParams& p, uint8_t* smem, int b
 
 template <int D, bool kSmallP, bool kList, int kW>
 __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p) {
-  static_assert(!kList || kW == 4, "tile lists mark two 64-query blocks per workgroup");
+  static_assert(kW == 4, "the 8-wave page walk is attn_pp_kernel");
   using L = AttnLayout<D, kW>;
   constexpr int kBM = kWaveQ * kW;
   constexpr int KK = D / 16;   // 16-wide d slices
@@ -469,37 +472,17 @@ __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p
       f32x16 s[2];
       {
         const uint8_t* kt_l = smem + kbuf * L::kKTile;
-        if constexpr (D == 128 && kW == 8) {
-          // registers to spare: four chains, even and odd d slices
-          // accumulated apart and added at the end, so that dependent MFMAs
-          // sit four issues apart
-          f32x16 s4[2][2];
+        s[0] = f32x16{0};
+        s[1] = f32x16{0};
 #pragma unroll
-          for (int h2 = 0; h2 < 2; ++h2) s4[h2][0] = s4[h2][1] = f32x16{0};
+        for (int kk = 0; kk < KK; ++kk)
 #pragma unroll
-          for (int kk = 0; kk < KK; ++kk)
-#pragma unroll
-            for (int h2 = 0; h2 < 2; ++h2) {
-              const int row = 32 * h2 + krow;
-              const int chunk = 2 * kk + half;
-              const u32x4 a = ld_lds16(kt_l + row * L::kRowK + ((chunk ^ swz_k<D>(row)) << 4));
-              s4[h2][kk & 1] = mfma32(a, qf[kk], s4[h2][kk & 1]);
-            }
-          s[0] = s4[0][0] + s4[0][1];
-          s[1] = s4[1][0] + s4[1][1];
-        } else {
-          s[0] = f32x16{0};
-          s[1] = f32x16{0};
-#pragma unroll
-          for (int kk = 0; kk < KK; ++kk)
-#pragma unroll
-            for (int h2 = 0; h2 < 2; ++h2) {
-              const int row = 32 * h2 + krow;
-              const int chunk = 2 * kk + half;
-              const u32x4 a = ld_lds16(kt_l + row * L::kRowK + ((chunk ^ swz_k<D>(row)) << 4));
-              s[h2] = mfma32(a, qf[kk], s[h2]);
-            }
-        }
+          for (int h2 = 0; h2 < 2; ++h2) {
+            const int row = 32 * h2 + krow;
+            const int chunk = 2 * kk + half;
+            const u32x4 a = ld_lds16(kt_l + row * L::kRowK + ((chunk ^ swz_k<D>(row)) << 4));
+            s[h2] = mfma32(a, qf[kk], s[h2]);
+          }
         pipeline_lds_mfma<2 * KK>();
       }
       // The last tile of a page: window rows holding keys outside the tile
@@ -605,6 +588,341 @@ __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p
     return;
   }
   finish<D, 64 * kW>(p, smem, b, h, q_idx, qf, acc, inv_l, lse);
+}
+
+// Page walk of the selected pages plus the current pages: 256 queries of one
+// head per workgroup (8 waves of 32 queries; waves w and w + 4 share a SIMD),
+// one workgroup per CU. Each 64-key tile t is two phases per wave:
+//   X(t): the scores S(t)^T = K(t) Q^T (16 MFMAs at d = 128, key fragments
+//         read from LDS eight ahead);
+//   Y(t): the softmax of S(t) and the value product O^T += V(t)^T P(t)^T; the
+//         four MFMAs of each 16-key group go out as soon as its P fragment is
+//         packed and run under the next group's exponentials.
+// Waves 0-3 run X in even slots and Y in odd ones, waves 4-7 the other way
+// round, with a workgroup barrier between slots. So in every slot each SIMD
+// receives the MFMAs of both its waves and the exponentials of one, and all
+// eight waves read LDS (a loaded LDS needs many reads in flight: four
+// waves alone return a fraction of its bandwidth). Key and value tiles sit in
+// 4-slot rings (128 KB at d = 128) filled by global-to-LDS copies that every
+// wave issues for its share right after a barrier.
+template <int D, bool kSmallP>
+__global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
+  using L = AttnLayout<D, 8>;
+  constexpr int kBM = 256;
+  constexpr int KK = D / 16;   // 16-wide d slices
+  constexpr int NM = D / 32;   // 32-wide d blocks of the output
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[L::kBytes];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool first = wave < 4;  // matrix phase in even slots
+  const int l32 = lane & 31, half = lane >> 5;
+  const int H = p.H, P = p.P;
+  const int nqt = p.sc.nqt;
+  const int b = blockIdx.y;
+  int qtile, h, split;
+  {
+    const int w = blockIdx.x, x = w & 7;
+    int k = w >> 3, c = p.sc.xcd_chunk[x];
+    const int c_end = p.sc.xcd_chunk[x + 1];
+    while (c < c_end && k >= p.sc.chunk_len[c]) {
+      k -= p.sc.chunk_len[c];
+      ++c;
+    }
+    if (c >= c_end) return;
+    const int item = p.sc.chunk_start[c] + k;
+    int oh = 0;
+    while (oh + 1 < p.sc.n_order && p.sc.item_off[oh + 1] <= item) ++oh;
+    h = p.sc.head_order[oh];
+    const int local = item - p.sc.item_off[oh];
+    split = local / nqt;
+    qtile = local % nqt;
+  }
+  const int ns = p.sc.n_split[h];
+  const int tpp = (P + kBN - 1) / kBN;
+
+  const int32_t* selrow = p.sel + ((size_t)b * H + h) * p.k_max;
+  const int32_t* ptrow = p.page_table + (size_t)b * p.max_pages;
+  int n_sel = 0;
+  while (n_sel < p.k_max) {
+    const int e = ld_const(selrow + n_sel);
+    if (e < 0 || e >= p.max_pages) break;
+    ++n_sel;
+  }
+  auto head_of = [&](int li) -> size_t {
+    const int lp = li < n_sel ? ld_const(selrow + li) : p.cur_first + (li - n_sel);
+    return (size_t)clampi(ld_const(ptrow + lp), 0, p.num_slots - 1) * H + h;
+  };
+  int pg0 = 0, pg1;
+  {
+    const int n_list = n_sel + p.n_cur;
+    pg1 = n_list;
+    if (ns > 1) {
+      const int len = p.sc.list_len[h], base = len / ns, rem = len % ns;
+      pg0 = min(n_list, split * base + min(split, rem));
+      pg1 = split == ns - 1 ? n_list : min(n_list, pg0 + base + (split < rem ? 1 : 0));
+    }
+  }
+  const int ntiles = (pg1 - pg0) * tpp;
+
+  const uint16_t* qb = static_cast<const uint16_t*>(p.q);
+  const int q_idx = qtile * kBM + wave * kWaveQ + l32;
+  const int q_ld = min(q_idx, p.n_q - 1);
+  u32x4 qf[KK];
+  {
+    const uint16_t* qrow = qb + (((size_t)b * p.n_q + q_ld) * H + h) * D + 8 * half;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) qf[kk] = ld_global16(qrow + 16 * kk);
+  }
+  const uint16_t* kpool = static_cast<const uint16_t*>(p.k);
+  const uint16_t* vpool = static_cast<const uint16_t*>(p.v);
+
+  auto k_row = [&](int n) { return (wave * L::kInstK + n) * L::kRowsPerInstK + lane / L::kChunksK; };
+  auto v_row = [&](int n) { return (wave * L::kInstV + n) * L::kRowsPerInstV + (lane >> 3); };
+  auto v_col = [&](int n) { return 8 * ((lane & 7) ^ swz_v(v_row(n))); };
+  uint32_t k_off[L::kInstK], v_off[L::kInstV];
+#pragma unroll
+  for (int n = 0; n < L::kInstK; ++n) {
+    const int r = k_row(n);
+    k_off[n] = (uint32_t)(r * D + 8 * ((lane % L::kChunksK) ^ swz_k<D>(r))) * 2u;
+  }
+#pragma unroll
+  for (int n = 0; n < L::kInstV; ++n) v_off[n] = (uint32_t)(v_row(n) * P + v_col(n)) * 2u;
+
+  auto window = [&](int t) { return kSmallP ? t * kBN : min(t * kBN, P - kBN); };
+  int kli = pg0, kt = 0, vli = pg0, vt = 0;
+  const char* kbase =
+      reinterpret_cast<const char*>(kpool) + (pg0 < pg1 ? head_of(pg0) : 0) * (size_t)P * D * 2;
+  const char* vbase =
+      reinterpret_cast<const char*>(vpool) + (pg0 < pg1 ? head_of(pg0) : 0) * (size_t)D * P * 2;
+  auto load_k = [&](int buf, const char* src) {
+    uint8_t* dst = smem + buf * L::kKTile + wave * L::kInstK * 1024;
+#pragma unroll
+    for (int n = 0; n < L::kInstK; ++n) {
+      uint32_t off = k_off[n];
+      if constexpr (kSmallP) off -= (uint32_t)(max(0, k_row(n) - (P - 1)) * D * 2);
+      g2lds16_hidden(src + off, dst + n * 1024);
+    }
+  };
+  auto load_v = [&](int buf, const char* src) {
+    uint8_t* dst = smem + L::kVBase + buf * L::kVTile + wave * L::kInstV * 1024;
+#pragma unroll
+    for (int n = 0; n < L::kInstV; ++n) {
+      uint32_t off = v_off[n];
+      if constexpr (kSmallP) off -= (uint32_t)(max(0, v_col(n) - (P - 8)) * 2);
+      g2lds16_hidden(src + off, dst + n * 1024);
+    }
+  };
+  auto issue_k = [&](int buf) {
+    load_k(buf, kbase + (size_t)window(kt) * D * 2);
+    if (kt + 1 < tpp) {
+      ++kt;
+    } else if (kli + 1 < pg1) {
+      kt = 0;
+      ++kli;
+      kbase = reinterpret_cast<const char*>(kpool) + head_of(kli) * (size_t)P * D * 2;
+    }
+  };
+  auto issue_v = [&](int buf) {
+    load_v(buf, vbase + (size_t)window(vt) * 2);
+    if (vt + 1 < tpp) {
+      ++vt;
+    } else if (vli + 1 < pg1) {
+      vt = 0;
+      ++vli;
+      vbase = reinterpret_cast<const char*>(vpool) + head_of(vli) * (size_t)D * P * 2;
+    }
+  };
+
+  f32x16 acc[NM];
+#pragma unroll
+  for (int m = 0; m < NM; ++m) acc[m] = f32x16{0};
+  float m_run = -INFINITY, l_run = 0.f;
+  const float c2 = p.scale_log2;
+  const int krow = key_perm(l32);
+
+  // The lane's byte offsets of its MFMA operands within a tile are fixed:
+  // one per d slice (key rows; the second key half is 32 rows further) and
+  // one per 16-key step (value rows; output block m is 32 rows further).
+  uint32_t offk[KK], offv[4];
+#pragma unroll
+  for (int j = 0; j < KK; ++j)
+    offk[j] = (uint32_t)(krow * L::kRowK + (((2 * j + half) ^ swz_k<D>(krow)) << 4));
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks)
+    offv[ks] = (uint32_t)(l32 * L::kRowV + (((2 * ks + half) ^ swz_v(l32)) << 4));
+  auto k_tile = [&](int t) { return smem + (t & 3) * L::kKTile; };
+  auto v_tile = [&](int t) { return smem + L::kVBase + ((t + 4) & 3) * L::kVTile; };
+
+  f32x16 s[2];
+  int tcs = 0;  // tile within its page of the next value phase
+
+  // X(t): the scores of tile t, S^T = K(t) Q^T (two chains, key halves 0 and
+  // 1), key fragments read kAheadX MFMAs ahead.
+  auto score_phase = [&](int t) {
+    constexpr int N = 2 * KK, kAheadX = N < 8 ? N : 8;
+    const uint8_t* kt_l = k_tile(t);
+    u32x4 f[kAheadX];
+#pragma unroll
+    for (int i = 0; i < kAheadX; ++i) f[i] = ld_lds16(kt_l + offk[i >> 1] + (i & 1) * 32 * L::kRowK);
+    s[0] = f32x16{0};
+    s[1] = f32x16{0};
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const u32x4 a = f[i % kAheadX];
+      const int n = i + kAheadX;
+      if (n < N) f[i % kAheadX] = ld_lds16(kt_l + offk[n >> 1] + (n & 1) * 32 * L::kRowK);
+      s[i & 1] = mfma32(a, qf[i >> 1], s[i & 1]);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, kAheadX, 0);
+#pragma unroll
+    for (int i = 0; i < N - kAheadX; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, kAheadX, 0);
+  };
+
+  // Y(t): softmax of the scores of tile t and the value product O^T +=
+  // V(t)^T P(t)^T. Each 16-key group's four value MFMAs (one per 32-row
+  // output block) are issued as soon as its P fragment is packed, so they
+  // run under the exponentials of the next group; value fragments (u = 4 ks
+  // + m) are read eight ahead.
+  auto value_phase = [&](int t) {
+    const uint8_t* vt_l = v_tile(t);
+    constexpr int NV = 4 * NM, kAheadV = NV < 8 ? NV : 8;
+    auto vop = [&](int u) { return ld_lds16(vt_l + offv[u / NM] + (u % NM) * 32 * L::kRowV); };
+    u32x4 f[kAheadV];
+#pragma unroll
+    for (int u = 0; u < kAheadV; ++u) f[u] = vop(u);
+    const int nv = min(kBN, P - tcs * kBN);
+    if (nv < kBN) {
+      asm volatile("" ::: "memory");
+      const int lo = kSmallP ? 0 : kBN - nv, hi = kSmallP ? nv : kBN;
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = 32 * h2 + 16 * (r >> 3) + 8 * half + (r & 7);
+          if (key < lo || key >= hi) s[h2][r] = -INFINITY;
+        }
+    }
+    if (++tcs == tpp) tcs = 0;
+    float mx = fmaxf(s[0][0], s[0][1]);
+#pragma unroll
+    for (int r = 2; r < 16; ++r) mx = fmaxf(mx, s[0][r]);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[1][r]);
+    // Online softmax against a reference max m_run (raw score units) that
+    // only moves when some score exceeds it by more than 8 in exp2 units:
+    // exponentials stay <= 256 and the final normalisation by the row sum
+    // is exact for any reference. The test uses each lane's own 32 scores;
+    // only when it fires are the two lane halves of a query combined.
+    if (__any(mx * c2 > m_run * c2 + 8.f)) {
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const bool grow = mx * c2 > m_run * c2 + 8.f;
+      const float m_new = grow ? mx : m_run;
+      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c2);
+      l_run *= alpha;
+#pragma unroll
+      for (int m = 0; m < NM; ++m) acc[m] *= alpha;
+      m_run = m_new;
+    }
+    const float mc = m_run * c2;
+    float rs[4];  // row sums per 16-key group
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      // keys 16 ks + 8 half + 0..7 of the tile: score registers 8 (ks & 1) +
+      // 0..7 of key half ks >> 1
+      float pv[8];
+#pragma unroll
+      for (int r = 0; r < 8; ++r) pv[r] = __builtin_amdgcn_exp2f(fmaf(s[ks >> 1][8 * (ks & 1) + r], c2, -mc));
+      rs[ks] = ((pv[0] + pv[1]) + (pv[2] + pv[3])) + ((pv[4] + pv[5]) + (pv[6] + pv[7]));
+      const u32x4 pk = u32x4{pack_bf16(pv[0], pv[1]), pack_bf16(pv[2], pv[3]), pack_bf16(pv[4], pv[5]),
+                             pack_bf16(pv[6], pv[7])};
+#pragma unroll
+      for (int m = 0; m < NM; ++m) {
+        const int u = ks * NM + m;
+        const u32x4 a = f[u % kAheadV];
+        if (u + kAheadV < NV) f[u % kAheadV] = vop(u + kAheadV);
+        acc[m] = mfma32(a, pk, acc[m]);
+      }
+    }
+    l_run += (rs[0] + rs[1]) + (rs[2] + rs[3]);
+  };
+
+  if (ntiles > 0) {
+    // prologue: K(0), V(0), K(1), V(1), K(2), V(2), then all of them and the
+    // query fragments (the compiler does not see the copies; the pinned
+    // fragments keep it from waiting for its own loads inside the walk)
+    issue_k(0);
+    issue_v(0);
+    issue_k(1);
+    issue_v(1);
+    issue_k(2);
+    issue_v(2);
+    wait_vmcnt<0>();
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) asm volatile("" : "+v"(qf[kk]));
+    // Slot j opens with a barrier. Waves 0-3 run X(t) in slot 2t and Y(t) in
+    // slot 2t + 1, waves 4-7 X(t) in slot 2t + 1 and Y(t) in slot 2t + 2; so
+    // K(t) is read in slots 2t and 2t + 1 and V(t) in slots 2t + 1 and 2t + 2.
+    // After the barrier of slot 2t every wave issues its share of K(t+3) into
+    // the ring slot of K(t-1), after that of slot 2t + 1 its share of V(t+3)
+    // into that of V(t-1); before the barrier of slot 2t it needs K(t) and
+    // before that of slot 2t + 1 V(t), with five of its loads issued after
+    // either. Both groups make 2 * ntiles + 1 barriers. The barriers are
+    // also hard scheduling boundaries: otherwise the compiler moves
+    // register-only work (exponentials, MFMAs) across them and the two
+    // groups of a SIMD fall back into step.
+    static_assert(L::kInstK == L::kInstV, "one wait count for both rings");
+    constexpr int kWait = 5 * L::kInstK;
+    auto open_slot = [&](bool wait) {
+      __builtin_amdgcn_sched_barrier(0);
+      if (wait) wait_vmcnt<kWait>();
+      lds_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    if (first) {
+      for (int t = 0; t < ntiles; ++t) {
+        open_slot(t > 0);
+        issue_k((t + 3) & 3);
+        score_phase(t);
+        open_slot(true);
+        issue_v((t + 3) & 3);
+        value_phase(t);
+      }
+      open_slot(true);
+      issue_k((ntiles + 3) & 3);
+    } else {
+      open_slot(false);
+      issue_k(3);
+      for (int t = 0; t < ntiles; ++t) {
+        open_slot(true);
+        issue_v((t + 3) & 3);
+        score_phase(t);
+        open_slot(true);
+        issue_k((t + 4) & 3);
+        value_phase(t);
+      }
+    }
+    wait_vmcnt<0>();  // the trailing re-reads
+  }
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float inv_l = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  const float lse = l_tot > 0.f ? m_run * p.sm_scale + __logf(l_tot) : -INFINITY;
+  if (ns > 1) {
+    const size_t cell = ((size_t)b * p.sc.n_part + p.sc.part_base[h] + split) * p.sc.nq32 + qtile * 8 + wave;
+    float* po = p.part_o + cell * (NM * 16 * 64) + lane;
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) po[(m * 16 + r) * 64] = acc[m][r] * inv_l;
+    p.part_lse[cell * 64 + lane] = lse;
+    return;
+  }
+  finish<D, 512>(p, smem, b, h, q_idx, qf, acc, inv_l, lse);
 }
 
 // Merge of the splits of one (head, 128 queries): weights exp(lse_s - max),
@@ -1009,8 +1327,8 @@ hipError_t launch_attention(int dtype, int d, int B, const AttnParams& p, hipStr
         if (small) attn_bf16_kernel<128, true, true, 4><<<grid, 256, 0, s>>>(p);
         else attn_bf16_kernel<128, false, true, 4><<<grid, 256, 0, s>>>(p);
       } else if (p.sc.waves == 8) {
-        if (small) attn_bf16_kernel<128, true, false, 8><<<grid, nt, 0, s>>>(p);
-        else attn_bf16_kernel<128, false, false, 8><<<grid, nt, 0, s>>>(p);
+        if (small) attn_pp_kernel<128, true><<<grid, nt, 0, s>>>(p);
+        else attn_pp_kernel<128, false><<<grid, nt, 0, s>>>(p);
       } else {
         if (small) attn_bf16_kernel<128, true, false, 4><<<grid, nt, 0, s>>>(p);
         else attn_bf16_kernel<128, false, false, 4><<<grid, nt, 0, s>>>(p);
@@ -1020,8 +1338,8 @@ hipError_t launch_attention(int dtype, int d, int B, const AttnParams& p, hipStr
         if (small) attn_bf16_kernel<64, true, true, 4><<<grid, 256, 0, s>>>(p);
         else attn_bf16_kernel<64, false, true, 4><<<grid, 256, 0, s>>>(p);
       } else if (p.sc.waves == 8) {
-        if (small) attn_bf16_kernel<64, true, false, 8><<<grid, nt, 0, s>>>(p);
-        else attn_bf16_kernel<64, false, false, 8><<<grid, nt, 0, s>>>(p);
+        if (small) attn_pp_kernel<64, true><<<grid, nt, 0, s>>>(p);
+        else attn_pp_kernel<64, false><<<grid, nt, 0, s>>>(p);
       } else {
         if (small) attn_bf16_kernel<64, true, false, 4><<<grid, nt, 0, s>>>(p);
         else attn_bf16_kernel<64, false, false, 4><<<grid, nt, 0, s>>>(p);

@@ -58,6 +58,21 @@ __device__ __forceinline__ void g2lds16(const void* gptr, void* lds_wave_base) {
                                    16, 0, 0);
 }
 
+// The same copy issued from inline assembly. hipcc's wait-count pass stops
+// using partial LDS counts (it waits lgkmcnt(0) before every use of an LDS
+// read) as soon as a global_load_lds it knows of is in flight; issued this
+// way the copy is invisible to it, and LDS operand reads can be pipelined
+// with exact lgkmcnt(N) waits. The caller orders the copies itself with
+// wait_vmcnt and a barrier before the data is read. Since the vector-memory
+// counter retires in order, the compiler's own vmcnt waits stay correct
+// (copies it does not count only make them wait longer).
+__device__ __forceinline__ void g2lds16_hidden(const void* gptr, void* lds_wave_base) {
+  const uint32_t la = (uint32_t)(uintptr_t)lds_wave_base;
+  // (one wait state between the write of m0 and the copy that reads it)
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(la)
+               : "memory", "m0");
+}
+
 // s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding).
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
