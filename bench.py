@@ -180,7 +180,7 @@ def bench_single(args, wl):
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
                      "traffic": measured_traffic(wl.name),
-                     "kernel": "attn_bf16_kernel (hsa_forward_selected launch)",
+                     "kernel": "attn_pp_kernel (hsa_forward_selected launch)",
                      "flops_per_launch": fa},
     }
     if not args.no_adaptive:
