@@ -65,6 +65,17 @@ def test_explicit_softmax_scale():
     _run_small(SMALL.replace(seed=16), sm_scale=0.05)
 
 
+@pytest.mark.parametrize("d", [128, 64])
+def test_one_and_two_tile_walks(d):
+    # The page walk's first and last slots: a single 64-key tile (one current
+    # page, no history), two tiles (one selected page), and a page shorter
+    # than a tile, each with a query tile of one query at the end (n_q = 257).
+    base = SMALL.replace(head_dim=d, n_q=257, page_size=64, n_cur=1, seed=17)
+    _run_small(base.replace(n_cand=0, k_h=(0, 0, 0)), k_max=1)
+    _run_small(base.replace(n_cand=2, k_h=(1, 0, 1), seed=18))
+    _run_small(base.replace(page_size=40, n_cand=2, k_h=(1, 2, 0), seed=19))
+
+
 def test_duplicate_pages_tie_to_lower_index():
     wl = SMALL.replace(heads=2, k_h=(1, 2), n_cand=9, seed=17)
 
