@@ -231,9 +231,12 @@ __device__ __forceinline__ void finish(const AttnParams& p, uint8_t* smem, int b
   }
 }
 
-template <int D, bool kSmallP, bool kList, int kW>
+// The tile-list walk (block-sparse mode): each (b, h, 128-query tile) walks
+// its own list of 64-key tiles; waves of a 64-query block that does not
+// keep a tile skip its MFMAs and softmax.
+template <int D, bool kSmallP, int kW>
 __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p) {
-  static_assert(kW == 4, "the 8-wave page walk is attn_pp_kernel");
+  static_assert(kW == 4, "tile lists mark two 64-query blocks per workgroup");
   using L = AttnLayout<D, kW>;
   constexpr int kBM = kWaveQ * kW;
   constexpr int KK = D / 16;   // 16-wide d slices
@@ -270,33 +273,13 @@ __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p
     qtile = local % nqt;
   }
   const int ns = p.sc.n_split[h];
-  const int tpp = (P + kBN - 1) / kBN;
 
-  // ---- key walk. Page mode: the selected pages (up to the first invalid
-  // entry), then the current pages, every page in tiles of 64 keys (a tile
-  // never straddles a page; the last one is partial when 64 does not divide
-  // P). List mode: the (b, h, query tile)'s own list of tiles, each with the
-  // query blocks that attend to it.
-  const int32_t* selrow = p.sel + ((size_t)b * H + h) * p.k_max;
-  const int32_t* ptrow = p.page_table + (size_t)b * p.max_pages;
-  int n_sel = 0;
-  if constexpr (!kList) {
-    while (n_sel < p.k_max) {
-      const int e = ld_const(selrow + n_sel);
-      if (e < 0 || e >= p.max_pages) break;
-      ++n_sel;
-    }
-  }
-  auto head_of = [&](int li) -> size_t {
-    const int lp = li < n_sel ? ld_const(selrow + li) : p.cur_first + (li - n_sel);
-    return (size_t)clampi(ld_const(ptrow + lp), 0, p.num_slots - 1) * H + h;
-  };
-  // This item's share of the walk: split `split` of n_split[h] near-equal
-  // parts (of list_len[h] pages, the last split taking whatever the list
-  // holds beyond the plan; of the tile list in list mode).
-  int pg0 = 0, pg1 = 0, u0 = 0, u1 = 0, ntiles;
-  const int2* lst = nullptr;
-  if constexpr (kList) {
+  // ---- key walk: the (b, h, query tile)'s own list of tiles, each with the
+  // query blocks that attend to it; this item's share is split `split` of
+  // n_split[h] near-equal parts of the list.
+  int u0 = 0, u1, ntiles;
+  const int2* lst;
+  {
     const size_t cell = ((size_t)b * H + h) * nqt + qtile;
     const int len = ld_const(p.blist_len + cell);
     lst = p.blist + cell * p.blist_cap;
@@ -307,15 +290,6 @@ __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p
       u1 = u0 + base + (split < rem ? 1 : 0);
     }
     ntiles = u1 - u0;
-  } else {
-    const int n_list = n_sel + p.n_cur;
-    pg1 = n_list;
-    if (ns > 1) {
-      const int len = p.sc.list_len[h], base = len / ns, rem = len % ns;
-      pg0 = min(n_list, split * base + min(split, rem));
-      pg1 = split == ns - 1 ? n_list : min(n_list, pg0 + base + (split < rem ? 1 : 0));
-    }
-    ntiles = (pg1 - pg0) * tpp;
   }
 
   // ---- Q fragment: lane holds query (l%32) of this wave, d = 16kk + 8*half + 0..7
@@ -358,20 +332,13 @@ __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p
   // extra loads re-read it into ring slots nobody reads, so that every tile
   // issues and waits alike; they are drained before the epilogue.
   auto window = [&](int t) { return kSmallP ? t * kBN : min(t * kBN, P - kBN); };
-  int kli = pg0, kt = 0, vli = pg0, vt = 0;
-  const char* kbase = nullptr;
-  const char* vbase = nullptr;
-  if constexpr (!kList) {
-    kbase = reinterpret_cast<const char*>(kpool) + (pg0 < pg1 ? head_of(pg0) : 0) * (size_t)P * D * 2;
-    vbase = reinterpret_cast<const char*>(vpool) + (pg0 < pg1 ? head_of(pg0) : 0) * (size_t)D * P * 2;
-  }
   auto load_k = [&](int buf, const char* src) {
     uint8_t* dst = smem + buf * L::kKTile + wave * L::kInstK * 1024;
 #pragma unroll
     for (int n = 0; n < L::kInstK; ++n) {
       uint32_t off = k_off[n];
       if constexpr (kSmallP) off -= (uint32_t)(max(0, k_row(n) - (P - 1)) * D * 2);
-      g2lds16(src + off, dst + n * 1024);
+      g2lds16_hidden(src + off, dst + n * 1024);
     }
   };
   auto load_v = [&](int buf, const char* src) {
@@ -380,32 +347,11 @@ __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p
     for (int n = 0; n < L::kInstV; ++n) {
       uint32_t off = v_off[n];
       if constexpr (kSmallP) off -= (uint32_t)(max(0, v_col(n) - (P - 8)) * 2);
-      g2lds16(src + off, dst + n * 1024);
+      g2lds16_hidden(src + off, dst + n * 1024);
     }
   };
-  // page mode: cursors (list position, tile) advance through the pages
-  auto issue_k = [&](int buf) {
-    load_k(buf, kbase + (size_t)window(kt) * D * 2);
-    if (kt + 1 < tpp) {
-      ++kt;
-    } else if (kli + 1 < pg1) {
-      kt = 0;
-      ++kli;
-      kbase = reinterpret_cast<const char*>(kpool) + head_of(kli) * (size_t)P * D * 2;
-    }
-  };
-  auto issue_v = [&](int buf) {
-    load_v(buf, vbase + (size_t)window(vt) * 2);
-    if (vt + 1 < tpp) {
-      ++vt;
-    } else if (vli + 1 < pg1) {
-      vt = 0;
-      ++vli;
-      vbase = reinterpret_cast<const char*>(vpool) + head_of(vli) * (size_t)D * P * 2;
-    }
-  };
-  // list mode: the tile of entry e; entries past the item's range repeat its
-  // last tile (loads into ring slots nobody reads, as in page mode)
+  // the tile of entry e; entries past the item's range repeat its last tile
+  // (loads into ring slots nobody reads)
   auto entry = [&](int u) { return ld_const(lst + min(u, u1 - 1)); };
   auto issue_k_at = [&](int buf, int2 e) {
     load_k(buf, reinterpret_cast<const char*>(kpool) + ((size_t)e.x * P + window(e.y >> 2)) * D * 2);
@@ -421,33 +367,29 @@ __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p
   const float c2 = p.scale_log2;
   const int krow = key_perm(l32);
 
-  // prologue: K(0), V(0), ..., K(S-2), V(S-2), K(S-1) for S = kVStages.
-  // List mode (S = 2) keeps the entries of the tile being computed (ec), of
-  // the next value issue (ev) and of the next key issue (ek) in scalar
-  // registers, read one iteration ahead.
+  // prologue: K(0), V(0), K(1). The entries of the tile being computed (ec),
+  // of the next value issue (ev) and of the next key issue (ek) sit in
+  // scalar registers, read one iteration ahead.
   constexpr int SK = L::kKStages, SV = L::kVStages;
-  static_assert(!kList || SV == 2, "the tile-list walk keeps three entries");
+  static_assert(SV == 2, "the tile-list walk keeps three entries");
   int2 ec = make_int2(0, 0), ev = ec, ek = ec;
   if (ntiles > 0) {
-    if constexpr (kList) {
-      ec = entry(u0);
-      ev = entry(u0 + 1);
-      issue_k_at(0, ec);
-      issue_v_at(0, ec);
-      issue_k_at(1, ev);
-      ek = entry(u0 + 2);
-    } else {
+    ec = entry(u0);
+    ev = entry(u0 + 1);
+    issue_k_at(0, ec);
+    issue_v_at(0, ec);
+    issue_k_at(1, ev);
+    ek = entry(u0 + 2);
+    // the query fragments have landed once the three tile copies alone may
+    // be outstanding; pinned, they keep the compiler (which does not see the
+    // copies) from waiting for its own loads inside the walk
+    wait_vmcnt<2 * L::kInstK + L::kInstV>();
 #pragma unroll
-      for (int i = 0; i < SV - 1; ++i) {
-        issue_k(i);
-        issue_v(i);
-      }
-      issue_k(SV - 1);
-    }
+    for (int kk = 0; kk < KK; ++kk) asm volatile("" : "+v"(qf[kk]));
   }
   // ring slots: kbuf / vbuf of the tile being computed, and of the tiles
   // issued in this iteration (tile + SK - 1 and tile + SV - 1)
-  int t = 0, kbuf = 0, vbuf = 0;
+  int kbuf = 0, vbuf = 0;
   int kbuf_in = SK - 1, vbuf_in = SV - 1;
   for (int tile = 0; tile < ntiles; ++tile) {
     // K(tile) and V(tile) have landed once at most the loads issued after
@@ -455,16 +397,11 @@ __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p
     // iteration
     wait_vmcnt<L::kInstK + (SV - 2) * (L::kInstK + L::kInstV)>();
     lds_barrier();
-    if constexpr (kList) {
-      issue_v_at(vbuf_in, ev);
-      issue_k_at(kbuf_in, ek);
-    } else {
-      issue_v(vbuf_in);
-      issue_k(kbuf_in);
-    }
-    // list mode: waves of a query block that does not keep this tile skip it
-    const int tc = kList ? (ec.y >> 2) : t;
-    const bool active = !kList || ((ec.y >> (wave >> 1)) & 1);
+    issue_v_at(vbuf_in, ev);
+    issue_k_at(kbuf_in, ek);
+    // waves of a query block that does not keep this tile skip it
+    const int tc = ec.y >> 2;
+    const bool active = (ec.y >> (wave >> 1)) & 1;
     if (active) {
       // S^T = K Q^T for the two 32-key halves of the tile: the two MFMA chains
       // alternate, and the key fragments are read from LDS kLdsAhead MFMAs
@@ -555,7 +492,7 @@ __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p
         pipeline_lds_mfma<4 * NM>();
       }
     }
-    if constexpr (kList) {
+    {
       // the key entry of tile + 3, read after this tile's LDS traffic so that
       // the scalar load never shares the LDS counter with the operand reads
       __builtin_amdgcn_sched_barrier(0);
@@ -564,7 +501,6 @@ __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p
       ev = ek;
       ek = en;
     }
-    if (++t == tpp) t = 0;
     kbuf = kbuf == SK - 1 ? 0 : kbuf + 1;
     vbuf = vbuf == SV - 1 ? 0 : vbuf + 1;
     kbuf_in = kbuf_in == SK - 1 ? 0 : kbuf_in + 1;
@@ -1319,30 +1255,24 @@ hipError_t launch_attention(int dtype, int d, int B, const AttnParams& p, hipStr
   if (dtype == HSA_DTYPE_BF16) {
     const dim3 grid(8 * std::max(1, p.sc.xcd_items), B);
     const bool small = p.P < kBN, list = p.blist != nullptr;
-    // tile lists (block-sparse mode) are built per 128-query tile
-    if (list && p.sc.waves != 4) return hipErrorInvalidValue;
-    const int nt = 64 * p.sc.waves;
+    // tile lists (block-sparse mode) are built per 128-query tile and walked
+    // by 4-wave workgroups; the page walk takes 8-wave ones
+    if (p.sc.waves != (list ? 4 : 8)) return hipErrorInvalidValue;
     if (d == 128) {
       if (list) {
-        if (small) attn_bf16_kernel<128, true, true, 4><<<grid, 256, 0, s>>>(p);
-        else attn_bf16_kernel<128, false, true, 4><<<grid, 256, 0, s>>>(p);
-      } else if (p.sc.waves == 8) {
-        if (small) attn_pp_kernel<128, true><<<grid, nt, 0, s>>>(p);
-        else attn_pp_kernel<128, false><<<grid, nt, 0, s>>>(p);
+        if (small) attn_bf16_kernel<128, true, 4><<<grid, 256, 0, s>>>(p);
+        else attn_bf16_kernel<128, false, 4><<<grid, 256, 0, s>>>(p);
       } else {
-        if (small) attn_bf16_kernel<128, true, false, 4><<<grid, nt, 0, s>>>(p);
-        else attn_bf16_kernel<128, false, false, 4><<<grid, nt, 0, s>>>(p);
+        if (small) attn_pp_kernel<128, true><<<grid, 512, 0, s>>>(p);
+        else attn_pp_kernel<128, false><<<grid, 512, 0, s>>>(p);
       }
     } else {
       if (list) {
-        if (small) attn_bf16_kernel<64, true, true, 4><<<grid, 256, 0, s>>>(p);
-        else attn_bf16_kernel<64, false, true, 4><<<grid, 256, 0, s>>>(p);
-      } else if (p.sc.waves == 8) {
-        if (small) attn_pp_kernel<64, true><<<grid, nt, 0, s>>>(p);
-        else attn_pp_kernel<64, false><<<grid, nt, 0, s>>>(p);
+        if (small) attn_bf16_kernel<64, true, 4><<<grid, 256, 0, s>>>(p);
+        else attn_bf16_kernel<64, false, 4><<<grid, 256, 0, s>>>(p);
       } else {
-        if (small) attn_bf16_kernel<64, true, false, 4><<<grid, nt, 0, s>>>(p);
-        else attn_bf16_kernel<64, false, false, 4><<<grid, nt, 0, s>>>(p);
+        if (small) attn_pp_kernel<64, true><<<grid, 512, 0, s>>>(p);
+        else attn_pp_kernel<64, false><<<grid, 512, 0, s>>>(p);
       }
     }
     hipError_t e = hipGetLastError();
