@@ -5,8 +5,9 @@
 // sums (the chunk is 14 MB at 4680 x 12 x 128 bf16, so it is read by many
 // workgroups). The second runs one workgroup per (batch, head): it finishes
 // the mean query in a fixed order, scores the candidates in fp64 and takes
-// the top k_h by repeated block-wide arg-max, comparing (score, -index)
-// lexicographically so equal scores keep the older page.
+// the top k_h by ranking every candidate in the (score desc, index asc)
+// order (repeated block-wide arg-max for very long lists), so equal scores
+// keep the older page.
 #include <float.h>
 
 #include "hsa_device.h"
@@ -34,7 +35,7 @@ __device__ __forceinline__ void load8<float>(const float* p, float (&x)[8]) {
 }
 
 // Column sums of a block of query rows, fp64: ws_qs[b][split][c]. Rows are
-// read eight at a time so that the loads are in flight together; the sum
+// read sixteen at a time so that the loads are in flight together; the sum
 // still runs over the rows in increasing order.
 template <typename T>
 __global__ __launch_bounds__(256) void qsum_kernel(QsumParams p) {
@@ -46,12 +47,12 @@ __global__ __launch_bounds__(256) void qsum_kernel(QsumParams p) {
   for (int vc = threadIdx.x; vc < nvec; vc += blockDim.x) {
     double s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     int r = r0;
-    for (; r + 8 <= r1; r += 8) {
-      float x[8][8];
+    for (; r + 16 <= r1; r += 16) {
+      float x[16][8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) load8<T>(q + (size_t)(r + u) * p.HD + vc * 8, x[u]);
+      for (int u = 0; u < 16; ++u) load8<T>(q + (size_t)(r + u) * p.HD + vc * 8, x[u]);
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
+      for (int u = 0; u < 16; ++u)
 #pragma unroll
         for (int e = 0; e < 8; ++e) s[e] += (double)x[u][e];
     }
@@ -84,24 +85,30 @@ __device__ __forceinline__ Best shfl_xor_best(Best v, int m) {
   return o;
 }
 
+// One 1024-thread workgroup per (batch, head).
+constexpr int kSelThreads = 1024;
+
 template <int D>
-__global__ __launch_bounds__(256) void select_kernel(SelectParams p) {
-  constexpr int DS = D / 16;  // d values per lane when 16 lanes share a candidate
-  __shared__ double qparts[4][D];
+__global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p) {
+  constexpr int NT = kSelThreads, NW = NT / 64;
+  constexpr int DS = D / 16;       // d values per lane when 16 lanes share a candidate
+  constexpr int NPART = NT / D;    // threads per column of the mean query
+  constexpr int SLOTS = NT / 16;   // candidates scored at once
+  constexpr int U = 4;             // candidates per slot with loads in flight together
+  __shared__ double qparts[NPART][D];
   __shared__ double qbar[D];
   __shared__ double score[HSA_MAX_CAND];
   __shared__ uint8_t taken[HSA_MAX_CAND];
-  __shared__ Best wbest[4];
+  __shared__ Best wbest[NW];
   const int bh = blockIdx.x, b = bh / p.H, h = bh % p.H;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
 
-  // mean query of head h: two threads per column each sum half of the splits
-  // (in order), then the halves are added in a fixed order
+  // mean query of head h: NPART threads per column each sum a contiguous
+  // range of the splits (in order), then the parts are added in order
   {
-    const int col = tid % D, part = tid / D;  // D = 128: parts 0, 1; D = 64: 0..3
-    const int nparts = 256 / D;
-    const int per = (p.n_split + nparts - 1) / nparts;
-    const int k0 = part * per, k1 = min(p.n_split, k0 + per);
+    const int col = tid % D, part = tid / D;
+    const int per = (p.n_split + NPART - 1) / NPART;
+    const int k0 = min(p.n_split, part * per), k1 = min(p.n_split, k0 + per);
     const double* src = p.ws_qs + (size_t)b * p.n_split * (p.H * D) + h * D + col;
     double sacc = 0.0;
     int k = k0;
@@ -117,7 +124,7 @@ __global__ __launch_bounds__(256) void select_kernel(SelectParams p) {
     __syncthreads();
     if (tid < D) {
       double t = 0.0;
-      for (int q = 0; q < nparts; ++q) t += qparts[q][tid];
+      for (int q = 0; q < NPART; ++q) t += qparts[q][tid];
       qbar[tid] = t / (double)p.n_q;
     }
     __syncthreads();
@@ -127,18 +134,19 @@ __global__ __launch_bounds__(256) void select_kernel(SelectParams p) {
   const int lo = p.cand_range ? clampi(p.cand_range[2 * b], 0, p.n_cand) : 0;
   const int n_c = p.cand_range ? clampi(p.cand_range[2 * b + 1], lo, p.n_cand) - lo : p.n_cand;
   // scores: 16 lanes per candidate, DS consecutive dims each, reduced in a
-  // fixed butterfly order
+  // fixed butterfly order; U candidates per lane group have their loads in
+  // flight together
   const double* km = p.page_kmean + ((size_t)bh * p.max_pages + lo) * D;
   const int sub = tid & 15;
   double qv[DS];
 #pragma unroll
   for (int e = 0; e < DS; ++e) qv[e] = qbar[sub * DS + e];
   const double rsd = sqrt((double)D);
-  for (int c0 = 0; c0 < n_c; c0 += 16 * 2) {
-    double part[2];
+  for (int c0 = 0; c0 < n_c; c0 += SLOTS * U) {
+    double part[U];
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int c = c0 + u * 16 + (tid >> 4);
+    for (int u = 0; u < U; ++u) {
+      const int c = c0 + u * SLOTS + (tid >> 4);
       part[u] = 0.0;
       if (c < n_c) {
         const double* kr = km + (size_t)c * D + sub * DS;
@@ -147,13 +155,13 @@ __global__ __launch_bounds__(256) void select_kernel(SelectParams p) {
       }
     }
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < U; ++u) {
       double v = part[u];
       v += __shfl_xor(v, 8);
       v += __shfl_xor(v, 4);
       v += __shfl_xor(v, 2);
       v += __shfl_xor(v, 1);
-      const int c = c0 + u * 16 + (tid >> 4);
+      const int c = c0 + u * SLOTS + (tid >> 4);
       if (sub == 0 && c < n_c) {
         score[c] = v / rsd;
         taken[c] = 0;
@@ -165,22 +173,29 @@ __global__ __launch_bounds__(256) void select_kernel(SelectParams p) {
   const int k_eff = min(p.k_h[h], n_c);
   int32_t* sel = p.sel + (size_t)bh * p.k_max;
   double* sc = p.sel_score ? p.sel_score + (size_t)bh * p.k_max : nullptr;
-  for (int r = k_eff + tid; r < p.k_max; r += 256) {
+  for (int r = k_eff + tid; r < p.k_max; r += NT) {
     sel[r] = -1;
     if (sc) sc[r] = 0.0;
   }
   if (k_eff == 0) return;
   if (n_c <= 2048) {
-    // rank of each candidate in the (score desc, index asc) order; ranks are
-    // a permutation for comparable scores (rows start at -1 in case a NaN
-    // score breaks that)
-    for (int r = tid; r < k_eff; r += 256) sel[r] = -1;
+    // rank of each candidate in the (score desc, index asc) order, counted by
+    // G lanes per candidate (each a strided share of the others) and summed
+    // across them; ranks are a permutation for comparable scores (rows start
+    // at -1 in case a NaN score breaks that)
+    for (int r = tid; r < k_eff; r += NT) sel[r] = -1;
     __syncthreads();
-    for (int c = tid; c < n_c; c += 256) {
-      const Best me{score[c], c};
+    int G = 16;
+    while (G > 1 && G * n_c > NT) G >>= 1;
+    const int q = tid & (G - 1);
+    for (int c = tid / G; c - tid / G < n_c; c += NT / G) {  // uniform trip count per lane group
+      const bool mine = c < n_c;
+      const Best me{mine ? score[c] : 0.0, c};
       int rank = 0;
-      for (int o = 0; o < n_c; ++o) rank += before(Best{score[o], o}, me) ? 1 : 0;
-      if (rank < k_eff) {
+      if (mine)
+        for (int o = q; o < n_c; o += G) rank += before(Best{score[o], o}, me) ? 1 : 0;
+      for (int m = 1; m < G; m <<= 1) rank += __shfl_xor(rank, m);
+      if (mine && q == 0 && rank < k_eff) {
         sel[rank] = lo + c;
         if (sc) sc[rank] = me.s;
       }
@@ -191,7 +206,7 @@ __global__ __launch_bounds__(256) void select_kernel(SelectParams p) {
   for (int r = 0; r < k_eff; ++r) {
     Best best{-DBL_MAX, INT32_MAX};
     bool have = false;
-    for (int c = tid; c < n_c; c += 256) {
+    for (int c = tid; c < n_c; c += NT) {
       if (taken[c]) continue;
       const Best cand{score[c], c};
       if (!have || before(cand, best)) { best = cand; have = true; }
@@ -206,7 +221,7 @@ __global__ __launch_bounds__(256) void select_kernel(SelectParams p) {
     __syncthreads();
     if (tid == 0) {
       Best bb = wbest[0];
-      for (int w = 1; w < 4; ++w)
+      for (int w = 1; w < NW; ++w)
         if (wbest[w].i < n_c && (bb.i >= n_c || before(wbest[w], bb))) bb = wbest[w];
       // a NaN score can leave no comparable candidate: pad instead of indexing
       const bool ok = bb.i >= 0 && bb.i < n_c;
@@ -296,8 +311,8 @@ hipError_t launch_page_select(int dtype, int d, int B, const QsumParams& qp,
   hipError_t e = launch_qsum(dtype, B, qp, s);
   if (e != hipSuccess) return e;
   const dim3 g2(B * sp.H);
-  if (d == 128) select_kernel<128><<<g2, 256, 0, s>>>(sp);
-  else select_kernel<64><<<g2, 256, 0, s>>>(sp);
+  if (d == 128) select_kernel<128><<<g2, kSelThreads, 0, s>>>(sp);
+  else select_kernel<64><<<g2, kSelThreads, 0, s>>>(sp);
   return hipGetLastError();
 }
 
