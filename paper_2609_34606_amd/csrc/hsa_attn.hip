@@ -513,13 +513,16 @@ __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p
   const float lse = l_tot > 0.f ? m_run * p.sm_scale + __logf(l_tot) : -INFINITY;
   if (ns > 1) {
     // partial result of this split: normalised output and log-sum-exp, in the
-    // accumulator register layout (register-major, lane fastest: coalesced)
+    // accumulator register layout (four registers of a lane contiguous, then
+    // lanes, then register groups: 16-byte accesses, coalesced)
     const size_t cell = ((size_t)b * p.sc.n_part + p.sc.part_base[h] + split) * p.sc.nq32 + qtile * kW + wave;
-    float* po = p.part_o + cell * (NM * 16 * 64) + lane;
+    f32x4* po = reinterpret_cast<f32x4*>(p.part_o + cell * (NM * 16 * 64)) + lane;
 #pragma unroll
     for (int m = 0; m < NM; ++m)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) po[(m * 16 + r) * 64] = acc[m][r] * inv_l;
+      for (int g = 0; g < 4; ++g)
+        po[(m * 4 + g) * 64] = f32x4{acc[m][4 * g] * inv_l, acc[m][4 * g + 1] * inv_l,
+                                     acc[m][4 * g + 2] * inv_l, acc[m][4 * g + 3] * inv_l};
     p.part_lse[cell * 64 + lane] = lse;
     return;
   }
@@ -849,12 +852,15 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
   const float inv_l = l_tot > 0.f ? 1.f / l_tot : 0.f;
   const float lse = l_tot > 0.f ? m_run * p.sm_scale + __logf(l_tot) : -INFINITY;
   if (ns > 1) {
+    // partial result of this split (layout as in the tile-list walk)
     const size_t cell = ((size_t)b * p.sc.n_part + p.sc.part_base[h] + split) * p.sc.nq32 + qtile * 8 + wave;
-    float* po = p.part_o + cell * (NM * 16 * 64) + lane;
+    f32x4* po = reinterpret_cast<f32x4*>(p.part_o + cell * (NM * 16 * 64)) + lane;
 #pragma unroll
     for (int m = 0; m < NM; ++m)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) po[(m * 16 + r) * 64] = acc[m][r] * inv_l;
+      for (int g = 0; g < 4; ++g)
+        po[(m * 4 + g) * 64] = f32x4{acc[m][4 * g] * inv_l, acc[m][4 * g + 1] * inv_l,
+                                     acc[m][4 * g + 2] * inv_l, acc[m][4 * g + 3] * inv_l};
     p.part_lse[cell * 64 + lane] = lse;
     return;
   }
@@ -889,11 +895,17 @@ __global__ __launch_bounds__(256, 2) void combine_bf16_kernel(AttnParams p) {
     const float ls = p.part_lse[cell * 64 + lane];
     const float w = ls == -INFINITY ? 0.f : __expf(ls - lmax);
     wsum += w;
-    const float* po = p.part_o + cell * (NM * 16 * 64) + lane;
+    const f32x4* po = reinterpret_cast<const f32x4*>(p.part_o + cell * (NM * 16 * 64)) + lane;
 #pragma unroll
     for (int m = 0; m < NM; ++m)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[m][r] = fmaf(w, po[(m * 16 + r) * 64], acc[m][r]);
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 x = po[(m * 4 + g) * 64];
+        acc[m][4 * g] = fmaf(w, x.x, acc[m][4 * g]);
+        acc[m][4 * g + 1] = fmaf(w, x.y, acc[m][4 * g + 1]);
+        acc[m][4 * g + 2] = fmaf(w, x.z, acc[m][4 * g + 2]);
+        acc[m][4 * g + 3] = fmaf(w, x.w, acc[m][4 * g + 3]);
+      }
   }
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
   const float lse = wsum > 0.f ? lmax + __logf(wsum) : -INFINITY;

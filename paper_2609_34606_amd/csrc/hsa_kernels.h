@@ -198,7 +198,7 @@ struct AttnParams {
   // sparse mode
   float* o_sp;              // [B, n_q, H, d]
   float* lse;               // [B, H, n_q] nullable
-  float* part_o;                         // [B, n_part, nq32, 16*d/32 regs, 64 lanes]
+  float* part_o;                         // [B, n_part, nq32, d/32 x 4 register groups, 64 lanes, 4 regs]
   float* part_lse;                       // [B, n_part, nq32, 64 lanes]
   // block-sparse mode (blist != NULL): each (b, h, query tile) walks its own
   // list of 64-key tiles, entry {slot * H + h, (tile index << 2) | mask}; mask
