@@ -235,11 +235,48 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p) {
 
 // Stage-1 prompt-level retrieval (Sec. 3.2): one workgroup of 16 waves per
 // batch entry. Each wave takes every sixteenth chunk: fp64 dot product and
-// norm over the embedding dimension (each lane keeps four partial sums over
-// its strided elements, added in a fixed order, then a fixed butterfly
+// norm over the embedding dimension (each lane keeps eight partial sums
+// over its elements, added in a fixed pairwise order, then a fixed butterfly
 // across the wave), cosine = dot / (|p| |c|), 0 for a zero norm; then the
 // top-1 by (cosine desc, index asc) over the workgroup.
 constexpr int kChunkWaves = 16;
+
+// Per-lane partial sums of a.b and a.a over E elements: a lane reads VW
+// consecutive floats per access (VW = 4: 16-byte loads) and issues U accesses
+// of each array per round before using them (the pass is latency-bound: one
+// workgroup streams every chunk embedding of its batch entry); the products
+// of a round go to eight fp64 partials in a fixed order.
+template <int VW>
+__device__ __forceinline__ void dot_norm(const float* a, const float* bv, int E, int lane,
+                                         double (&dot)[8], double (&na)[8]) {
+  constexpr int U = VW == 4 ? 4 : 8;
+  const int n = E / VW;
+  for (int g0 = lane; g0 < n; g0 += 64 * U) {
+    float x[U][VW], y[U][VW];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int g = g0 + 64 * u;
+      const bool in = g < n;
+      if constexpr (VW == 4) {
+        const float4 xa = in ? reinterpret_cast<const float4*>(a)[g] : float4{0.f, 0.f, 0.f, 0.f};
+        const float4 ya = in ? reinterpret_cast<const float4*>(bv)[g] : float4{0.f, 0.f, 0.f, 0.f};
+        x[u][0] = xa.x; x[u][1] = xa.y; x[u][2] = xa.z; x[u][3] = xa.w;
+        y[u][0] = ya.x; y[u][1] = ya.y; y[u][2] = ya.z; y[u][3] = ya.w;
+      } else {
+        x[u][0] = in ? a[g] : 0.f;
+        y[u][0] = in ? bv[g] : 0.f;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int e = 0; e < VW; ++e) {
+        const int k = (u * VW + e) & 7;
+        dot[k] = fma((double)x[u][e], (double)y[u][e], dot[k]);
+        na[k] = fma((double)x[u][e], (double)x[u][e], na[k]);
+      }
+  }
+}
 
 __global__ __launch_bounds__(64 * kChunkWaves) void chunk_select_kernel(ChunkSelectParams p) {
   __shared__ Best wbest[kChunkWaves];
@@ -250,28 +287,25 @@ __global__ __launch_bounds__(64 * kChunkWaves) void chunk_select_kernel(ChunkSel
     for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
     return v;
   };
-  double pa[4] = {0, 0, 0, 0};
-  for (int e = lane; e < p.E; e += 256)
+  auto lane_sum = [](const double (&a)[8]) {
+    return ((a[0] + a[4]) + (a[2] + a[6])) + ((a[1] + a[5]) + (a[3] + a[7]));
+  };
+  // 16-byte loads when every row starts 16-byte aligned
+  const bool vec = (p.E & 3) == 0 && ((uintptr_t)p.prompt & 15) == 0 && ((uintptr_t)p.chunks & 15) == 0;
+  auto sums = [&](const float* x, double (&dot)[8], double (&na)[8]) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (e + 64 * u < p.E) pa[u] = fma((double)pr[e + 64 * u], (double)pr[e + 64 * u], pa[u]);
-  const double pn = wave_sum((pa[0] + pa[1]) + (pa[2] + pa[3]));
+    for (int k = 0; k < 8; ++k) dot[k] = na[k] = 0.0;
+    if (vec) dot_norm<4>(x, pr, p.E, lane, dot, na);
+    else dot_norm<1>(x, pr, p.E, lane, dot, na);
+  };
+  double d8[8], n8[8];
+  sums(pr, d8, n8);
+  const double pn = wave_sum(lane_sum(n8));
   Best best{-DBL_MAX, INT32_MAX};
   for (int c = wave; c < p.M; c += kChunkWaves) {
-    const float* cr = p.chunks + ((size_t)b * p.M + c) * p.E;
-    double dot[4] = {0, 0, 0, 0}, cn[4] = {0, 0, 0, 0};
-    for (int e = lane; e < p.E; e += 256)
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int i = e + 64 * u;
-        if (i < p.E) {
-          const double x = (double)cr[i];
-          dot[u] = fma(x, (double)pr[i], dot[u]);
-          cn[u] = fma(x, x, cn[u]);
-        }
-      }
-    const double dt = wave_sum((dot[0] + dot[1]) + (dot[2] + dot[3]));
-    const double cc = wave_sum((cn[0] + cn[1]) + (cn[2] + cn[3]));
+    sums(p.chunks + ((size_t)b * p.M + c) * p.E, d8, n8);
+    const double dt = wave_sum(lane_sum(d8));
+    const double cc = wave_sum(lane_sum(n8));
     const double den = sqrt(cc) * sqrt(pn);
     const Best cand{den > 0.0 ? dt / den : 0.0, c};
     if (best.i == INT32_MAX || before(cand, best)) best = cand;

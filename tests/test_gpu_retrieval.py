@@ -92,6 +92,14 @@ def test_tied_chunks_pick_the_lower_index():
     assert ref["chunk"][0] == 1
 
 
+@pytest.mark.parametrize("emb_dim", [1000, 2102])
+def test_many_chunks_ragged_embedding(emb_dim):
+    # 40 one-page chunks (more than one per wave of the Stage-1 workgroup)
+    # and embedding sizes that end inside a round of a lane's loads (1000:
+    # 16-byte loads, 2102: 4-byte loads)
+    _small(SMALL.replace(page_size=64, n_cand=40, n_cur=1, k_h=(1, 0, 1), seed=83), emb_dim=emb_dim)
+
+
 def test_c4_prompt_switch_full_size():
     import torch
     from synth_inputs import make_case_torch
