@@ -107,12 +107,18 @@ def sigmoid(g: np.ndarray) -> np.ndarray:
 def gated_merge(o_lin, o_sp, g_lin=None, g_sp=None):
     """O = O_lin * sigmoid(G_lin) + O_sp * sigmoid(G_sp) (Sec. 3.3, gated fusion).
 
-    Gates are per query and head (broadcast over the head dimension); absent
-    gates mean logit 0, i.e. weight 1/2 each.
+    The paper leaves the gate shape open (head-level gates, yet an
+    element-wise product with the branch outputs). A gate array with one axis
+    fewer than the outputs is per query and head and broadcast over the head
+    dimension; one with the outputs' shape is element-wise. Absent gates mean
+    logit 0, i.e. weight 1/2 each.
     """
-    wl = 0.5 if g_lin is None else sigmoid(g_lin)[..., None]
-    ws = 0.5 if g_sp is None else sigmoid(g_sp)[..., None]
-    return wl * o_lin + ws * o_sp
+    def weight(g):
+        if g is None:
+            return 0.5
+        w = sigmoid(g)
+        return w if w.ndim == np.ndim(o_lin) else w[..., None]
+    return weight(g_lin) * o_lin + weight(g_sp) * o_sp
 
 
 # --------------------------------------------------------------------------

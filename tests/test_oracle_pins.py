@@ -168,6 +168,38 @@ def test_sigmoid_and_gate_limits():
     np.testing.assert_allclose(O.gated_merge(a, b), 0.5 * (a + b), rtol=1e-15)
 
 
+def test_elementwise_gate_limits_pick_a_branch_per_element():
+    # element-wise gates (the outputs' shape): a per-element choice of branch
+    # in the saturated limit, and a gate constant over the last axis equals
+    # the per-(query, head) gate
+    a, b = rng0.standard_normal((4, 3, 5)), rng0.standard_normal((4, 3, 5))
+    mask = rng0.random((4, 3, 5)) < 0.5
+    g = np.where(mask, 40.0, -40.0)
+    np.testing.assert_allclose(O.gated_merge(a, b, g, -g), np.where(mask, a, b), atol=1e-15)
+    gh = rng0.standard_normal((4, 3))
+    ge = np.repeat(gh[..., None], 5, axis=-1)
+    np.testing.assert_array_equal(O.gated_merge(a, b, ge, -ge), O.gated_merge(a, b, gh, -gh))
+
+
+def test_forward_with_elementwise_gates_picks_branches_per_element():
+    wl = small_wl(gates=True)
+    case = make_case(wl)
+    d = wl.head_dim
+    mask = np.random.default_rng(5).random(case.g_lin.shape + (d,)) < 0.5
+    g = np.where(mask, 40.0, -40.0).astype(np.float32)
+    out = O.hsa_forward(case.q, case.k_pool, case.v_pool, case.page_table, wl.n_cand, wl.n_cur,
+                        list(case.k_h), g, -g)
+    np.testing.assert_allclose(out["O"], np.where(mask, out["O_lin"], out["O_sp"]), atol=1e-14)
+    # constant over d: the head-wise result
+    ge = np.repeat(case.g_lin[..., None], d, axis=-1)
+    se = np.repeat(case.g_sp[..., None], d, axis=-1)
+    e = O.hsa_forward(case.q, case.k_pool, case.v_pool, case.page_table, wl.n_cand, wl.n_cur,
+                      list(case.k_h), ge, se)
+    h = O.hsa_forward(case.q, case.k_pool, case.v_pool, case.page_table, wl.n_cand, wl.n_cur,
+                      list(case.k_h), case.g_lin, case.g_sp)
+    np.testing.assert_array_equal(e["O"], h["O"])
+
+
 # ---------------------------------------------------------------- whole pass
 def test_full_budget_equals_dense_attention_over_all_pages():
     wl = small_wl(k_h=(6, 9, 100))
