@@ -41,7 +41,8 @@
  *   kv_state     [B, H, d, d] fp32      kv_state[b][h][j][i] = sum_t phi(k_t)[i] v_t[j]
  *   k_state      [B, H, d] fp32         k_state[b][h][i]     = sum_t phi(k_t)[i]
  *   page_kmean   [B, H, max_pages, d] fp64  mean key of each page
- *   g_lin, g_sp  [B, n_q, H] fp32       gate logits (nullable: logit 0)
+ *   g_lin, g_sp  [B, n_q, H] fp32       gate logits (nullable: logit 0), or
+ *                [B, n_q, H, d] fp32    with cfg->gate_dims == d (element-wise)
  *   sel          [B, H, k_max] int32    selected logical pages, -1 padded
  */
 #ifndef HSA_H_
@@ -87,6 +88,11 @@ typedef struct hsa_config {
   int32_t page_size; /* P >= 8, P % 8 == 0 */
   int32_t dtype;     /* hsa_dtype_t of q, k, v, o */
   float sm_scale;    /* softmax scale; 0 means 1/sqrt(d) (App. A.1 eq. attention) */
+  int32_t gate_dims; /* gate logits per element of a head's output row: 0 or 1 means
+                        one logit per (query, head) broadcast over d; head_dim means
+                        one per (query, head, dim) (Sec. 3.3 "Gated fusion" describes
+                        head-level gates applied element-wise); other values are
+                        INVALID_ARG */
 } hsa_config_t;
 
 typedef struct hsa_kv_pool {
@@ -197,7 +203,8 @@ hsa_status_t hsa_sparse_attn(const hsa_config_t* cfg, const void* q, int32_t n_q
  *   3. linear branch from the running state:
  *        O_lin[i] = (sum_a phi(q_i)[a] kv_state[j][a]) / (phi(q_i) . k_state);
  *   4. gated fusion (Sec. 3.3): o = sigmoid(g_lin) O_lin + sigmoid(g_sp) O_sp,
- *      gates broadcast over d; a NULL gate array means logit 0 (weight 1/2).
+ *      gates broadcast over d (element-wise when cfg->gate_dims == d); a NULL
+ *      gate array means logit 0 (weight 1/2).
  * The state and page index must already cover the pages (hsa_state_update
  * over [0, n_cand + n_cur_pages) or its streaming equivalent).
  *

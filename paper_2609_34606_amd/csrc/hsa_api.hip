@@ -36,6 +36,8 @@ hsa_status_t check_cfg(const hsa_config_t* c) {
   if (c->head_dim != 64 && c->head_dim != 128) return HSA_ERR_UNSUPPORTED;
   if (c->page_size < 8 || c->page_size % 8 != 0) return HSA_ERR_UNSUPPORTED;
   if (!(c->sm_scale >= 0.f) || isinf(c->sm_scale)) return HSA_ERR_INVALID_ARG;
+  if (c->gate_dims != 0 && c->gate_dims != 1 && c->gate_dims != c->head_dim)
+    return HSA_ERR_INVALID_ARG;
   return HSA_OK;
 }
 
@@ -671,6 +673,7 @@ hsa_status_t run_attend(const hsa_config_t* cfg, const void* q, int32_t n_q,
   p.k_state = k_state;
   p.g_lin = g_lin;
   p.g_sp = g_sp;
+  p.gate_elem = cfg->gate_dims > 1;
   p.o = o;
   int list_len[HSA_MAX_HEADS];
   for (int h = 0; h < cfg->num_heads; ++h) list_len[h] = std::min(k_h[h], n_cand) + n_cur_pages;

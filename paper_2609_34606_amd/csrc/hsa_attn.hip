@@ -92,13 +92,19 @@ __device__ __forceinline__ int key_perm(int m) {
   return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1);
 }
 
+// Gate weight sigmoid(g[i]); a missing gate array means logit 0 (weight 1/2).
+__device__ __forceinline__ float gate_w(const float* g, size_t i) {
+  return g ? 1.f / (1.f + __expf(-g[i])) : 0.5f;
+}
+
 // Output of one (head, 128-query tile) from its normalised sparse-branch
 // accumulators (acc * inv_l; lane holds query l%32, dims 32m + 8(r/4) +
 // 4(l/32) + r%4) and log-sum-exp. Sparse mode writes O_sp and the LSE;
 // final mode adds the linear branch and the gated fusion:
 //   O_lin^T = S^T phi(Q)^T / (phi(Q) . z), the state split into bf16 hi + lo
 //   parts (~16 bits kept) and staged through LDS in two halves of its rows;
-//   o = sigmoid(g_lin) O_lin + sigmoid(g_sp) O_sp, rounded to bf16.
+//   o = sigmoid(g_lin) O_lin + sigmoid(g_sp) O_sp, rounded to bf16, with one
+//   gate logit per (query, head) or, with gate_elem, per (query, head, dim).
 // Every thread of the workgroup must call it (it synchronises).
 template <int D, int NT>
 __device__ __forceinline__ void finish(const AttnParams& p, uint8_t* smem, int b, int h, int q_idx,
@@ -129,8 +135,8 @@ __device__ __forceinline__ void finish(const AttnParams& p, uint8_t* smem, int b
     // linear branch from another launch (Linformer): gated sum only
     if (q_ok) {
       const size_t gi = ((size_t)b * p.n_q + q_idx) * H + h;
-      const float wl = p.g_lin ? 1.f / (1.f + __expf(-p.g_lin[gi])) : 0.5f;
-      const float wsp = p.g_sp ? 1.f / (1.f + __expf(-p.g_sp[gi])) : 0.5f;
+      const float wl = p.gate_elem ? 0.f : gate_w(p.g_lin, gi);
+      const float wsp = p.gate_elem ? 0.f : gate_w(p.g_sp, gi);
       const float a_sp = wsp * inv_l;
       const float* lrow = p.o_lin + gi * D;
       uint16_t* orow = static_cast<uint16_t*>(p.o) + gi * D;
@@ -141,8 +147,15 @@ __device__ __forceinline__ void finish(const AttnParams& p, uint8_t* smem, int b
           const int d0 = 32 * m + 8 * g + 4 * half;
           const f32x4 l = *reinterpret_cast<const f32x4*>(lrow + d0);
           float v[4];
+          if (p.gate_elem) {
 #pragma unroll
-          for (int q2 = 0; q2 < 4; ++q2) v[q2] = wl * l[q2] + a_sp * acc[m][4 * g + q2];
+            for (int q2 = 0; q2 < 4; ++q2)
+              v[q2] = gate_w(p.g_lin, gi * D + d0 + q2) * l[q2] +
+                      gate_w(p.g_sp, gi * D + d0 + q2) * inv_l * acc[m][4 * g + q2];
+          } else {
+#pragma unroll
+            for (int q2 = 0; q2 < 4; ++q2) v[q2] = wl * l[q2] + a_sp * acc[m][4 * g + q2];
+          }
           *reinterpret_cast<u32x2*>(orow + d0) = u32x2{pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
         }
     }
@@ -190,11 +203,11 @@ __device__ __forceinline__ void finish(const AttnParams& p, uint8_t* smem, int b
   }
   den += __shfl_xor(den, 32);
   const float inv_den = 1.f / den;
+  const size_t gi = ((size_t)b * p.n_q + q_idx) * H + h;
   float wl = 0.5f, wsp = 0.5f;
-  if (q_ok) {
-    const size_t gi = ((size_t)b * p.n_q + q_idx) * H + h;
-    if (p.g_lin) wl = 1.f / (1.f + __expf(-p.g_lin[gi]));
-    if (p.g_sp) wsp = 1.f / (1.f + __expf(-p.g_sp[gi]));
+  if (q_ok && !p.gate_elem) {
+    wl = gate_w(p.g_lin, gi);
+    wsp = gate_w(p.g_sp, gi);
   }
   const float a_lin = wl * inv_den, a_sp = wsp * inv_l;
   uint16_t* orow = q_ok ? static_cast<uint16_t*>(p.o) + (((size_t)b * p.n_q + q_idx) * H + h) * D
@@ -222,8 +235,15 @@ __device__ __forceinline__ void finish(const AttnParams& p, uint8_t* smem, int b
         for (int g = 0; g < 4; ++g) {
           const int d0 = 32 * m + 8 * g + 4 * half;
           float v[4];
+          if (p.gate_elem) {
 #pragma unroll
-          for (int q2 = 0; q2 < 4; ++q2) v[q2] = a_lin * al[4 * g + q2] + a_sp * acc[m][4 * g + q2];
+            for (int q2 = 0; q2 < 4; ++q2)
+              v[q2] = gate_w(p.g_lin, gi * D + d0 + q2) * inv_den * al[4 * g + q2] +
+                      gate_w(p.g_sp, gi * D + d0 + q2) * inv_l * acc[m][4 * g + q2];
+          } else {
+#pragma unroll
+            for (int q2 = 0; q2 < 4; ++q2) v[q2] = a_lin * al[4 * g + q2] + a_sp * acc[m][4 * g + q2];
+          }
           *reinterpret_cast<u32x2*>(orow + d0) = u32x2{pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
         }
       }
@@ -1021,13 +1041,17 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
     return;
   }
   const size_t gi = ((size_t)b * p.n_q + qi) * H + h;
-  const float wl = p.g_lin ? 1.f / (1.f + expf(-p.g_lin[gi])) : 0.5f;
-  const float wsp = p.g_sp ? 1.f / (1.f + expf(-p.g_sp[gi])) : 0.5f;
+  // gate weights of element e of this thread's part of the row
+  auto sig = [](const float* g, size_t i) { return g ? 1.f / (1.f + expf(-g[i])) : 0.5f; };
+  const float wl_h = p.gate_elem ? 0.f : sig(p.g_lin, gi);
+  const float wsp_h = p.gate_elem ? 0.f : sig(p.g_sp, gi);
+  auto wl = [&](int e) { return p.gate_elem ? sig(p.g_lin, gi * D + part * DP + e) : wl_h; };
+  auto wsp = [&](int e) { return p.gate_elem ? sig(p.g_sp, gi * D + part * DP + e) : wsp_h; };
   float* orow = static_cast<float*>(p.o) + gi * D + part * DP;
   if (p.o_lin) {
     // linear branch from another launch (Linformer): gated sum only
     const float* lrow = p.o_lin + gi * D + part * DP;
-    for (int e = 0; e < DP; ++e) orow[e] = wl * lrow[e] + wsp * acc[e] * inv_l;
+    for (int e = 0; e < DP; ++e) orow[e] = wl(e) * lrow[e] + wsp(e) * acc[e] * inv_l;
     return;
   }
   const float* st = p.kv_state + ((size_t)b * H + h) * D * D;
@@ -1038,7 +1062,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
     const int j = part * DP + e;
     float num = 0.f;
     for (int i = 0; i < D; ++i) num = fmaf(phi(qs[qr][i]), st[(size_t)j * D + i], num);
-    orow[e] = wl * (num / den) + wsp * acc[e] * inv_l;
+    orow[e] = wl(e) * (num / den) + wsp(e) * acc[e] * inv_l;
   }
 }
 

@@ -190,8 +190,9 @@ struct AttnParams {
   // final mode
   const float* kv_state;    // [B, H, d, d]
   const float* k_state;     // [B, H, d]
-  const float* g_lin;       // [B, n_q, H] nullable
+  const float* g_lin;       // [B, n_q, H] nullable, [B, n_q, H, d] with gate_elem
   const float* g_sp;
+  int gate_elem;            // gates per (query, head, dim) instead of per (query, head)
   void* o;                  // [B, n_q, H, d] dtype
   const float* o_lin;       // [B, n_q, H, d] fp32 linear-branch output of another
                             // launch; NULL: the kernelised branch from the state

@@ -26,7 +26,8 @@ c_i32, c_vp, c_sz = ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t
 
 class HsaConfig(ctypes.Structure):
     _fields_ = [("batch", c_i32), ("num_heads", c_i32), ("head_dim", c_i32),
-                ("page_size", c_i32), ("dtype", c_i32), ("sm_scale", ctypes.c_float)]
+                ("page_size", c_i32), ("dtype", c_i32), ("sm_scale", ctypes.c_float),
+                ("gate_dims", c_i32)]
 
 
 class HsaTierStats(ctypes.Structure):
@@ -183,10 +184,12 @@ def _workspace(nbytes: int, device):
 
 
 def config(batch: int, num_heads: int, head_dim: int, page_size: int, dtype,
-           sm_scale: float = 0.0) -> HsaConfig:
+           sm_scale: float = 0.0, gate_dims: int = 0) -> HsaConfig:
+    """gate_dims: 0 for gate logits per (query, head), head_dim for logits per
+    (query, head, dim)."""
     if not isinstance(dtype, int):
         dtype = HSA_DTYPE_BF16 if str(dtype).endswith("bfloat16") or dtype == "bf16" else HSA_DTYPE_F32
-    return HsaConfig(batch, num_heads, head_dim, page_size, dtype, sm_scale)
+    return HsaConfig(batch, num_heads, head_dim, page_size, dtype, sm_scale, gate_dims)
 
 
 def kv_pool(k_pool, v_pool, page_table) -> HsaKvPool:

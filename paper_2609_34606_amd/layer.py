@@ -11,17 +11,19 @@ class HsaLayer:
 
     Shapes follow include/hsa.h: k_pool [slots,H,P,d], v_pool [slots,H,d,P],
     page_table [B,max_pages], kv_state [B,H,d,d], k_state [B,H,d],
-    page_kmean [B,H,max_pages,d].
+    page_kmean [B,H,max_pages,d]; gate logits [B,n_q,H], or [B,n_q,H,d] with
+    gate_dims = d.
     """
 
     def __init__(self, batch: int, heads: int, head_dim: int, page_size: int,
                  dtype, device, k_pool=None, v_pool=None, page_table=None,
-                 num_slots: int = 0, max_pages: int = 0, sm_scale: float = 0.0):
+                 num_slots: int = 0, max_pages: int = 0, sm_scale: float = 0.0,
+                 gate_dims: int = 0):
         import torch
         self.torch = torch
         self.device = torch.device(device)
         self.dtype = dtype
-        self.cfg = _h.config(batch, heads, head_dim, page_size, dtype, sm_scale)
+        self.cfg = _h.config(batch, heads, head_dim, page_size, dtype, sm_scale, gate_dims)
         if k_pool is None:
             k_pool = torch.empty((num_slots, heads, page_size, head_dim), dtype=dtype, device=device)
             v_pool = torch.empty((num_slots, heads, head_dim, page_size), dtype=dtype, device=device)

@@ -62,6 +62,24 @@ def to_host(x):
     return x.cpu().numpy()
 
 
+def gate_dims_of(dev: Dict) -> int:
+    """head_dim when the case carries element-wise gate logits [B, n_q, H, d],
+    else 0 (one logit per query and head)."""
+    for k in ("g_lin", "g_sp"):
+        g = dev.get(k)
+        if g is not None and g.dim() == 4:
+            return int(g.shape[-1])
+    return 0
+
+
+def elementwise_gates(case, seed=23):
+    """Replace a case's gate logits by seeded N(0,1) logits per output element."""
+    r = np.random.default_rng(seed)
+    B, n_q, H, d = case.q.shape
+    case.g_lin = r.standard_normal((B, n_q, H, d)).astype(np.float32)
+    case.g_sp = r.standard_normal((B, n_q, H, d)).astype(np.float32)
+
+
 def run_library(wl, dev: Dict, k_h: Sequence[int], k_max: Optional[int] = None,
                 sm_scale: float = 0.0, with_parts: bool = True):
     """Cold state over every page, then the full forward; optionally also the
@@ -73,7 +91,7 @@ def run_library(wl, dev: Dict, k_h: Sequence[int], k_max: Optional[int] = None,
     k_max = max(1, max(k_h)) if k_max is None else k_max
     layer = HsaLayer(B, H, d, wl.page_size, dev["q"].dtype, dev["q"].device,
                      k_pool=dev["k_pool"], v_pool=dev["v_pool"], page_table=dev["page_table"],
-                     sm_scale=sm_scale)
+                     sm_scale=sm_scale, gate_dims=gate_dims_of(dev))
     layer.fold(0, wl.n_cand + wl.n_cur)
     sel = torch.full((B, H, k_max), -7, dtype=torch.int32, device=dev["q"].device)
     o = layer.forward(dev["q"], wl.n_cand, wl.n_cur, list(k_h), k_max=k_max,

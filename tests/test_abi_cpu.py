@@ -96,6 +96,11 @@ def test_validation_errors_without_launch():
     # negative scale
     neg = P.config(1, 2, 64, 256, "f32", sm_scale=-1.0)
     assert lib.hsa_state_update(by(neg), by(pool), 0, 1, fake, fake, fake, None, 0, None) == 1
+    # gate shape: one logit per (query, head) (0 or 1) or per element (head_dim)
+    for gd, want in ((1, 0), (64, 0), (5, 1), (128, 1), (-1, 1)):
+        g = P.config(1, 2, 64, 256, "f32", gate_dims=gd)
+        assert lib.hsa_state_update(by(g), by(pool), 0, 2, fake, fake, fake, None, 0, None) == (
+            4 if want == 0 else 1), gd
 
 
 def test_adaptive_entry_points_validate_before_launch():

@@ -15,7 +15,7 @@ import pytest
 from synth_inputs import WORKLOADS, make_case
 from synth_inputs.configs import Workload
 
-from hsa_testlib import BF16_TOL, F32_TOL, assert_close, say, to_host, upload
+from hsa_testlib import BF16_TOL, F32_TOL, assert_close, elementwise_gates, gate_dims_of, say, to_host, upload
 from oracle import hsa_blocks_oracle as BO
 
 pytestmark = pytest.mark.gpu
@@ -34,7 +34,8 @@ def run_library(wl, dev, k_h, tau_min=BO.TAU_MIN, tau_max=BO.TAU_MAX, k_max=None
     k_max = max(1, max(k_h)) if k_max is None else k_max
     cuda = dev["q"].device
     layer = HsaLayer(B, H, d, wl.page_size, dev["q"].dtype, cuda, k_pool=dev["k_pool"],
-                     v_pool=dev["v_pool"], page_table=dev["page_table"], sm_scale=sm_scale)
+                     v_pool=dev["v_pool"], page_table=dev["page_table"], sm_scale=sm_scale,
+                     gate_dims=gate_dims_of(dev))
     layer.fold(0, wl.n_cand + wl.n_cur)
     sel = torch.full((B, H, k_max), -7, dtype=torch.int32, device=cuda)
     o = layer.forward_adaptive(dev["q"], wl.n_cand, wl.n_cur, list(k_h), k_max=k_max,
@@ -128,6 +129,11 @@ def test_small_ragged(d, dtype):
     # blocks of 128 + 72, current blocks of 64, 64, 64, 8), a head with no
     # budget and a head whose budget exceeds the history
     _run_small(SMALL.replace(head_dim=d, dtype=dtype))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_elementwise_gates_adaptive(dtype):
+    _run_small(SMALL.replace(dtype=dtype, seed=25), mutate=elementwise_gates)
 
 
 def test_full_coverage_keeps_every_block_and_matches_page_attention():

@@ -13,7 +13,7 @@ import pytest
 from synth_inputs import WORKLOADS, make_case, make_projections
 from synth_inputs.configs import Workload
 
-from hsa_testlib import BF16_TOL, F32_TOL, assert_close, say, to_host, upload
+from hsa_testlib import BF16_TOL, F32_TOL, assert_close, elementwise_gates, gate_dims_of, say, to_host, upload
 from oracle import hsa_blocks_oracle as BO
 from oracle import hsa_linformer_oracle as LO
 from oracle import hsa_oracle as O
@@ -29,7 +29,8 @@ def _layer(wl, dev, e_k, e_v):
     from paper_2609_34606_amd import HsaLayer
     B, n_q, H, d = dev["q"].shape
     layer = HsaLayer(B, H, d, wl.page_size, dev["q"].dtype, dev["q"].device, k_pool=dev["k_pool"],
-                     v_pool=dev["v_pool"], page_table=dev["page_table"])
+                     v_pool=dev["v_pool"], page_table=dev["page_table"],
+                     gate_dims=gate_dims_of(dev))
     dt = dev["q"].dtype
     to = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev["q"].device).to(dt)
     layer.set_projections(to(e_k), to(e_v))
@@ -109,6 +110,18 @@ def _run(wl, rank=64, kind="gaussian", tau=(BO.TAU_MIN, BO.TAU_MAX), query_block
 def test_small_ragged_bf16(d, rank):
     # pages of 200 tokens (a partial last tile), 5 query blocks with a ragged tail
     _run(SMALL.replace(head_dim=d), rank=rank)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_elementwise_gates_linformer(dtype):
+    wl = SMALL.replace(dtype=dtype, seed=26)
+    case = make_case(wl)
+    elementwise_gates(case, seed=26)
+    host = dict(q=case.q, k_pool=case.k_pool, v_pool=case.v_pool, page_table=case.page_table,
+                g_lin=case.g_lin, g_sp=case.g_sp)
+    dev = upload(case)
+    dev["k_h"] = list(case.k_h)
+    _run(wl, rank=64, host=host, dev=dev)
 
 
 def test_fp32_tiny():

@@ -12,7 +12,7 @@ import pytest
 from synth_inputs import WORKLOADS, make_case
 from synth_inputs.configs import Workload
 
-from hsa_testlib import compare, run_library, run_oracle, say, upload
+from hsa_testlib import compare, elementwise_gates, run_library, run_oracle, say, upload
 
 pytestmark = pytest.mark.gpu
 
@@ -45,6 +45,16 @@ def test_small_ragged(d, dtype):
     # 3 query tiles with a ragged tail, pages that straddle 64-key tiles,
     # a head with no budget and a head whose budget exceeds the history.
     _run_small(SMALL.replace(head_dim=d, dtype=dtype))
+
+
+@pytest.mark.parametrize("d", [128, 64])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_elementwise_gates(d, dtype):
+    # one gate logit per output element (cfg.gate_dims = d), in the fused
+    # epilogue of the walk and of the split combine
+    _run_small(SMALL.replace(head_dim=d, dtype=dtype, seed=23), mutate=elementwise_gates)
+    _run_small(SMALL.replace(head_dim=d, dtype=dtype, batch=2, heads=2, k_h=(2, 5), n_q=129,
+                             seed=24), mutate=elementwise_gates)
 
 
 def test_batch_two_and_gates():
