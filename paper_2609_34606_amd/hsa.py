@@ -155,6 +155,20 @@ def _ptr(t) -> Optional[int]:
     return int(t)
 
 
+def _gate(cfg, g, n_q: int) -> Optional[int]:
+    """Pointer of a gate-logit tensor after checking that it holds what the
+    kernels read: fp32, [B, n_q, H] or, with cfg.gate_dims = d, [B, n_q, H, d]."""
+    if g is None:
+        return None
+    per = cfg.head_dim if cfg.gate_dims > 1 else 1
+    want = cfg.batch * n_q * cfg.num_heads * per
+    if hasattr(g, "numel"):
+        if g.numel() != want or str(g.dtype) != "torch.float32":
+            raise ValueError(f"gate logits must be {want} fp32 values ([B, n_q, H"
+                             f"{', d' if per > 1 else ''}]), got {tuple(g.shape)} {g.dtype}")
+    return _ptr(g)
+
+
 def _stream(stream) -> Optional[int]:
     """A HIP stream handle: an int, a torch stream, or None for torch's
     current stream."""
@@ -272,7 +286,7 @@ def hsa_forward(cfg, q, n_q, pool, n_cand, n_cur_pages, k_h, k_max, kv_state, k_
     _keep, kp = _budgets(k_h)
     st = lib().hsa_forward(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool), n_cand,
                            n_cur_pages, kp, k_max, _ptr(kv_state), _ptr(k_state),
-                           _ptr(page_kmean), _ptr(g_lin), _ptr(g_sp), _ptr(o), _ptr(sel_out),
+                           _ptr(page_kmean), _gate(cfg, g_lin, n_q), _gate(cfg, g_sp, n_q), _ptr(o), _ptr(sel_out),
                            _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream))
     if check:
         _check("hsa_forward", st)
@@ -286,7 +300,7 @@ def hsa_forward_selected(cfg, q, n_q, pool, sel, k_max, k_h, n_cand, n_cur_pages
     _keep, kp = _budgets(k_h)
     st = lib().hsa_forward_selected(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool), _ptr(sel),
                                     k_max, kp, n_cand, n_cur_pages, _ptr(kv_state), _ptr(k_state),
-                                    _ptr(g_lin), _ptr(g_sp), _ptr(o), _ptr(ws),
+                                    _gate(cfg, g_lin, n_q), _gate(cfg, g_sp, n_q), _ptr(o), _ptr(ws),
                                     0 if ws is None else ws.numel(), _stream(stream))
     if check:
         _check("hsa_forward_selected", st)
@@ -337,8 +351,8 @@ def hsa_forward_adaptive(cfg, q, n_q, pool, n_cand, n_cur_pages, k_h, k_max, kv_
     _keep, kp = _budgets(k_h)
     st = lib().hsa_forward_adaptive(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool), n_cand,
                                     n_cur_pages, kp, k_max, float(tau_min), float(tau_max),
-                                    _ptr(kv_state), _ptr(k_state), _ptr(page_kmean), _ptr(g_lin),
-                                    _ptr(g_sp), _ptr(o), _ptr(sel_out), _ptr(ws),
+                                    _ptr(kv_state), _ptr(k_state), _ptr(page_kmean), _gate(cfg, g_lin, n_q),
+                                    _gate(cfg, g_sp, n_q), _ptr(o), _ptr(sel_out), _ptr(ws),
                                     0 if ws is None else ws.numel(), _stream(stream))
     if check:
         _check("hsa_forward_adaptive", st)
@@ -373,8 +387,8 @@ def hsa_forward_linformer(cfg, q, n_q, pool, ck, cv, rank, n_cand, n_cur_pages, 
     _keep, kp = _budgets(k_h)
     st = lib().hsa_forward_linformer(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool), _ptr(ck),
                                      _ptr(cv), rank, n_cand, n_cur_pages, kp, k_max,
-                                     float(tau_min), float(tau_max), _ptr(page_kmean), _ptr(g_lin),
-                                     _ptr(g_sp), _ptr(o), _ptr(sel_out), _ptr(ws),
+                                     float(tau_min), float(tau_max), _ptr(page_kmean), _gate(cfg, g_lin, n_q),
+                                     _gate(cfg, g_sp, n_q), _ptr(o), _ptr(sel_out), _ptr(ws),
                                      0 if ws is None else ws.numel(), _stream(stream))
     if check:
         _check("hsa_forward_linformer", st)
@@ -406,8 +420,8 @@ def hsa_forward_retrieval(cfg, q, n_q, pool, prompt_emb, chunk_emb, emb_dim, n_c
     st = lib().hsa_forward_retrieval(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool),
                                      _ptr(prompt_emb), _ptr(chunk_emb), emb_dim, n_chunks,
                                      _ptr(chunk_first), n_cand, n_cur_pages, kp, k_max,
-                                     _ptr(kv_state), _ptr(k_state), _ptr(page_kmean), _ptr(g_lin),
-                                     _ptr(g_sp), _ptr(o), _ptr(chunk_out), _ptr(sel_out), _ptr(ws),
+                                     _ptr(kv_state), _ptr(k_state), _ptr(page_kmean), _gate(cfg, g_lin, n_q),
+                                     _gate(cfg, g_sp, n_q), _ptr(o), _ptr(chunk_out), _ptr(sel_out), _ptr(ws),
                                      0 if ws is None else ws.numel(), _stream(stream))
     if check:
         _check("hsa_forward_retrieval", st)

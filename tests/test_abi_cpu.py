@@ -198,3 +198,19 @@ def test_tier_three_levels_and_prefetch_plan_only():
     assert [t.locate(0, p) for p in range(6)] == [0, 1, L3(2), L2(0), L3(0), L3(1)]
     assert t.stats() == dict(evictions=10, fetches=6, spills=7, reloads=4, prefetched=1)
     t.close()
+
+
+def test_gate_tensors_are_checked_against_the_gate_shape():
+    import torch
+    from paper_2609_34606_amd import hsa as H
+    head = P.config(2, 3, 64, 256, "bf16")
+    elem = P.config(2, 3, 64, 256, "bf16", gate_dims=64)
+    n_q = 5
+    assert H._gate(head, None, n_q) is None
+    assert H._gate(head, torch.zeros((2, n_q, 3)), n_q) is not None
+    assert H._gate(elem, torch.zeros((2, n_q, 3, 64)), n_q) is not None
+    for cfg, g in ((head, torch.zeros((2, n_q, 3, 64))), (elem, torch.zeros((2, n_q, 3))),
+                   (head, torch.zeros((2, n_q + 1, 3))), (head, torch.zeros((2, n_q, 3), dtype=torch.float64))):
+        with pytest.raises(ValueError):
+            H._gate(cfg, g, n_q)
+
