@@ -169,6 +169,17 @@ def _gate(cfg, g, n_q: int) -> Optional[int]:
     return _ptr(g)
 
 
+def _rows(cfg, t, n_q: int, what: str) -> Optional[int]:
+    """Pointer of a [B, n_q, H, d] tensor (queries or outputs) after checking
+    its size against the config (the kernels index it with these sizes)."""
+    if t is not None and hasattr(t, "numel"):
+        want = cfg.batch * n_q * cfg.num_heads * cfg.head_dim
+        if t.numel() != want:
+            raise ValueError(f"{what} must hold [B, n_q, H, d] = {want} values, "
+                             f"got {tuple(t.shape)}")
+    return _ptr(t)
+
+
 def _stream(stream) -> Optional[int]:
     """A HIP stream handle: an int, a torch stream, or None for torch's
     current stream."""
@@ -270,8 +281,9 @@ def hsa_sparse_attn(cfg, q, n_q, pool, sel, k_max, k_h, cur_first_page, n_cur_pa
     if ws is None:
         ws = _workspace(hsa_sparse_attn_workspace_size(cfg, n_q, k_max, n_cur_pages), q.device)
     _keep, kp = _budgets(k_h)
-    st = lib().hsa_sparse_attn(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool), _ptr(sel),
-                               k_max, kp, cur_first_page, n_cur_pages, _ptr(o_sp), _ptr(lse),
+    qp, op = _rows(cfg, q, n_q, "q"), _rows(cfg, o_sp, n_q, "o_sp")
+    st = lib().hsa_sparse_attn(ctypes.byref(cfg), qp, n_q, ctypes.byref(pool), _ptr(sel),
+                               k_max, kp, cur_first_page, n_cur_pages, op, _ptr(lse),
                                _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream))
     if check:
         _check("hsa_sparse_attn", st)
@@ -284,9 +296,11 @@ def hsa_forward(cfg, q, n_q, pool, n_cand, n_cur_pages, k_h, k_max, kv_state, k_
     if ws is None:
         ws = _workspace(hsa_forward_workspace_size(cfg, n_q, k_max, n_cur_pages), q.device)
     _keep, kp = _budgets(k_h)
-    st = lib().hsa_forward(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool), n_cand,
+    qp, op = _rows(cfg, q, n_q, "q"), _rows(cfg, o, n_q, "o")
+    glp, gsp = _gate(cfg, g_lin, n_q), _gate(cfg, g_sp, n_q)
+    st = lib().hsa_forward(ctypes.byref(cfg), qp, n_q, ctypes.byref(pool), n_cand,
                            n_cur_pages, kp, k_max, _ptr(kv_state), _ptr(k_state),
-                           _ptr(page_kmean), _gate(cfg, g_lin, n_q), _gate(cfg, g_sp, n_q), _ptr(o), _ptr(sel_out),
+                           _ptr(page_kmean), glp, gsp, op, _ptr(sel_out),
                            _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream))
     if check:
         _check("hsa_forward", st)
@@ -298,9 +312,11 @@ def hsa_forward_selected(cfg, q, n_q, pool, sel, k_max, k_h, n_cand, n_cur_pages
     if ws is None:
         ws = _workspace(hsa_forward_workspace_size(cfg, n_q, k_max, n_cur_pages), q.device)
     _keep, kp = _budgets(k_h)
-    st = lib().hsa_forward_selected(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool), _ptr(sel),
+    qp, op = _rows(cfg, q, n_q, "q"), _rows(cfg, o, n_q, "o")
+    glp, gsp = _gate(cfg, g_lin, n_q), _gate(cfg, g_sp, n_q)
+    st = lib().hsa_forward_selected(ctypes.byref(cfg), qp, n_q, ctypes.byref(pool), _ptr(sel),
                                     k_max, kp, n_cand, n_cur_pages, _ptr(kv_state), _ptr(k_state),
-                                    _gate(cfg, g_lin, n_q), _gate(cfg, g_sp, n_q), _ptr(o), _ptr(ws),
+                                    glp, gsp, op, _ptr(ws),
                                     0 if ws is None else ws.numel(), _stream(stream))
     if check:
         _check("hsa_forward_selected", st)
@@ -349,10 +365,12 @@ def hsa_forward_adaptive(cfg, q, n_q, pool, n_cand, n_cur_pages, k_h, k_max, kv_
     if ws is None:
         ws = _workspace(hsa_adaptive_workspace_size(cfg, n_q, k_max, n_cur_pages), q.device)
     _keep, kp = _budgets(k_h)
-    st = lib().hsa_forward_adaptive(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool), n_cand,
+    qp, op = _rows(cfg, q, n_q, "q"), _rows(cfg, o, n_q, "o")
+    glp, gsp = _gate(cfg, g_lin, n_q), _gate(cfg, g_sp, n_q)
+    st = lib().hsa_forward_adaptive(ctypes.byref(cfg), qp, n_q, ctypes.byref(pool), n_cand,
                                     n_cur_pages, kp, k_max, float(tau_min), float(tau_max),
-                                    _ptr(kv_state), _ptr(k_state), _ptr(page_kmean), _gate(cfg, g_lin, n_q),
-                                    _gate(cfg, g_sp, n_q), _ptr(o), _ptr(sel_out), _ptr(ws),
+                                    _ptr(kv_state), _ptr(k_state), _ptr(page_kmean), glp,
+                                    gsp, op, _ptr(sel_out), _ptr(ws),
                                     0 if ws is None else ws.numel(), _stream(stream))
     if check:
         _check("hsa_forward_adaptive", st)
@@ -385,10 +403,12 @@ def hsa_forward_linformer(cfg, q, n_q, pool, ck, cv, rank, n_cand, n_cur_pages, 
     if ws is None:
         ws = _workspace(hsa_linformer_workspace_size(cfg, n_q, k_max, n_cur_pages), q.device)
     _keep, kp = _budgets(k_h)
-    st = lib().hsa_forward_linformer(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool), _ptr(ck),
+    qp, op = _rows(cfg, q, n_q, "q"), _rows(cfg, o, n_q, "o")
+    glp, gsp = _gate(cfg, g_lin, n_q), _gate(cfg, g_sp, n_q)
+    st = lib().hsa_forward_linformer(ctypes.byref(cfg), qp, n_q, ctypes.byref(pool), _ptr(ck),
                                      _ptr(cv), rank, n_cand, n_cur_pages, kp, k_max,
-                                     float(tau_min), float(tau_max), _ptr(page_kmean), _gate(cfg, g_lin, n_q),
-                                     _gate(cfg, g_sp, n_q), _ptr(o), _ptr(sel_out), _ptr(ws),
+                                     float(tau_min), float(tau_max), _ptr(page_kmean), glp,
+                                     gsp, op, _ptr(sel_out), _ptr(ws),
                                      0 if ws is None else ws.numel(), _stream(stream))
     if check:
         _check("hsa_forward_linformer", st)
@@ -417,11 +437,13 @@ def hsa_forward_retrieval(cfg, q, n_q, pool, prompt_emb, chunk_emb, emb_dim, n_c
     if ws is None:
         ws = _workspace(hsa_retrieval_workspace_size(cfg, n_q, k_max, n_cur_pages), q.device)
     _keep, kp = _budgets(k_h)
-    st = lib().hsa_forward_retrieval(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool),
+    qp, op = _rows(cfg, q, n_q, "q"), _rows(cfg, o, n_q, "o")
+    glp, gsp = _gate(cfg, g_lin, n_q), _gate(cfg, g_sp, n_q)
+    st = lib().hsa_forward_retrieval(ctypes.byref(cfg), qp, n_q, ctypes.byref(pool),
                                      _ptr(prompt_emb), _ptr(chunk_emb), emb_dim, n_chunks,
                                      _ptr(chunk_first), n_cand, n_cur_pages, kp, k_max,
-                                     _ptr(kv_state), _ptr(k_state), _ptr(page_kmean), _gate(cfg, g_lin, n_q),
-                                     _gate(cfg, g_sp, n_q), _ptr(o), _ptr(chunk_out), _ptr(sel_out), _ptr(ws),
+                                     _ptr(kv_state), _ptr(k_state), _ptr(page_kmean), glp,
+                                     gsp, op, _ptr(chunk_out), _ptr(sel_out), _ptr(ws),
                                      0 if ws is None else ws.numel(), _stream(stream))
     if check:
         _check("hsa_forward_retrieval", st)

@@ -214,3 +214,13 @@ def test_gate_tensors_are_checked_against_the_gate_shape():
         with pytest.raises(ValueError):
             H._gate(cfg, g, n_q)
 
+
+def test_query_and_output_tensors_are_checked_against_the_config():
+    import torch
+    from paper_2609_34606_amd import hsa as H
+    cfg = P.config(2, 3, 64, 256, "bf16")
+    assert H._rows(cfg, torch.zeros((2, 5, 3, 64)), 5, "q") is not None
+    for t in (torch.zeros((2, 6, 3, 64)), torch.zeros((2, 5, 3, 128)), torch.zeros((1, 5, 3, 64))):
+        with pytest.raises(ValueError):
+            H._rows(cfg, t, 5, "q")
+
