@@ -325,7 +325,7 @@ def bench_linformer(args, wl, layer, q, k_h, k_max, sel, rank=64):
     ms_fwd = time_loop(lambda: layer.forward_linformer(q, wl.n_cand, wl.n_cur, k_h, k_max=k_max,
                                                        out=out, sel_out=sel), args.steps, torch)
     crank = mkcfg(wl.batch, wl.heads, wl.head_dim, rank, q.dtype)
-    cpool = kv_pool(layer.ck, layer.cv, layer.page_table)
+    cpool = kv_pool(layer.ck, layer.cv, layer.page_table, crank)
     o_lin = torch.empty(q.shape, dtype=torch.float32, device=q.device)
     ws = layer.workspace("lin_attn", hsa_sparse_attn_workspace_size(crank, n_q, k_max, wl.n_cur))
     ms_br = time_loop(lambda: hsa_sparse_attn(crank, q, n_q, cpool, sel, k_max, k_h, wl.n_cand,

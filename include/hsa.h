@@ -119,6 +119,21 @@ size_t hsa_forward_workspace_size(const hsa_config_t* cfg, int32_t n_q,
 size_t hsa_adaptive_workspace_size(const hsa_config_t* cfg, int32_t n_q,
                                    int32_t k_max, int32_t n_cur_pages);
 
+/* Work schedule of the bf16 attention launch (host-only inspection: it
+ * launches nothing and needs no device). For per-head list lengths
+ * list_len[h] (selected pages + current pages, host array of H entries, each
+ * in [1, HSA_MAX_LIST]) and n_q queries it runs the planner that
+ * hsa_forward (adaptive = 0) or the tile-list walk of the adaptive calls
+ * (adaptive = 1) use, and writes the number of work items (query tile x key
+ * split), of chunks in the launch's schedule table (at most
+ * HSA_PLAN_MAX_CHUNKS) and the largest key split of a head. Each output
+ * pointer is nullable. Errors: INVALID_ARG, UNSUPPORTED (no schedule fits;
+ * the attention calls then return the same). */
+#define HSA_PLAN_MAX_CHUNKS 256
+hsa_status_t hsa_attention_plan(const hsa_config_t* cfg, int32_t n_q, const int32_t* list_len,
+                                int32_t adaptive, int32_t* n_items, int32_t* n_chunks,
+                                int32_t* max_split);
+
 /* Key blocks of a list of n_hist_pages history pages and n_cur_pages current
  * pages: n_hist_pages * ceil(P / HSA_BLOCK_HIST) + n_cur_pages * ceil(P /
  * HSA_BLOCK_CUR). With n_hist_pages = k_max it is the row length of the

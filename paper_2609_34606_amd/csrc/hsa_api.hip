@@ -420,8 +420,9 @@ hsa_status_t run_sparse(const hsa_config_t* cfg, const void* q, int32_t n_q,
   int list_len[HSA_MAX_HEADS];
   for (int h = 0; h < cfg->num_heads; ++h)
     list_len[h] = std::min(k_h ? k_h[h] : k_max, pool->max_pages) + n_cur_pages;
-  plan_attention(p, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
-                 kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16, w ? 4 : kPageWaves);
+  if (!plan_attention(p, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
+                      kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16, w ? 4 : kPageWaves))
+    return HSA_ERR_UNSUPPORTED;
   if (cfg->dtype == HSA_DTYPE_BF16) set_partials(p, cfg, n_q, partials);
   if (w) set_block_lists(p, *w, static_cast<uint8_t*>(partials) - w->part_off);
   return from_hip(launch_attention(cfg->dtype, cfg->head_dim, cfg->batch, p, s));
@@ -556,6 +557,27 @@ size_t hsa_adaptive_workspace_size(const hsa_config_t* cfg, int32_t n_q, int32_t
   return adaptive_ws(cfg, n_q, k_max, n_cur_pages).total;
 }
 
+hsa_status_t hsa_attention_plan(const hsa_config_t* cfg, int32_t n_q, const int32_t* list_len,
+                                int32_t adaptive, int32_t* n_items, int32_t* n_chunks,
+                                int32_t* max_split) {
+  hsa_status_t st = check_cfg(cfg);
+  if (st != HSA_OK) return st;
+  if (!list_len || n_q < 1) return HSA_ERR_INVALID_ARG;
+  for (int h = 0; h < cfg->num_heads; ++h)
+    if (list_len[h] < 1 || list_len[h] > HSA_MAX_LIST) return HSA_ERR_INVALID_ARG;
+  AttnParams p{};
+  if (!plan_attention(p, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
+                      kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16,
+                      adaptive ? 4 : kPageWaves))
+    return HSA_ERR_UNSUPPORTED;
+  int widest = 1;
+  for (int h = 0; h < cfg->num_heads; ++h) widest = std::max(widest, (int)p.sc.n_split[h]);
+  if (n_items) *n_items = p.sc.n_items;
+  if (n_chunks) *n_chunks = p.sc.n_chunks;
+  if (max_split) *max_split = widest;
+  return HSA_OK;
+}
+
 int32_t hsa_block_count(const hsa_config_t* cfg, int32_t n_hist_pages, int32_t n_cur_pages) {
   if (check_cfg(cfg) != HSA_OK || n_hist_pages < 0 || n_cur_pages < 0) return -1;
   if ((long)n_hist_pages + n_cur_pages > HSA_MAX_LIST) return -1;
@@ -677,8 +699,9 @@ hsa_status_t run_attend(const hsa_config_t* cfg, const void* q, int32_t n_q,
   p.o = o;
   int list_len[HSA_MAX_HEADS];
   for (int h = 0; h < cfg->num_heads; ++h) list_len[h] = std::min(k_h[h], n_cand) + n_cur_pages;
-  plan_attention(p, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
-                 kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16, w ? 4 : kPageWaves);
+  if (!plan_attention(p, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
+                      kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16, w ? 4 : kPageWaves))
+    return HSA_ERR_UNSUPPORTED;
   if (cfg->dtype == HSA_DTYPE_BF16) set_partials(p, cfg, n_q, partials);
   if (w) set_block_lists(p, *w, wbase);
   return from_hip(launch_attention(cfg->dtype, cfg->head_dim, cfg->batch, p, s));

@@ -1135,12 +1135,12 @@ struct PlanKey {
   }
 };
 
-void plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_len, int max_part,
+bool plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_len, int max_part,
                    bool split, int waves);
 
 }  // namespace
 
-void plan_attention(AttnParams& p, int H, int d, int n_q, int P, const int* list_len, int max_part,
+bool plan_attention(AttnParams& p, int H, int d, int n_q, int P, const int* list_len, int max_part,
                     bool split, int waves) {
   constexpr int kCache = 8;
   static std::mutex mu;
@@ -1154,20 +1154,21 @@ void plan_attention(AttnParams& p, int H, int d, int n_q, int P, const int* list
     for (int i = 0; i < n_cached; ++i)
       if (keys[i] == key) {
         p.sc = scheds[i];
-        return;
+        return true;
       }
   }
-  plan_schedule(p, H, d, n_q, P, list_len, max_part, split, waves);
+  if (!plan_schedule(p, H, d, n_q, P, list_len, max_part, split, waves)) return false;
   std::lock_guard<std::mutex> lock(mu);
   keys[next] = key;
   scheds[next] = p.sc;
   next = (next + 1) % kCache;
   n_cached = std::min(n_cached + 1, kCache);
+  return true;
 }
 
 namespace {
 
-void plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_len, int max_part,
+bool plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_len, int max_part,
                    bool split, int waves) {
   const int kBM = kWaveQ * waves;
   const int nqt = (n_q + kBM - 1) / kBM;
@@ -1184,17 +1185,22 @@ void plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_
   // split size), split-major, query tile fastest. The chunks of a (head,
   // split) group read the same pages, so each XCD should run few groups;
   // cutting groups into more chunks balances the XCDs better.
+  // Returns false when the (head, split) groups alone exceed the chunk table.
   auto build = [&](const int* ns, int per_group, std::vector<int>& order, std::vector<Chunk>& chunks) {
     order.resize(H);
     for (int h = 0; h < H; ++h) order[h] = h;
     auto split_size = [&](int h) { return (list_len[h] + ns[h] - 1) / ns[h]; };
     std::stable_sort(order.begin(), order.end(),
                      [&](int a, int b) { return split_size(a) > split_size(b); });
-    int items = 0;
-    for (int h = 0; h < H; ++h) items += ns[h] * nqt;
-    const int min_len = (items + HSA_MAX_CHUNKS - 1) / HSA_MAX_CHUNKS;
-    const int len_c = std::max(min_len, (nqt + per_group - 1) / per_group);
+    int groups = 0;
+    for (int h = 0; h < H; ++h) groups += ns[h];
+    // every group has nqt items, cut into ceil(nqt / len_c) chunks; the
+    // table holds HSA_MAX_CHUNKS of them
+    const int per_group_max = HSA_MAX_CHUNKS / groups;
     chunks.clear();
+    if (per_group_max < 1) return false;
+    const int len_c = std::max((nqt + per_group_max - 1) / per_group_max,
+                               (nqt + per_group - 1) / per_group);
     for (int i = 0, it = 0; i < H; ++i) {
       const int h = order[i], base = list_len[h] / ns[h], rem = list_len[h] % ns[h];
       for (int sp = 0; sp < ns[h]; ++sp, it += nqt) {
@@ -1208,15 +1214,17 @@ void plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_
     // largest item cost first (stable: groups stay in item order)
     std::stable_sort(chunks.begin(), chunks.end(),
                      [](const Chunk& a, const Chunk& b) { return a.cost / a.len > b.cost / b.len; });
+    return (int)chunks.size() <= HSA_MAX_CHUNKS;
   };
   std::vector<int> order, xcd_of;
   std::vector<Chunk> chunks;
+  constexpr double kInfeasible = 1e30;
   auto evaluate = [&](const int* ns, int per_group) -> double {
     int n_part = 0;
     for (int h = 0; h < H; ++h)
       if (ns[h] > 1) n_part += ns[h];
-    if (n_part > max_part) return 1e30;
-    build(ns, per_group, order, chunks);
+    if (n_part > max_part) return kInfeasible;
+    if (!build(ns, per_group, order, chunks)) return kInfeasible;
     double us = deal_chunks(chunks, slots_per_xcd, xcd_of) * kTileUs * (waves / 4.0);
     if (n_part > 0) us += kCombineUsFixed + 2.0 * n_part * nqt * (double)kBM * d * 4 / kPartialBytesPerUs;
     return us;
@@ -1240,7 +1248,9 @@ void plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_
       }
     }
   }
-  evaluate(best_ns, best_g);  // rebuild order, chunks and xcd_of of the choice
+  // rebuild order, chunks and xcd_of of the choice (the unsplit plan, the
+  // first candidate, always fits: at most HSA_MAX_HEADS groups)
+  if (evaluate(best_ns, best_g) >= kInfeasible || chunks.size() > (size_t)HSA_MAX_CHUNKS) return false;
   p.sc.nqt = nqt;
   p.sc.nq32 = nqt * waves;
   p.sc.waves = waves;
@@ -1283,6 +1293,7 @@ void plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_
   p.sc.xcd_chunk[8] = n;
   p.sc.n_chunks = n;
   p.sc.xcd_items = widest;
+  return true;
 }
 
 }  // namespace

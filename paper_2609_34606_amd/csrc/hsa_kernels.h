@@ -10,7 +10,7 @@
 
 namespace hsa {
 
-constexpr int HSA_MAX_CHUNKS = 256;
+constexpr int HSA_MAX_CHUNKS = HSA_PLAN_MAX_CHUNKS;
 
 // ------------------------------------------------------------ state update
 struct StateParams {
@@ -158,11 +158,11 @@ struct AttnSchedule {
   int32_t nq32;                          // 32-query wave slots per (head, split): nqt * waves
   int32_t n_items;                       // attention items per batch entry
   int32_t n_order;                       // heads listed in head_order
-  int32_t head_order[HSA_MAX_HEADS];
+  int16_t head_order[HSA_MAX_HEADS];
   int32_t item_off[HSA_MAX_HEADS + 1];   // first item of head_order[i]
-  int32_t n_split[HSA_MAX_HEADS];        // splits of head h (by head index)
-  int32_t list_len[HSA_MAX_HEADS];       // pages the splits of head h cover
-  int32_t part_base[HSA_MAX_HEADS];      // first partial slot of head h (n_split > 1)
+  int16_t n_split[HSA_MAX_HEADS];        // splits of head h (by head index)
+  int16_t list_len[HSA_MAX_HEADS];       // pages the splits of head h cover (<= HSA_MAX_LIST)
+  int16_t part_base[HSA_MAX_HEADS];      // first partial slot of head h (n_split > 1)
   int32_t n_part;                        // partial slots per batch entry
   // Items are cut into chunks of consecutive items of one (head, split);
   // XCD x runs chunks [xcd_chunk[x], xcd_chunk[x+1]) in that order.
@@ -173,7 +173,7 @@ struct AttnSchedule {
   int32_t xcd_items;                     // most items on one XCD
   // combine items: n_chead heads with n_split > 1, nqt items each
   int32_t n_chead;
-  int32_t c_head[HSA_MAX_HEADS];
+  int16_t c_head[HSA_MAX_HEADS];
 };
 
 struct AttnParams {
@@ -209,15 +209,19 @@ struct AttnParams {
   int32_t blist_cap;
   AttnSchedule sc;                       // work schedule of the bf16 kernels
 };
+// Kernels take AttnParams by value; the kernel-argument segment holds 4 KB.
+static_assert(sizeof(AttnParams) <= 3584, "AttnParams must leave room in the 4 KB argument segment");
+static_assert(HSA_MAX_LIST <= 32767 && 4 * HSA_MAX_HEADS <= 32767, "per-head schedule fields are int16");
 
 // Chooses the split of each head's page list and the item order for
 // list_len[h] pages per head (H heads, head dim d, n_q queries, page size P);
 // at most max_part partial slots. split = false keeps every head whole.
 // waves: 8 (256-query workgroups, one per CU) for the page walk, 4 (128
-// queries, two per CU) for tile lists. Fills p.sc; the last few schedules
-// are cached (thread-safe), so a call with the inputs of a recent one costs
-// a table lookup.
-void plan_attention(AttnParams& p, int H, int d, int n_q, int P, const int* list_len,
+// queries, two per CU) for tile lists. Fills p.sc and returns true; false
+// if no schedule fits the chunk table (p.sc is then not written). The last
+// few schedules are cached (thread-safe), so a call with the inputs of a
+// recent one costs a table lookup.
+bool plan_attention(AttnParams& p, int H, int d, int n_q, int P, const int* list_len,
                     int max_part, bool split, int waves);
 // Workspace bytes for max_part partial slots (any workgroup width), and
 // the offset of the LSE partials in it.

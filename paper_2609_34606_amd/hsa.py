@@ -110,6 +110,8 @@ def lib():
     L.hsa_tier_locate.argtypes = [c_vp, c_i32, c_i32]
     L.hsa_tier_stats.restype = None
     L.hsa_tier_stats.argtypes = [c_vp, P(HsaTierStats)]
+    L.hsa_attention_plan.restype = ctypes.c_int
+    L.hsa_attention_plan.argtypes = [P(HsaConfig), c_i32, c_vp, c_i32, c_vp, c_vp, c_vp]
     L.hsa_block_count.restype = c_i32
     L.hsa_block_count.argtypes = [P(HsaConfig), c_i32, c_i32]
     c_f64 = ctypes.c_double
@@ -169,14 +171,23 @@ def _gate(cfg, g, n_q: int) -> Optional[int]:
     return _ptr(g)
 
 
-def _rows(cfg, t, n_q: int, what: str) -> Optional[int]:
+def _elem_dtype(cfg) -> str:
+    return "torch.bfloat16" if cfg.dtype == HSA_DTYPE_BF16 else "torch.float32"
+
+
+def _rows(cfg, t, n_q: int, what: str, fp32: bool = False) -> Optional[int]:
     """Pointer of a [B, n_q, H, d] tensor (queries or outputs) after checking
-    its size against the config (the kernels index it with these sizes)."""
+    its size and element type against the config (the kernels index it with
+    these sizes and read or write elements of the config's dtype; fp32 = True
+    for the fp32 sparse-branch output)."""
     if t is not None and hasattr(t, "numel"):
         want = cfg.batch * n_q * cfg.num_heads * cfg.head_dim
         if t.numel() != want:
             raise ValueError(f"{what} must hold [B, n_q, H, d] = {want} values, "
                              f"got {tuple(t.shape)}")
+        dt = "torch.float32" if fp32 else _elem_dtype(cfg)
+        if str(t.dtype) != dt:
+            raise ValueError(f"{what} must be {dt}, got {t.dtype}")
     return _ptr(t)
 
 
@@ -217,7 +228,20 @@ def config(batch: int, num_heads: int, head_dim: int, page_size: int, dtype,
     return HsaConfig(batch, num_heads, head_dim, page_size, dtype, sm_scale, gate_dims)
 
 
-def kv_pool(k_pool, v_pool, page_table) -> HsaKvPool:
+def kv_pool(k_pool, v_pool, page_table, cfg: Optional[HsaConfig] = None) -> HsaKvPool:
+    """The pool descriptor. With cfg, the tensors are checked against it
+    first: k_pool [slots, H, P, d] and v_pool [slots, H, d, P] of the config's
+    dtype, page_table [B, max_pages] int32."""
+    if cfg is not None:
+        H, P, d = cfg.num_heads, cfg.page_size, cfg.head_dim
+        slots = int(k_pool.shape[0])
+        dt = _elem_dtype(cfg)
+        for name, t, shape in (("k_pool", k_pool, (slots, H, P, d)), ("v_pool", v_pool, (slots, H, d, P))):
+            if tuple(t.shape) != shape or str(t.dtype) != dt:
+                raise ValueError(f"{name} must be {dt} {shape}, got {t.dtype} {tuple(t.shape)}")
+        if page_table.dim() != 2 or page_table.shape[0] != cfg.batch or str(page_table.dtype) != "torch.int32":
+            raise ValueError(f"page_table must be int32 [B={cfg.batch}, max_pages], got "
+                             f"{page_table.dtype} {tuple(page_table.shape)}")
     return HsaKvPool(_ptr(k_pool), _ptr(v_pool), _ptr(page_table), int(k_pool.shape[0]),
                      int(page_table.shape[-1]))
 
@@ -268,7 +292,7 @@ def hsa_page_select(cfg, q, n_q, page_kmean, max_pages, n_cand, k_h, k_max, sel,
     if ws is None:
         ws = _workspace(hsa_page_select_workspace_size(cfg, n_q), q.device)
     _keep, kp = _budgets(k_h)
-    st = lib().hsa_page_select(ctypes.byref(cfg), _ptr(q), n_q, _ptr(page_kmean), max_pages,
+    st = lib().hsa_page_select(ctypes.byref(cfg), _rows(cfg, q, n_q, "q"), n_q, _ptr(page_kmean), max_pages,
                                n_cand, kp, k_max, _ptr(sel), _ptr(sel_score), _ptr(ws),
                                0 if ws is None else ws.numel(), _stream(stream))
     if check:
@@ -281,7 +305,7 @@ def hsa_sparse_attn(cfg, q, n_q, pool, sel, k_max, k_h, cur_first_page, n_cur_pa
     if ws is None:
         ws = _workspace(hsa_sparse_attn_workspace_size(cfg, n_q, k_max, n_cur_pages), q.device)
     _keep, kp = _budgets(k_h)
-    qp, op = _rows(cfg, q, n_q, "q"), _rows(cfg, o_sp, n_q, "o_sp")
+    qp, op = _rows(cfg, q, n_q, "q"), _rows(cfg, o_sp, n_q, "o_sp", fp32=True)
     st = lib().hsa_sparse_attn(ctypes.byref(cfg), qp, n_q, ctypes.byref(pool), _ptr(sel),
                                k_max, kp, cur_first_page, n_cur_pages, op, _ptr(lse),
                                _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream))
@@ -333,7 +357,7 @@ def hsa_block_select(cfg, q, n_q, pool, sel, k_max, cur_first_page, n_cur_pages,
                      check=True) -> int:
     if ws is None:
         ws = _workspace(hsa_adaptive_workspace_size(cfg, n_q, k_max, n_cur_pages), q.device)
-    st = lib().hsa_block_select(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool), _ptr(sel),
+    st = lib().hsa_block_select(ctypes.byref(cfg), _rows(cfg, q, n_q, "q"), n_q, ctypes.byref(pool), _ptr(sel),
                                 k_max, cur_first_page, n_cur_pages, float(tau_min),
                                 float(tau_max), _ptr(gini), _ptr(tau), _ptr(n_kept), _ptr(kept),
                                 _ptr(pooled), kept_len, _ptr(ws),
@@ -349,9 +373,10 @@ def hsa_sparse_attn_adaptive(cfg, q, n_q, pool, sel, k_max, k_h, cur_first_page,
     if ws is None:
         ws = _workspace(hsa_adaptive_workspace_size(cfg, n_q, k_max, n_cur_pages), q.device)
     _keep, kp = _budgets(k_h)
-    st = lib().hsa_sparse_attn_adaptive(ctypes.byref(cfg), _ptr(q), n_q, ctypes.byref(pool),
-                                        _ptr(sel), k_max, kp, cur_first_page, n_cur_pages,
-                                        float(tau_min), float(tau_max), _ptr(o_sp), _ptr(lse),
+    st = lib().hsa_sparse_attn_adaptive(ctypes.byref(cfg), _rows(cfg, q, n_q, "q"), n_q,
+                                        ctypes.byref(pool), _ptr(sel), k_max, kp, cur_first_page,
+                                        n_cur_pages, float(tau_min), float(tau_max),
+                                        _rows(cfg, o_sp, n_q, "o_sp", fp32=True), _ptr(lse),
                                         _ptr(ws), 0 if ws is None else ws.numel(),
                                         _stream(stream))
     if check:

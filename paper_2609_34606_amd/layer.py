@@ -39,7 +39,7 @@ class HsaLayer:
 
     @property
     def pool(self) -> _h.HsaKvPool:
-        return _h.kv_pool(self.k_pool, self.v_pool, self.page_table)
+        return _h.kv_pool(self.k_pool, self.v_pool, self.page_table, self.cfg)
 
     def workspace(self, key, nbytes: int):
         if nbytes == 0:

@@ -219,8 +219,71 @@ def test_query_and_output_tensors_are_checked_against_the_config():
     import torch
     from paper_2609_34606_amd import hsa as H
     cfg = P.config(2, 3, 64, 256, "bf16")
-    assert H._rows(cfg, torch.zeros((2, 5, 3, 64)), 5, "q") is not None
-    for t in (torch.zeros((2, 6, 3, 64)), torch.zeros((2, 5, 3, 128)), torch.zeros((1, 5, 3, 64))):
+    bf = torch.bfloat16
+    assert H._rows(cfg, torch.zeros((2, 5, 3, 64), dtype=bf), 5, "q") is not None
+    for t in (torch.zeros((2, 6, 3, 64), dtype=bf), torch.zeros((2, 5, 3, 128), dtype=bf),
+              torch.zeros((1, 5, 3, 64), dtype=bf)):
         with pytest.raises(ValueError):
             H._rows(cfg, t, 5, "q")
+    # element type: the kernels read and write the config's dtype (twice the
+    # bytes for fp32), so a mismatch is rejected before any pointer is passed
+    with pytest.raises(ValueError):
+        H._rows(cfg, torch.zeros((2, 5, 3, 64)), 5, "q")
+    f32 = P.config(2, 3, 64, 256, "f32")
+    assert H._rows(f32, torch.zeros((2, 5, 3, 64)), 5, "q") is not None
+    with pytest.raises(ValueError):
+        H._rows(f32, torch.zeros((2, 5, 3, 64), dtype=bf), 5, "o")
+    # the sparse-branch output is fp32 under either config
+    assert H._rows(cfg, torch.zeros((2, 5, 3, 64)), 5, "o_sp", fp32=True) is not None
+    with pytest.raises(ValueError):
+        H._rows(cfg, torch.zeros((2, 5, 3, 64), dtype=bf), 5, "o_sp", fp32=True)
 
+
+def test_pool_tensors_are_checked_against_the_config():
+    import torch
+    from paper_2609_34606_amd import hsa as H
+    cfg = P.config(2, 3, 64, 16, "bf16")
+    bf = torch.bfloat16
+    k = torch.zeros((5, 3, 16, 64), dtype=bf)
+    v = torch.zeros((5, 3, 64, 16), dtype=bf)
+    pt = torch.zeros((2, 4), dtype=torch.int32)
+    pool = H.kv_pool(k, v, pt, cfg)
+    assert (pool.num_slots, pool.max_pages) == (5, 4)
+    bad = [(k.float(), v, pt), (k, v.float(), pt), (k.transpose(2, 3).contiguous(), v, pt),
+           (k, v.transpose(2, 3).contiguous(), pt), (k[:, :2].contiguous(), v, pt),
+           (k, v, pt.long()), (k, v, pt[:1].contiguous())]
+    for a, b, c in bad:
+        with pytest.raises(ValueError):
+            H.kv_pool(a, b, c, cfg)
+
+
+
+def test_attention_planner_fits_its_chunk_table():
+    # The planner's chunk table holds HSA_PLAN_MAX_CHUNKS entries. Long page
+    # lists split heads into several key ranges and every (head, split) group
+    # is cut into chunks of query tiles; with many heads the plan must still
+    # fit (a coarser cut or fewer splits), for every head count the config
+    # accepts, both walks and P = 1560 as well as short pages.
+    lib = P.lib()
+    n_items, n_chunks, widest = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    rng = __import__("numpy").random.default_rng(5)
+    checked = 0
+    for H_ in list(range(1, 65, 3)) + [17, 32, 63, 64]:
+        for n_q in (1, 257, 2560, 4680, 20000):
+            for lens in ((50,) * H_, tuple(int(x) for x in rng.integers(1, 120, H_)), (1,) * H_):
+                for adaptive in (0, 1):
+                    cfg = P.config(1, H_, 128, 1560 if adaptive == 0 else 512, "bf16")
+                    arr = (ctypes.c_int32 * H_)(*lens)
+                    st = lib.hsa_attention_plan(ctypes.byref(cfg), n_q, arr, adaptive,
+                                                ctypes.byref(n_items), ctypes.byref(n_chunks),
+                                                ctypes.byref(widest))
+                    assert st == 0, (H_, n_q, lens[:3], adaptive, st)
+                    assert 1 <= n_chunks.value <= 256, (H_, n_q, n_chunks.value)
+                    waves = 4 if adaptive else 8
+                    assert n_items.value >= H_ * -(-n_q // (32 * waves))
+                    assert 1 <= widest.value <= max(lens)
+                    checked += 1
+    assert checked > 500
+    cfg = P.config(1, 4, 128, 1560, "bf16")
+    bad = (ctypes.c_int32 * 4)(3, 0, 3, 3)
+    assert lib.hsa_attention_plan(ctypes.byref(cfg), 100, bad, 0, None, None, None) == 1

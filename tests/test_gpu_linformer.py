@@ -83,7 +83,7 @@ def _run(wl, rank=64, kind="gaussian", tau=(BO.TAU_MIN, BO.TAU_MAX), query_block
                                 sel_out=sel)
     # the branch alone: sparse attention over the compressed pool
     crank = mkcfg(B, H, d, rank, dev["q"].dtype)
-    cpool = kv_pool(layer.ck, layer.cv, dev["page_table"])
+    cpool = kv_pool(layer.ck, layer.cv, dev["page_table"], crank)
     o_lin = torch.zeros((B, n_q, H, d), dtype=torch.float32, device=dev["q"].device)
     lse = torch.zeros((B, H, n_q), dtype=torch.float32, device=dev["q"].device)
     hsa_sparse_attn(crank, dev["q"], n_q, cpool, sel, k_max, k_h, wl.n_cand, wl.n_cur, o_lin, lse=lse)
