@@ -137,8 +137,9 @@ def adaptive_head(q: np.ndarray, k_list: Sequence[np.ndarray], v_list: Sequence[
     n_list = len(k_list)
     P = k_list[0].shape[0] if n_list else 0
     blocks = list_blocks(n_hist, n_list - n_hist, P, b_hist, b_cur)
-    kbar = np.stack([np.asarray(k_list[li], np.float64)[s:e].mean(axis=0) for li, s, e in blocks]) \
-        if blocks else np.zeros((0, d))
+    # mean key of every block, page by page in list order
+    kbar = np.concatenate([block_means(k_list[li], page_blocks(P, b_hist if li < n_hist else b_cur))
+                           for li in range(n_list)], 0) if blocks else np.zeros((0, d))
     qb = page_blocks(n_q, block_q)
     qbar = block_means(q, qb)
     pm = pooled_map(qbar, kbar, scale) if blocks else np.zeros((len(qb), 0))

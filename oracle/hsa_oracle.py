@@ -145,31 +145,6 @@ def gather_pages(k_pool, v_pool, page_table, b, h, pages: Sequence[int]):
 # whole pass
 # --------------------------------------------------------------------------
 
-def page_index(k_pool, page_table, pages: Sequence[int]) -> np.ndarray:
-    """Mean key of each listed page, per batch and head: [B,H,len(pages),d]."""
-    B = page_table.shape[0]
-    H, d = k_pool.shape[1], k_pool.shape[3]
-    out = np.zeros((B, H, len(pages), d))
-    for b in range(B):
-        for h in range(H):
-            for i, p in enumerate(pages):
-                out[b, h, i] = page_key_mean(k_pool[int(page_table[b, p]), h])
-    return out
-
-
-def state(k_pool, v_pool, page_table, pages: Sequence[int]):
-    """Linear state over the listed pages: S [B,H,d_k,d_v], z [B,H,d_k]."""
-    B = page_table.shape[0]
-    H, d = k_pool.shape[1], k_pool.shape[3]
-    S = np.zeros((B, H, d, d))
-    z = np.zeros((B, H, d))
-    for b in range(B):
-        for h in range(H):
-            k, v = gather_pages(k_pool, v_pool, page_table, b, h, pages)
-            S[b, h], z[b, h] = linear_state(k, v)
-    return S, z
-
-
 def hsa_forward(q, k_pool, v_pool, page_table, n_cand: int, n_cur: int,
                 k_h: Sequence[int], g_lin=None, g_sp=None,
                 sm_scale: Optional[float] = None, k_max: Optional[int] = None,

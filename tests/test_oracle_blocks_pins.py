@@ -196,3 +196,81 @@ def test_threshold_one_keeps_every_block_even_if_the_sum_rounds_early():
     assert np.cumsum(p)[1] == 1.0 or np.cumsum(p)[2] == 1.0
     assert len(BO.select_blocks(p, 1.0)) == 4
     assert len(BO.select_blocks(p, 0.75)) == 2
+
+
+def test_block_means_equal_reshaped_page_means():
+    # on a page that the block size divides, the block means are the means of
+    # the page reshaped into [P / B, B, d]
+    rng = np.random.default_rng(7)
+    for P, B in [(1536, 128), (1536, 64), (256, 64)]:
+        x = rng.standard_normal((P, 16))
+        got = BO.block_means(x, BO.page_blocks(P, B))
+        np.testing.assert_allclose(got, x.reshape(-1, B, 16).mean(1), rtol=0, atol=1e-15)
+
+
+def _blocky_head(rng, n_hist, n_cur, P, d, n_q, b_hist=BO.BLOCK_HIST, b_cur=BO.BLOCK_CUR):
+    """Keys constant inside every key block (a distinct random vector per
+    block, page by page in list order) and queries constant inside every
+    query block."""
+    k_list, v_list = [], []
+    for li in range(n_hist + n_cur):
+        B = b_hist if li < n_hist else b_cur
+        k = np.zeros((P, d))
+        for s, e in BO.page_blocks(P, B):
+            k[s:e] = rng.standard_normal(d) * 1.5
+        k_list.append(k)
+        v_list.append(rng.standard_normal((P, d)))
+    q = np.zeros((n_q, d))
+    for s, e in BO.page_blocks(n_q, BO.BLOCK_Q):
+        q[s:e] = rng.standard_normal(d) * 1.5
+    return q, k_list, v_list
+
+
+def _token_mass(q, k_list, scale, blocks):
+    """Softmax over every token of the list (torch, fp64) for each query, the
+    mass it puts on each key block: [n_q, n_blocks]."""
+    keys = torch.from_numpy(np.concatenate(k_list, 0))
+    p = torch.softmax(torch.from_numpy(q) @ keys.T * scale, dim=-1)
+    off = np.cumsum([0] + [k.shape[0] for k in k_list])
+    cols = [p[:, off[li] + s: off[li] + e].sum(-1) for li, s, e in blocks]
+    return torch.stack(cols, -1).numpy()
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_pooled_map_equals_token_softmax_mass_on_blocky_inputs(seed):
+    # With keys constant inside equal-size key blocks and queries constant
+    # inside each query block, the softmax of a query over all tokens puts on
+    # block j exactly the weight that the pooled (block-level) map gives it:
+    # each token of block j has score s q.k_j, so the block's mass is
+    # B exp(s q.k_j) / sum_j' B exp(s q.k_j'). This fixes the pooling to the
+    # mean (sum pooling scales every score by B), the scale, and which page
+    # and rows each block id stands for.
+    rng = np.random.default_rng(100 + seed)
+    d, n_q, P = 32, 200, 384            # history blocks of 128 divide the page
+    q, k_list, v_list = _blocky_head(rng, 3, 0, P, d, n_q)
+    scale = 1.0 / np.sqrt(d)
+    r = BO.adaptive_head(q, k_list, v_list, 3, scale, query_blocks=[])
+    mass = _token_mass(q, k_list, scale, r["blocks"])
+    for i, (s, e) in enumerate(BO.page_blocks(n_q, BO.BLOCK_Q)):
+        np.testing.assert_allclose(mass[s:e], np.broadcast_to(r["pooled"][i], mass[s:e].shape),
+                                   rtol=1e-12, atol=1e-15)
+
+
+def test_pooled_map_against_token_mass_with_unequal_block_sizes():
+    # History blocks hold 128 tokens and current-chunk blocks 64, so the
+    # token-level mass of block j is proportional to n_j exp(s q.k_j) while
+    # the pooled weight is proportional to exp(s q.k_j): dividing the mass by
+    # the block size and renormalising gives the pooled map.
+    rng = np.random.default_rng(9)
+    d, n_q, P = 32, 130, 256
+    q, k_list, v_list = _blocky_head(rng, 2, 2, P, d, n_q)
+    scale = 0.2
+    r = BO.adaptive_head(q, k_list, v_list, 2, scale, query_blocks=[])
+    mass = _token_mass(q, k_list, scale, r["blocks"])
+    sizes = np.array([e - s for _, s, e in r["blocks"]], np.float64)
+    assert set(sizes.tolist()) == {64.0, 128.0}
+    per = mass / sizes
+    per /= per.sum(-1, keepdims=True)
+    for i, (s, e) in enumerate(BO.page_blocks(n_q, BO.BLOCK_Q)):
+        np.testing.assert_allclose(per[s:e], np.broadcast_to(r["pooled"][i], per[s:e].shape),
+                                   rtol=1e-12, atol=1e-15)
