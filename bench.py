@@ -5,13 +5,19 @@ A step is one pass of the whole path over one chunk of synthetic input with
 everything resident in HBM: hsa_state_update over every page of the layer
 (cold build of the linear state and page index) followed by hsa_forward
 (query summary, page selection, sparse branch, linear branch, gated merge).
-Default workload: one layer, 12 heads x d128, 4680 queries, 21 history pages
-of 1560 tokens plus the 3 current pages, k_h = 4 (``--config c2``). The
-streaming 30-layer workload is ``--config c5``.
+Default workload (``--config c3``): one layer, 12 heads x d128, 4680
+queries, 120 history pages of 1560 tokens (187,200 keys) plus the 3 current
+pages, head-adaptive budgets k_h drawn from {2, 4, 8, 16}. The other
+workloads (single layer c2, prompt switch c4, streaming 30 layers c5) are
+reported as sub-objects (``--sub``).
+
+Every step and every phase is timed with its own HIP event pair on the
+stream the library launches on; ``value`` is the median step time over
+``--steps`` steps after ``--warmup`` untimed ones, with p10/p90 beside it.
 
 Prints one JSON line. ``value`` is milliseconds per chunk (lower is better);
 the line also carries effective TFLOP/s, per-phase times, the roofline of the
-dominant kernel (the attention kernel inside hsa_forward) and the fp64 oracle
+dominant kernel (the attention launch inside hsa_forward) and the fp64 oracle
 timed on this host's cores.
 """
 from __future__ import annotations
@@ -21,6 +27,8 @@ import json
 import os
 import sys
 import time
+
+import numpy as np
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
@@ -50,6 +58,8 @@ def state_flops_bytes(wl, n_pages):
 
 
 def time_loop(fn, iters, torch):
+    """Mean ms of fn over iters back-to-back calls (one event pair around all
+    of them, on torch's current stream, where the library launches)."""
     torch.cuda.synchronize()
     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     s.record()
@@ -58,6 +68,34 @@ def time_loop(fn, iters, torch):
     e.record()
     torch.cuda.synchronize()
     return s.elapsed_time(e) / iters
+
+
+def time_each(fn, iters, torch):
+    """Per-call ms of fn: one event pair around each call, on torch's current
+    stream (the stream the library launches on). Returns the sorted times."""
+    import numpy as np
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(iters)]
+    torch.cuda.synchronize()
+    for a, b in evs:
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    return np.sort(np.array([a.elapsed_time(b) for a, b in evs]))
+
+
+def time_med(fn, iters, torch):
+    """Median per-call ms of fn (time_each)."""
+    return float(np.median(time_each(fn, iters, torch)))
+
+
+def stats(t):
+    """median / p10 / p90 / mean of per-call times (ms)."""
+    import numpy as np
+    return {"median": round(float(np.median(t)), 4), "p10": round(float(np.percentile(t, 10)), 4),
+            "p90": round(float(np.percentile(t, 90)), 4), "mean": round(float(np.mean(t)), 4),
+            "n": int(len(t))}
 
 
 def kernel_source_hash() -> str:
@@ -93,15 +131,29 @@ def measured_traffic(workload: str, key: str = "hbm_bytes_per_launch"):
         return None
 
 
+def host_cpu():
+    """(logical CPUs, CPU model) of this host."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:  # pragma: no cover
+        pass
+    return os.cpu_count(), model
+
+
 def cpu_baseline(wl, dev, k_h, heads):
     """The fp64 oracle on this host's cores over a bounded sample of heads."""
-    import numpy as np
     from oracle import hsa_oracle as O
     try:
         from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
-        cores = os.cpu_count()
+        threads = 1
+    nproc, model = host_cpu()
     host = dict(q=dev["q"].float().cpu().numpy(), k_pool=dev["k_pool"].float().cpu().numpy(),
                 v_pool=dev["v_pool"].float().cpu().numpy(),
                 page_table=dev["page_table"].cpu().numpy())
@@ -110,18 +162,24 @@ def cpu_baseline(wl, dev, k_h, heads):
                   wl.n_cur, list(k_h), heads=heads)
     dt = time.perf_counter() - t0
     scale = wl.heads / len(heads)
-    return {"value": round(dt * scale * 1e3, 1), "unit": "ms/chunk", "cores": int(cores),
-            "kind": "oracle",
+    return {"value": round(dt * scale * 1e3, 1), "unit": "ms/chunk", "cores": int(threads),
+            "kind": "oracle", "nproc": nproc, "cpu_model": model,
+            "threads_note": "cores = BLAS threads the numpy oracle ran with (its matrix products "
+                            "are the multi-threaded part; the rest is one Python thread)",
             "sample": f"{len(heads)} of {wl.heads} heads of one {wl.name} chunk (all queries, "
                       f"cold state), {dt:.1f} s, scaled x{scale:g} to the chunk"}
 
 
-def bench_single(args, wl):
+def bench_core(args, wl, dev=None):
+    """One workload: the step (cold fold + hsa_forward) timed per step, its
+    phases, and the attention launch with its roofline. Returns (result,
+    layer, inputs, selection)."""
     import torch
     from paper_2609_34606_amd import HsaLayer, hsa_page_select
     from synth_inputs import make_case_torch
 
-    dev = make_case_torch(wl, "cuda:0")
+    if dev is None:
+        dev = make_case_torch(wl, "cuda:0")
     torch.cuda.synchronize()
     q, k_h = dev["q"], [int(x) for x in dev["k_h"]]
     k_max = max(1, max(k_h))
@@ -137,63 +195,86 @@ def bench_single(args, wl):
 
     for _ in range(args.warmup):
         step()
+    # the timed region: exactly `steps` steps between two synchronisations,
+    # each step bracketed by its own event pair
     torch.cuda.synchronize()
-    ms = time_loop(step, args.steps, torch)
-    log(f"step {ms:.4f} ms")
-    # phases, each timed over the same number of launches
-    ms_state = time_loop(lambda: layer.fold(0, n_pages), args.steps, torch)
-    ms_warm = time_loop(lambda: layer.fold(wl.n_cand, wl.n_cur), args.steps, torch)
+    t0 = time.perf_counter()
+    t_step = time_each(step, args.steps, torch)
+    wall_ms = (time.perf_counter() - t0) * 1e3
+    log(f"{wl.name}: step median {np.median(t_step):.4f} ms")
+    n = args.steps
+    t_state = time_each(lambda: layer.fold(0, n_pages), n, torch)
+    t_warm = time_each(lambda: layer.fold(wl.n_cand, wl.n_cur), n, torch)
     ws = layer.workspace("sel", 1 << 24)
-    ms_sel = time_loop(lambda: hsa_page_select(layer.cfg, q, n_q, layer.page_kmean, layer.max_pages,
-                                               wl.n_cand, k_h, k_max, sel, ws=ws), args.steps, torch)
-    ms_fwd = time_loop(lambda: layer.forward(q, wl.n_cand, wl.n_cur, k_h, k_max=k_max, out=out),
-                       args.steps, torch)
+    t_sel = time_each(lambda: hsa_page_select(layer.cfg, q, n_q, layer.page_kmean, layer.max_pages,
+                                              wl.n_cand, k_h, k_max, sel, ws=ws), n, torch)
+    t_fwd = time_each(lambda: layer.forward(q, wl.n_cand, wl.n_cur, k_h, k_max=k_max, out=out),
+                      n, torch)
     # the attention launch alone: sparse branch + linear branch + merge for the
-    # selection just computed (one kernel, plus a combine kernel when the
-    # schedule splits long page lists)
-    ms_attn = time_loop(lambda: layer.forward_selected(q, sel, wl.n_cand, wl.n_cur, k_h, k_max=k_max,
-                                                       out=out), args.steps, torch)
+    # selection just computed
+    t_attn = time_each(lambda: layer.forward_selected(q, sel, wl.n_cand, wl.n_cur, k_h, k_max=k_max,
+                                                      out=out), n, torch)
     k_eff = [min(k, wl.n_cand) for k in k_h]
     fa = attn_flops(wl, k_eff, n_q)
     fl = linear_flops(wl, n_q)
     fs, bs = state_flops_bytes(wl, n_pages)
     total = fa + fl + fs
     peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
-    achieved = fa / (ms_attn * 1e-3) / 1e12
+    ms = float(np.median(t_step))
+    ms_attn_mean = float(np.mean(t_attn))
+    achieved = fa / (ms_attn_mean * 1e-3) / 1e12
+    ms_state = float(np.median(t_state))
     res = {
-        "metric": "HSA ms/chunk + effective TFLOP/s (MFMA util %) at 12 heads x d128, 4680 queries",
-        "value": round(ms, 4), "unit": "ms/chunk", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": False,
-        "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
+        "value": round(ms, 4), "unit": "ms/chunk", "ms_per_step": round(ms, 4),
+        "step_ms": stats(t_step), "timed_region_wall_ms": round(wall_ms, 3),
         "effective_tflops": round(total / (ms * 1e-3) / 1e12, 2),
         "mfma_util_attention": round(achieved / peak, 4),
         "config": {"workload": wl.name, "batch": wl.batch, "heads": wl.heads,
                    "head_dim": wl.head_dim, "n_q": n_q, "page_size": wl.page_size,
                    "history_pages": wl.n_cand, "current_pages": wl.n_cur, "k_h": k_h,
                    "state": "cold (all pages folded every step)", "parallelism": "single GPU"},
-        "phases_ms": {"state_update_cold": round(ms_state, 4),
-                      "state_update_warm_current_pages": round(ms_warm, 4),
-                      "page_select": round(ms_sel, 4), "forward": round(ms_fwd, 4),
-                      "attention_launch": round(ms_attn, 4)},
+        "phases_ms": {"state_update_cold": stats(t_state),
+                      "state_update_warm_current_pages": stats(t_warm),
+                      "page_select": stats(t_sel), "forward": stats(t_fwd),
+                      "attention_launch": stats(t_attn)},
         "state_update_hbm_gbs": round(bs / (ms_state * 1e-3) / 1e9, 1),
         "state_update_hbm_frac": round(bs / (ms_state * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
                      "traffic": measured_traffic(wl.name),
-                     "kernel": "attn_pp_kernel (hsa_forward_selected launch)",
-                     "flops_per_launch": fa},
+                     "kernel": "attention launch of hsa_forward_selected (mean of per-launch "
+                               "HIP event times)",
+                     "flops_per_launch": fa,
+                     "frac_at_median_launch": round(fa / (float(np.median(t_attn)) * 1e-3) / 1e12 / peak, 4)},
     }
+    return res, layer, dev, sel
+
+
+def bench_single(args, wl):
+    import torch
+    res, layer, dev, sel = bench_core(args, wl)
+    q, k_h = dev["q"], [int(x) for x in dev["k_h"]]
+    k_max = max(1, max(k_h))
+    line = {
+        "metric": "HSA ms/chunk + effective TFLOP/s (MFMA util %) at 12 heads x d128, 4680 queries",
+        "value": res["value"], "unit": "ms/chunk", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": res["ms_per_step"], "higher_is_better": False,
+        "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
+    }
+    line.update({k: v for k, v in res.items() if k not in line})
     if not args.no_adaptive:
-        res["adaptive"] = bench_adaptive(args, wl, layer, q, k_h, k_max, sel)
+        line["adaptive"] = bench_adaptive(args, wl, layer, q, k_h, k_max, sel)
         if wl.dtype == "bf16":
-            res["linformer"] = bench_linformer(args, wl, layer, q, k_h, k_max, sel)
-            res["retrieval"] = bench_retrieval(args, wl, layer, q, k_h, k_max)
-            res["tier"] = bench_tier(args, wl, dev, layer, q, k_h, k_max, sel)
+            line["linformer"] = bench_linformer(args, wl, layer, q, k_h, k_max, sel)
+            line["retrieval"] = bench_retrieval(args, wl, layer, q, k_h, k_max)
+            line["tier"] = bench_tier(args, wl, dev, layer, q, k_h, k_max, sel)
     if not args.no_cpu_baseline:
         heads = list(range(wl.heads)) if wl.heads * wl.n_pages <= 12 * 24 else [0, 1]
         log("timing the oracle on the host ...")
-        res["cpu_baseline"] = cpu_baseline(wl, dev, k_h, heads)
-    return res
+        line["cpu_baseline"] = cpu_baseline(wl, dev, k_h, heads)
+    del layer, dev, sel
+    torch.cuda.empty_cache()
+    return line
 
 
 def kept_work(wl, sel_row, kept, n_kept, n_q):
@@ -248,15 +329,15 @@ def bench_adaptive(args, wl, layer, q, k_h, k_max, sel):
 
     for _ in range(args.warmup):
         step()
-    ms = time_loop(step, args.steps, torch)
-    ms_fwd = time_loop(lambda: layer.forward_adaptive(q, wl.n_cand, wl.n_cur, k_h, k_max=k_max,
+    ms = time_med(step, args.steps, torch)
+    ms_fwd = time_med(lambda: layer.forward_adaptive(q, wl.n_cand, wl.n_cur, k_h, k_max=k_max,
                                                       out=out, sel_out=sel), args.steps, torch)
     ws = layer.workspace("adaptive_parts", hsa_adaptive_workspace_size(layer.cfg, n_q, k_max,
                                                                        wl.n_cur))
-    ms_bsel = time_loop(lambda: hsa_block_select(layer.cfg, q, n_q, layer.pool, sel, k_max,
+    ms_bsel = time_med(lambda: hsa_block_select(layer.cfg, q, n_q, layer.pool, sel, k_max,
                                                  wl.n_cand, wl.n_cur, ws=ws), args.steps, torch)
     o_sp = torch.empty(q.shape, dtype=torch.float32, device=q.device)
-    ms_sp = time_loop(lambda: hsa_sparse_attn_adaptive(layer.cfg, q, n_q, layer.pool, sel, k_max,
+    ms_sp = time_med(lambda: hsa_sparse_attn_adaptive(layer.cfg, q, n_q, layer.pool, sel, k_max,
                                                        k_h, wl.n_cand, wl.n_cur, o_sp, ws=ws),
                       args.steps, torch)
     # kept sets of this chunk (untimed) for the algorithmic flops
@@ -319,16 +400,16 @@ def bench_linformer(args, wl, layer, q, k_h, k_max, sel, rank=64):
 
     for _ in range(args.warmup):
         step()
-    ms = time_loop(step, args.steps, torch)
-    ms_cold = time_loop(lambda: layer.compress(0, n_pages), args.steps, torch)
-    ms_warm = time_loop(lambda: layer.compress(wl.n_cand, wl.n_cur), args.steps, torch)
-    ms_fwd = time_loop(lambda: layer.forward_linformer(q, wl.n_cand, wl.n_cur, k_h, k_max=k_max,
+    ms = time_med(step, args.steps, torch)
+    ms_cold = time_med(lambda: layer.compress(0, n_pages), args.steps, torch)
+    ms_warm = time_med(lambda: layer.compress(wl.n_cand, wl.n_cur), args.steps, torch)
+    ms_fwd = time_med(lambda: layer.forward_linformer(q, wl.n_cand, wl.n_cur, k_h, k_max=k_max,
                                                        out=out, sel_out=sel), args.steps, torch)
     crank = mkcfg(wl.batch, wl.heads, wl.head_dim, rank, q.dtype)
     cpool = kv_pool(layer.ck, layer.cv, layer.page_table, crank)
     o_lin = torch.empty(q.shape, dtype=torch.float32, device=q.device)
     ws = layer.workspace("lin_attn", hsa_sparse_attn_workspace_size(crank, n_q, k_max, wl.n_cur))
-    ms_br = time_loop(lambda: hsa_sparse_attn(crank, q, n_q, cpool, sel, k_max, k_h, wl.n_cand,
+    ms_br = time_med(lambda: hsa_sparse_attn(crank, q, n_q, cpool, sel, k_max, k_h, wl.n_cand,
                                               wl.n_cur, o_lin, ws=ws), args.steps, torch)
     k_eff = [min(k, wl.n_cand) for k in k_h]
     fb = sum(4.0 * n_q * (k + wl.n_cur) * rank * wl.head_dim for k in k_eff) * wl.batch
@@ -363,11 +444,11 @@ def bench_retrieval(args, wl, layer, q, k_h, k_max):
     pe, ce, cf = t(pe), t(ce), t(cf)
     M, E = ce.shape[1], ce.shape[2]
     rng = torch.empty((wl.batch, 2), dtype=torch.int32, device=q.device)
-    ms_s1 = time_loop(lambda: hsa_chunk_select(layer.cfg, pe, ce, E, M, cf, wl.n_cand, rng),
+    ms_s1 = time_med(lambda: hsa_chunk_select(layer.cfg, pe, ce, E, M, cf, wl.n_cand, rng),
                       args.steps, torch)
     out = torch.empty_like(q)
     ws = layer.workspace("retrieval", hsa_retrieval_workspace_size(layer.cfg, wl.n_q, k_max, wl.n_cur))
-    ms_fwd = time_loop(lambda: hsa_forward_retrieval(
+    ms_fwd = time_med(lambda: hsa_forward_retrieval(
         layer.cfg, q, wl.n_q, layer.pool, pe, ce, E, M, cf, wl.n_cand, wl.n_cur, k_h, k_max,
         layer.kv_state, layer.k_state, layer.page_kmean, None, None, out, ws=ws), args.steps, torch)
     return {"chunks": M, "emb_dim": E, "pages_per_chunk": int(cf[0, 1] - cf[0, 0]),
@@ -564,7 +645,9 @@ def bench_streaming(args, wl):
         "data": "synthetic",
         "effective_tflops": round(flops / (seq.sum() * 1e-3) / 1e12, 2),
         "ms_per_chunk_t_ge_4": round(float(seq[3:].mean()), 3) if T > 3 else None,
+        "chunk_ms": stats(np.sort(seq)),
         "batched_layers": {"ms_per_chunk": round(float(bat.mean()), 3),
+                           "chunk_ms": stats(np.sort(bat)),
                            "ms_per_chunk_t_ge_4": round(float(bat[3:].mean()), 3) if T > 3 else None,
                            "effective_tflops": round(flops / (bat.sum() * 1e-3) / 1e12, 2)},
         "config": {"workload": wl.name, "layers": L, "chunks": T, "heads": H, "head_dim": d,
@@ -574,15 +657,35 @@ def bench_streaming(args, wl):
     }
 
 
+def bench_sub(args, name):
+    """A further workload as a sub-object of the line: its step and phase
+    times and the attention roofline (c2, c4), or the streaming summary (c5)."""
+    import torch
+    from synth_inputs import WORKLOADS
+    wl = WORKLOADS[name]
+    if wl.layers > 1:
+        r = bench_streaming(args, wl)
+        keep = ("value", "unit", "ms_per_step", "effective_tflops", "ms_per_chunk_t_ge_4",
+                "chunk_ms", "batched_layers", "config")
+        return {k: r[k] for k in keep if k in r}
+    r, layer, dev, sel = bench_core(args, wl)
+    del layer, dev, sel
+    torch.cuda.empty_cache()
+    return r
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", default="c2", help="c1..c5")
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="c3", help="main workload, c1..c5")
+    ap.add_argument("--sub", default="c2,c4,c5",
+                    help="comma-separated further workloads reported as sub-objects ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-adaptive", action="store_true",
-                    help="skip the head-adaptive block-sparse measurement")
+                    help="skip the head-adaptive block-sparse, Linformer, retrieval and tier "
+                         "measurements")
     ap.add_argument("--layers", type=int, default=0, help="c5 only: override the layer count")
     ap.add_argument("--chunks", type=int, default=0, help="c5 only: override the chunk count")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -595,9 +698,18 @@ def main():
               "(sharding over heads or pages is described in the design notes, not implemented); "
               "run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    if args.steps < 1:
+        print("--steps must be >= 1", file=sys.stderr)
+        sys.exit(2)
     from synth_inputs import WORKLOADS
     wl = WORKLOADS[args.config]
     res = bench_streaming(args, wl) if wl.layers > 1 else bench_single(args, wl)
+    subs = [x for x in args.sub.split(",") if x and x != args.config]
+    if subs:
+        res["sub_configs"] = {}
+        for name in subs:
+            log(f"sub-workload {name} ...")
+            res["sub_configs"][name] = bench_sub(args, name)
     if args.copy_calibration:
         import torch
         n = args.copy_calibration << 20

@@ -162,11 +162,19 @@ size_t partial_ws_bytes(const hsa_config_t* c, int n_q) {
   return attention_partial_bytes(c->batch, c->head_dim, n_q, kPartPerHead * c->num_heads);
 }
 
+// Split partials of a planned launch: the schedule's p.sc.n_part slots (at
+// most kPartPerHead * H, what partial_ws_bytes provides for), the LSE
+// partials after the output partials.
 void set_partials(AttnParams& p, const hsa_config_t* c, int n_q, void* base) {
   p.part_o = static_cast<float*>(base);
   p.part_lse = reinterpret_cast<float*>(
-      static_cast<uint8_t*>(base) +
-      attention_partial_o_bytes(c->batch, c->head_dim, n_q, kPartPerHead * c->num_heads));
+      static_cast<uint8_t*>(base) + attention_partial_o_bytes(c->batch, c->head_dim, n_q, p.sc.n_part));
+}
+
+// Bytes of split partials a planned launch writes.
+size_t planned_partial_bytes(const AttnParams& p, const hsa_config_t* c, int n_q) {
+  if (c->dtype != HSA_DTYPE_BF16 || p.sc.n_part == 0) return 0;
+  return attention_partial_bytes(c->batch, c->head_dim, n_q, p.sc.n_part);
 }
 
 hsa_status_t from_hip(hipError_t e) { return e == hipSuccess ? HSA_OK : HSA_ERR_DEVICE; }
@@ -665,6 +673,17 @@ hsa_status_t check_forward(const hsa_config_t* cfg, const void* q, int32_t n_q,
   return HSA_OK;
 }
 
+// Schedule of the attention launch of the forward calls: each head's list
+// is its selected pages (at most n_cand) plus the current pages.
+bool plan_attend(AttnParams& p, const hsa_config_t* cfg, int n_q, const int32_t* k_h, int n_cand,
+                 int n_cur_pages, bool tile_lists) {
+  int list_len[HSA_MAX_HEADS];
+  for (int h = 0; h < cfg->num_heads; ++h) list_len[h] = std::min(k_h[h], n_cand) + n_cur_pages;
+  return plan_attention(p, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
+                        kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16,
+                        tile_lists ? 4 : kPageWaves);
+}
+
 // Sparse branch + linear branch + gated fusion for a selection in `sel`.
 hsa_status_t run_attend(const hsa_config_t* cfg, const void* q, int32_t n_q,
                         const hsa_kv_pool_t* pool, const int32_t* sel, int32_t k_max,
@@ -697,14 +716,28 @@ hsa_status_t run_attend(const hsa_config_t* cfg, const void* q, int32_t n_q,
   p.g_sp = g_sp;
   p.gate_elem = cfg->gate_dims > 1;
   p.o = o;
-  int list_len[HSA_MAX_HEADS];
-  for (int h = 0; h < cfg->num_heads; ++h) list_len[h] = std::min(k_h[h], n_cand) + n_cur_pages;
-  if (!plan_attention(p, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
-                      kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16, w ? 4 : kPageWaves))
-    return HSA_ERR_UNSUPPORTED;
+  if (!plan_attend(p, cfg, n_q, k_h, n_cand, n_cur_pages, w != nullptr)) return HSA_ERR_UNSUPPORTED;
   if (cfg->dtype == HSA_DTYPE_BF16) set_partials(p, cfg, n_q, partials);
   if (w) set_block_lists(p, *w, wbase);
   return from_hip(launch_attention(cfg->dtype, cfg->head_dim, cfg->batch, p, s));
+}
+
+// hsa_forward after its checks: page selection into sel_out (or the
+// workspace), then the attention launch. Workspace layout: [query sums]
+// [selection][split partials].
+hsa_status_t forward_body(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                          const hsa_kv_pool_t* pool, int32_t n_cand, int32_t n_cur_pages,
+                          const int32_t* k_h, int32_t k_max, const float* kv_state,
+                          const float* k_state, const double* page_kmean, const float* g_lin,
+                          const float* g_sp, void* o, int32_t* sel_out, uint8_t* base,
+                          hipStream_t s) {
+  int32_t* sel = sel_out ? sel_out : reinterpret_cast<int32_t*>(base + select_ws_bytes(cfg, n_q));
+  void* partials = base + select_ws_bytes(cfg, n_q) + sel_ws_bytes(cfg, k_max);
+  hsa_status_t st =
+      run_select(cfg, q, n_q, page_kmean, pool->max_pages, n_cand, k_h, k_max, sel, nullptr, base, s);
+  if (st != HSA_OK) return st;
+  return run_attend(cfg, q, n_q, pool, sel, k_max, k_h, n_cand, n_cur_pages, kv_state, k_state,
+                    g_lin, g_sp, o, partials, s);
 }
 
 }  // namespace
@@ -725,13 +758,8 @@ hsa_status_t hsa_forward(const hsa_config_t* cfg, const void* q, int32_t n_q,
   if ((st = check_ws(ws, ws_bytes, need)) != HSA_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if ((st = validate_pages(cfg, pool, 0, n_cand + n_cur_pages, s)) != HSA_OK) return st;
-  uint8_t* base = static_cast<uint8_t*>(ws);
-  int32_t* sel = sel_out ? sel_out : reinterpret_cast<int32_t*>(base + select_ws_bytes(cfg, n_q));
-  void* partials = base + select_ws_bytes(cfg, n_q) + sel_ws_bytes(cfg, k_max);
-  st = run_select(cfg, q, n_q, page_kmean, pool->max_pages, n_cand, k_h, k_max, sel, nullptr, ws, s);
-  if (st != HSA_OK) return st;
-  return run_attend(cfg, q, n_q, pool, sel, k_max, k_h, n_cand, n_cur_pages, kv_state, k_state,
-                    g_lin, g_sp, o, partials, s);
+  return forward_body(cfg, q, n_q, pool, n_cand, n_cur_pages, k_h, k_max, kv_state, k_state,
+                      page_kmean, g_lin, g_sp, o, sel_out, static_cast<uint8_t*>(ws), s);
 }
 
 hsa_status_t hsa_forward_selected(const hsa_config_t* cfg, const void* q, int32_t n_q,

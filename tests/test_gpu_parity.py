@@ -114,22 +114,89 @@ def _rows(n_q, k=192, seed=0):
     return np.unique(np.concatenate([r, [t for t in tail if 0 <= t < n_q]]))
 
 
-def _full_size(name, rows_k=160):
+def _full_size(name, rows_k=None, gate_cases=True):
+    """A full-size workload through the library and the oracle. rows_k None
+    compares every query row; otherwise a sample of rows_k rows plus the
+    first, last and tile-boundary rows. With gate_cases, the same layer also
+    runs with saturated gates (see _saturated_gates)."""
     import torch
     from synth_inputs import make_case_torch
     wl = WORKLOADS[name]
-    say(f"[case] full-size {wl.name}")
+    say(f"[case] full-size {wl.name} rows={'all' if rows_k is None else rows_k}")
     dev = make_case_torch(wl, "cuda:0")
     torch.cuda.synchronize()
     k_h = dev["k_h"]
-    gpu, _ = run_library(wl, dev, k_h)
+    gpu, layer = run_library(wl, dev, k_h)
     host = {k: (None if v is None else v.float().cpu().numpy())
             for k, v in dev.items() if k in ("q", "k_pool", "v_pool")}
     host["page_table"] = dev["page_table"].cpu().numpy()
-    rows = _rows(wl.n_q, rows_k)
+    rows = None if rows_k is None else _rows(wl.n_q, rows_k)
     ref = run_oracle(host, wl, k_h, rows=rows)
     compare(gpu, ref, wl, k_h, rows=rows)
+    if gate_cases:
+        _saturated_gates(wl, dev, layer, ref, rows)
     return gpu, ref, dev
+
+
+def _saturated_gates(wl, dev, layer, ref, rows):
+    """Gate logits of +-40 make one branch's weight 1 (to fp32 precision) and
+    the other's 4e-18, so O is the linear branch alone or the sparse branch
+    alone (Sec. 3.3 "Gated fusion"). Head-wise gates isolate each branch for
+    whole rows; element-wise gates alternate the branch by output dim. The
+    expected values are the oracle's merge of its own two branches."""
+    import torch
+    from oracle import hsa_oracle as O
+    from paper_2609_34606_amd import HsaLayer
+    from hsa_testlib import BF16_TOL, F32_TOL, assert_close, to_host
+    tol = BF16_TOL if wl.dtype == "bf16" else F32_TOL
+    B, n_q, H, d = dev["q"].shape
+    k_h = [int(x) for x in dev["k_h"]]
+    k_max = max(1, max(k_h))
+    r = slice(None) if rows is None else np.asarray(rows)
+    ones = torch.ones((B, n_q, H), dtype=torch.float32, device=dev["q"].device) * 40.0
+    elem = torch.ones((B, n_q, H, d), dtype=torch.float32, device=dev["q"].device) * 40.0
+    elem[..., 1::2] = -40.0
+    lay_e = HsaLayer(B, H, d, wl.page_size, dev["q"].dtype, dev["q"].device, k_pool=dev["k_pool"],
+                     v_pool=dev["v_pool"], page_table=dev["page_table"], gate_dims=d)
+    lay_e.kv_state, lay_e.k_state, lay_e.page_kmean = layer.kv_state, layer.k_state, layer.page_kmean
+    cases = [("linear branch alone (head-wise +40/-40)", layer, ones, -ones),
+             ("sparse branch alone (head-wise -40/+40)", layer, -ones, ones),
+             ("branches by dim (element-wise +-40)", lay_e, elem, -elem)]
+    for what, lay, gl, gs in cases:
+        o = lay.forward(dev["q"], wl.n_cand, wl.n_cur, k_h, k_max=k_max, g_lin=gl, g_sp=gs)
+        torch.cuda.synchronize()
+        glh, gsh = to_host(gl)[:, r], to_host(gs)[:, r]
+        want = np.stack([O.gated_merge(ref["O_lin"][:, :, h], ref["O_sp"][:, :, h], glh[:, :, h],
+                                       gsh[:, :, h]) for h in range(H)], 2)
+        assert_close(f"O, {what}", to_host(o)[:, r], want, **tol)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("uneven", [False, True])
+def test_saturated_gates_isolate_each_branch(dtype, uneven):
+    # small cases on the page walk (uneven = False) and on a schedule that
+    # splits the long list of one head across work items and merges the
+    # splits before the epilogue (uneven = True; bf16 only splits)
+    import ctypes
+    from paper_2609_34606_amd import config, lib
+    wl = SMALL.replace(dtype=dtype, seed=51, gates=False)
+    if uneven:
+        wl = wl.replace(heads=2, n_q=600, page_size=64, n_cand=40, n_cur=2, k_h=(1, 40), seed=52)
+        if dtype == "bf16":
+            lens = (ctypes.c_int32 * 2)(1 + 2, 40 + 2)
+            widest = ctypes.c_int32()
+            cfg = config(1, 2, 128, 64, "bf16")
+            assert lib().hsa_attention_plan(ctypes.byref(cfg), 600, lens, 0, None, None,
+                                            ctypes.byref(widest)) == 0
+            assert widest.value > 1, "the case must split a list"
+    say(f"[case] saturated gates {wl}")
+    case = make_case(wl)
+    dev = upload(case)
+    dev["k_h"] = case.k_h
+    gpu, layer = run_library(wl, dev, case.k_h, with_parts=False)
+    ref = run_oracle(_case_dict(case), wl, case.k_h)
+    compare(gpu, ref, wl, case.k_h)
+    _saturated_gates(wl, dev, layer, ref, None)
 
 
 def test_c2_single_layer_full_size():
@@ -141,7 +208,7 @@ def test_c3_long_history_full_size():
 
 
 def test_c4_prompt_switch_recall_full_size():
-    gpu, ref, dev = _full_size("c4", rows_k=96)
+    gpu, ref, dev = _full_size("c4")
     pc, cs = dev["meta"]["page_cluster"], dev["meta"]["c_star"]
     star = set(np.nonzero(pc == cs)[0].tolist())
     for h in range(gpu["sel"].shape[1]):
@@ -222,12 +289,118 @@ def test_streaming_incremental_state_and_outputs():
     np.testing.assert_array_equal(layer.page_kmean.cpu().numpy(), cold.page_kmean.cpu().numpy())
 
 
-def test_c5_last_chunk_full_size():
-    # streaming workload at its longest history: chunk 60, 177 history pages
+def _stream_pages(wl, layers, T, device="cuda:0"):
+    """The streaming workload's pages of chunks 1..T for `layers` layers on
+    one shared pool (layer l owns slots [l*3T, (l+1)*3T)), as the bench
+    draws them, and each layer's query chunks."""
+    import torch
+    from synth_inputs import make_case_torch
     from synth_inputs.configs import streaming_chunk
-    wl = streaming_chunk(WORKLOADS["c5"], 60)
-    WORKLOADS["_c5_t60"] = wl
-    try:
-        _full_size("_c5_t60", rows_k=96)
-    finally:
-        del WORKLOADS["_c5_t60"]
+    npg = wl.n_cur * T
+    H, d, P = wl.heads, wl.head_dim, wl.page_size
+    k_pool = torch.empty((layers * npg, H, P, d), dtype=torch.bfloat16, device=device)
+    v_pool = torch.empty((layers * npg, H, d, P), dtype=torch.bfloat16, device=device)
+    table = torch.full((layers, npg), -1, dtype=torch.int32, device=device)
+    qs = {}
+    for t in range(1, T + 1):
+        wt = streaming_chunk(wl, t).replace(n_cand=0)
+        for l in range(layers):
+            dd = make_case_torch(wt, device, layer=l, chunk=t, k_pool=k_pool, v_pool=v_pool,
+                                 slot_base=l * npg + wl.n_cur * (t - 1))
+            table[l, wl.n_cur * (t - 1):wl.n_cur * t] = dd["page_table"][0]
+            qs[(l, t)] = dd["q"]
+    torch.cuda.synchronize()
+    return k_pool, v_pool, table, qs
+
+
+def _layer_host(k_pool, v_pool, table, l, npg):
+    """Host copies of layer l's slots, with its page table rebased to them."""
+    sl = slice(l * npg, (l + 1) * npg)
+    return dict(k_pool=k_pool[sl].float().cpu().numpy(), v_pool=v_pool[sl].float().cpu().numpy(),
+                page_table=(table[l:l + 1] - l * npg).cpu().numpy())
+
+
+def test_c5_sixty_incremental_chunks_full_size():
+    # One layer of the streaming workload at full shape: 60 chunks, each
+    # folding its 3 new pages (4680 keys) into the state and page index and
+    # running the forward pass over the grown history. After chunk 60 the
+    # state (180 pages, 280,800 keys) must equal a cold fold of the same pages
+    # and the oracle's, and the chunk-60 output (177 history pages, k_h = 8)
+    # the oracle's.
+    import torch
+    from hsa_testlib import BF16_TOL, assert_close
+    from paper_2609_34606_amd import HsaLayer
+    wl = WORKLOADS["c5"]
+    T = wl.chunks
+    say(f"[case] c5 one layer, {T} incremental chunks")
+    k_pool, v_pool, table, qs = _stream_pages(wl, 1, T)
+    H, d, P = wl.heads, wl.head_dim, wl.page_size
+    k_h = list(wl.budgets())
+    layer = HsaLayer(1, H, d, P, torch.bfloat16, "cuda:0", k_pool=k_pool, v_pool=v_pool,
+                     page_table=table)
+    sel = torch.full((1, H, max(k_h)), -7, dtype=torch.int32, device="cuda:0")
+    for t in range(1, T + 1):
+        n_cand = wl.n_cur * (t - 1)
+        layer.fold(n_cand, wl.n_cur)
+        o = layer.forward(qs[(0, t)], n_cand, wl.n_cur, k_h, sel_out=sel)
+    torch.cuda.synchronize()
+    npg = wl.n_cur * T
+    cold = HsaLayer(1, H, d, P, torch.bfloat16, "cuda:0", k_pool=k_pool, v_pool=v_pool,
+                    page_table=table)
+    cold.fold(0, npg)
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(layer.kv_state.cpu().numpy(), cold.kv_state.cpu().numpy(),
+                               rtol=1e-5, atol=2e-3)
+    np.testing.assert_allclose(layer.k_state.cpu().numpy(), cold.k_state.cpu().numpy(), rtol=1e-5)
+    np.testing.assert_array_equal(layer.page_kmean.cpu().numpy(), cold.page_kmean.cpu().numpy())
+    host = _layer_host(k_pool, v_pool, table, 0, npg)
+    host["q"] = qs[(0, T)].float().cpu().numpy()
+    wt = wl.replace(n_cand=wl.n_cur * (T - 1), layers=1, chunks=1)
+    rows = _rows(wl.n_q, 96)
+    ref = run_oracle(host, wt, k_h, rows=rows)
+    np.testing.assert_array_equal(sel.cpu().numpy(), ref["sel"])
+    assert_close("kv_state after 60 folds", np.swapaxes(layer.kv_state.cpu().numpy(), -1, -2),
+                 ref["S"], max_abs=np.inf, rel_l2=4e-3)
+    assert_close("k_state after 60 folds", layer.k_state.cpu().numpy(), ref["z"], max_abs=np.inf,
+                 rel_l2=1e-5)
+    assert_close("O chunk 60", o.float().cpu().numpy()[:, rows], ref["O"], **BF16_TOL)
+
+
+def test_c5_batched_layers_full_size():
+    # The streaming workload's batched launch mode: the 30 layers are the 30
+    # batch entries of one hsa_state_update and one hsa_forward over a shared
+    # pool (each layer's pages its own page-table row), at chunk 10 (27
+    # history pages + 3 current per layer). Every layer is checked against the
+    # oracle on its own pages: selection bit-exact, state, and O on sampled
+    # rows.
+    import torch
+    from hsa_testlib import BF16_TOL, assert_close
+    from paper_2609_34606_amd import HsaLayer
+    wl = WORKLOADS["c5"]
+    T, L = 10, wl.layers
+    say(f"[case] c5 batched {L} layers at chunk {T}")
+    k_pool, v_pool, table, qs = _stream_pages(wl, L, T)
+    H, d, P = wl.heads, wl.head_dim, wl.page_size
+    npg = wl.n_cur * T
+    k_h = list(wl.budgets())
+    n_cand = wl.n_cur * (T - 1)
+    q = torch.cat([qs[(l, T)] for l in range(L)], 0).contiguous()
+    layer = HsaLayer(L, H, d, P, torch.bfloat16, "cuda:0", k_pool=k_pool, v_pool=v_pool,
+                     page_table=table)
+    layer.fold(0, npg)
+    sel = torch.full((L, H, max(k_h)), -7, dtype=torch.int32, device="cuda:0")
+    o = layer.forward(q, n_cand, wl.n_cur, k_h, sel_out=sel)
+    torch.cuda.synchronize()
+    o_h, sel_h = o.float().cpu().numpy(), sel.cpu().numpy()
+    S_h, z_h = layer.kv_state.cpu().numpy(), layer.k_state.cpu().numpy()
+    wt = wl.replace(n_cand=n_cand, layers=1, chunks=1)
+    rows = _rows(wl.n_q, 32, seed=3)
+    for l in range(L):
+        host = _layer_host(k_pool, v_pool, table, l, npg)
+        host["q"] = qs[(l, T)].float().cpu().numpy()
+        ref = run_oracle(host, wt, k_h, rows=rows)
+        np.testing.assert_array_equal(sel_h[l:l + 1], ref["sel"], err_msg=f"layer {l}")
+        assert_close(f"layer {l} kv_state", np.swapaxes(S_h[l:l + 1], -1, -2), ref["S"],
+                     max_abs=np.inf, rel_l2=4e-3)
+        assert_close(f"layer {l} k_state", z_h[l:l + 1], ref["z"], max_abs=np.inf, rel_l2=1e-5)
+        assert_close(f"layer {l} O", o_h[l:l + 1, rows], ref["O"], **BF16_TOL)
