@@ -255,6 +255,36 @@ hsa_status_t hsa_forward_selected(const hsa_config_t* cfg, const void* q, int32_
                                   void* o, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * hsa_forward_noalloc -- hsa_forward for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc. Same arguments, computation and outputs as hsa_forward,
+ * except that there is no ws / ws_bytes: the workspace is a library-owned
+ * static device buffer of HSA_NOALLOC_SCRATCH_BYTES bytes. Each GPU the
+ * library runs on holds its own copy of that buffer from the first use of
+ * the library on it until the process ends. The call allocates nothing and
+ * frees nothing (no hipMalloc / hipFree, no allocating library routine).
+ *
+ * hsa_forward_noalloc_bytes returns the bytes of that buffer a call with
+ * these sizes uses (query sums, the selection when sel_out is NULL, and the
+ * split partials of the attention schedule it plans), or 0 on invalid input.
+ * A call that needs more than HSA_NOALLOC_SCRATCH_BYTES returns
+ * HSA_ERR_WORKSPACE without launching (use hsa_forward with a larger
+ * workspace then). The buffer keeps the last call's contents; every byte a
+ * call reads it first writes in the same call. Calls that overlap on one GPU
+ * (on different streams, or from different threads without ordering) share
+ * the one buffer and race: serialise them.
+ */
+#define HSA_NOALLOC_SCRATCH_BYTES (128u << 20)
+size_t hsa_forward_noalloc_bytes(const hsa_config_t* cfg, int32_t n_q, int32_t n_cand,
+                                 int32_t n_cur_pages, const int32_t* k_h, int32_t k_max);
+hsa_status_t hsa_forward_noalloc(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                                 const hsa_kv_pool_t* pool, int32_t n_cand, int32_t n_cur_pages,
+                                 const int32_t* k_h, int32_t k_max, const float* kv_state,
+                                 const float* k_state, const double* page_kmean,
+                                 const float* g_lin, const float* g_sp, void* o,
+                                 int32_t* sel_out, void* stream);
+
+/*
  * Head-adaptive block-sparse sparse branch (Sec. 3.3 "Sparse branch" and
  * "Head-level sparsity adaptation"; the appendix on the sparse branch defines
  * the pooled map, the coverage rule and the Gini coefficient; Sec. 4.5 fixes

@@ -20,6 +20,8 @@ from .hsa import (  # noqa: F401
     hsa_block_select,
     hsa_chunk_select,
     hsa_forward_adaptive,
+    hsa_forward_noalloc,
+    hsa_forward_noalloc_bytes,
     hsa_forward_retrieval,
     hsa_retrieval_workspace_size,
     hsa_forward_linformer,

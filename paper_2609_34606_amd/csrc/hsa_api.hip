@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "hsa_kernels.h"
@@ -954,6 +955,73 @@ hsa_status_t hsa_forward_linformer(const hsa_config_t* cfg, const void* q, int32
   if (st != HSA_OK) return st;
   return run_attend(cfg, q, n_q, pool, sel, k_max, k_h, n_cand, n_cur_pages, nullptr, nullptr,
                     g_lin, g_sp, o, base + w.part_off, s, &w, base, o_lin);
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------- no-allocation forward
+// hsa_forward_noalloc runs hsa_forward with its workspace in `scratch`, a
+// file-scope device array. Each GPU the library runs on holds its own copy
+// (allocated when the code object is loaded on that device, kept until the
+// process ends). In host code `scratch` names a host-side stand-in, not the
+// device memory: its device address is taken once per device with
+// hipGetSymbolAddress and only that address is ever passed to kernels.
+// The forward kernels write every workspace byte they read within a call
+// (query sums, selection, split partials), so nothing needs clearing.
+namespace {
+
+__device__ __align__(256) uint8_t scratch[HSA_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint8_t* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's scratch address (NULL on failure).
+uint8_t* scratch_for_current_device() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    g_scratch_ptr[dev] = static_cast<uint8_t*>(ptr);
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t hsa_forward_noalloc_bytes(const hsa_config_t* cfg, int32_t n_q, int32_t n_cand,
+                                 int32_t n_cur_pages, const int32_t* k_h, int32_t k_max) {
+  if (check_cfg(cfg) != HSA_OK || !k_h || n_q < 1 || n_cand < 0 || n_cur_pages < 0 || k_max < 1)
+    return 0;
+  if (check_budgets(cfg, k_h, k_max) != HSA_OK) return 0;
+  AttnParams p{};
+  if (!plan_attend(p, cfg, n_q, k_h, n_cand, n_cur_pages, false)) return 0;
+  return select_ws_bytes(cfg, n_q) + sel_ws_bytes(cfg, k_max) + planned_partial_bytes(p, cfg, n_q);
+}
+
+hsa_status_t hsa_forward_noalloc(const hsa_config_t* cfg, const void* q, int32_t n_q,
+                                 const hsa_kv_pool_t* pool, int32_t n_cand, int32_t n_cur_pages,
+                                 const int32_t* k_h, int32_t k_max, const float* kv_state,
+                                 const float* k_state, const double* page_kmean,
+                                 const float* g_lin, const float* g_sp, void* o,
+                                 int32_t* sel_out, void* stream) {
+  hsa_status_t st = check_forward(cfg, q, n_q, pool, n_cand, n_cur_pages, k_h, k_max, kv_state,
+                                  k_state, o);
+  if (st != HSA_OK) return st;
+  if (!page_kmean) return HSA_ERR_INVALID_ARG;
+  const size_t need = hsa_forward_noalloc_bytes(cfg, n_q, n_cand, n_cur_pages, k_h, k_max);
+  if (need == 0) return HSA_ERR_UNSUPPORTED;
+  if (need > (size_t)HSA_NOALLOC_SCRATCH_BYTES) return HSA_ERR_WORKSPACE;
+  uint8_t* base = scratch_for_current_device();
+  if (!base) return HSA_ERR_DEVICE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = validate_pages(cfg, pool, 0, n_cand + n_cur_pages, s)) != HSA_OK) return st;
+  return forward_body(cfg, q, n_q, pool, n_cand, n_cur_pages, k_h, k_max, kv_state, k_state,
+                      page_kmean, g_lin, g_sp, o, sel_out, base, s);
 }
 
 }  // extern "C"

@@ -110,6 +110,11 @@ def lib():
     L.hsa_tier_locate.argtypes = [c_vp, c_i32, c_i32]
     L.hsa_tier_stats.restype = None
     L.hsa_tier_stats.argtypes = [c_vp, P(HsaTierStats)]
+    L.hsa_forward_noalloc_bytes.restype = c_sz
+    L.hsa_forward_noalloc_bytes.argtypes = [P(HsaConfig), c_i32, c_i32, c_i32, c_vp, c_i32]
+    L.hsa_forward_noalloc.restype = ctypes.c_int
+    L.hsa_forward_noalloc.argtypes = [P(HsaConfig), c_vp, c_i32, P(HsaKvPool), c_i32, c_i32, c_vp,
+                                      c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp]
     L.hsa_attention_plan.restype = ctypes.c_int
     L.hsa_attention_plan.argtypes = [P(HsaConfig), c_i32, c_vp, c_i32, c_vp, c_vp, c_vp]
     L.hsa_block_count.restype = c_i32
@@ -344,6 +349,26 @@ def hsa_forward_selected(cfg, q, n_q, pool, sel, k_max, k_h, n_cand, n_cur_pages
                                     0 if ws is None else ws.numel(), _stream(stream))
     if check:
         _check("hsa_forward_selected", st)
+    return st
+
+
+def hsa_forward_noalloc_bytes(cfg, n_q, n_cand, n_cur_pages, k_h, k_max) -> int:
+    _keep, kp = _budgets(k_h)
+    return lib().hsa_forward_noalloc_bytes(ctypes.byref(cfg), n_q, n_cand, n_cur_pages, kp, k_max)
+
+
+def hsa_forward_noalloc(cfg, q, n_q, pool, n_cand, n_cur_pages, k_h, k_max, kv_state, k_state,
+                        page_kmean, g_lin, g_sp, o, sel_out=None, stream=None, check=True) -> int:
+    """hsa_forward with the library's static per-GPU workspace (no device
+    allocation by the library or by this binding)."""
+    _keep, kp = _budgets(k_h)
+    qp, op = _rows(cfg, q, n_q, "q"), _rows(cfg, o, n_q, "o")
+    glp, gsp = _gate(cfg, g_lin, n_q), _gate(cfg, g_sp, n_q)
+    st = lib().hsa_forward_noalloc(ctypes.byref(cfg), qp, n_q, ctypes.byref(pool), n_cand,
+                                   n_cur_pages, kp, k_max, _ptr(kv_state), _ptr(k_state),
+                                   _ptr(page_kmean), glp, gsp, op, _ptr(sel_out), _stream(stream))
+    if check:
+        _check("hsa_forward_noalloc", st)
     return st
 
 

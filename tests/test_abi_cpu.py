@@ -287,3 +287,23 @@ def test_attention_planner_fits_its_chunk_table():
     cfg = P.config(1, 4, 128, 1560, "bf16")
     bad = (ctypes.c_int32 * 4)(3, 0, 3, 3)
     assert lib.hsa_attention_plan(ctypes.byref(cfg), 100, bad, 0, None, None, None) == 1
+
+
+def test_noalloc_rejects_calls_beyond_its_static_workspace():
+    # host-side: the size check comes before any device call, so fake
+    # non-NULL pointers are enough
+    lib = P.lib()
+    kh = (ctypes.c_int32 * 12)(*([16] * 12))
+    small = P.config(1, 12, 128, 1560, "bf16")
+    need = lib.hsa_forward_noalloc_bytes(ctypes.byref(small), 4680, 120, 3, kh, 16)
+    assert 0 < need <= (128 << 20)
+    big = P.config(8, 12, 128, 1560, "bf16")     # 8 x 60,000 queries: 184 MB of query sums
+    need_big = lib.hsa_forward_noalloc_bytes(ctypes.byref(big), 60000, 120, 3, kh, 16)
+    assert need_big > (128 << 20)
+    pool = H.HsaKvPool(0x1000, 0x2000, 0x3000, 8 * 123, 123)
+    st = lib.hsa_forward_noalloc(ctypes.byref(big), 0x4000, 60000, ctypes.byref(pool), 120, 3, kh, 16,
+                                 0x5000, 0x6000, 0x7000, None, None, 0x8000, None, None)
+    assert st == 4  # HSA_ERR_WORKSPACE
+    st = lib.hsa_forward_noalloc(ctypes.byref(small), None, 4680, ctypes.byref(pool), 120, 3, kh, 16,
+                                 0x5000, 0x6000, 0x7000, None, None, 0x8000, None, None)
+    assert st == 1  # HSA_ERR_INVALID_ARG
