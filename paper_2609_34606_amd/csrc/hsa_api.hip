@@ -160,22 +160,24 @@ size_t sel_ws_bytes(const hsa_config_t* c, int k_max) {
 // partial outputs of split key lists (bf16 kernels only)
 size_t partial_ws_bytes(const hsa_config_t* c, int n_q) {
   if (c->dtype != HSA_DTYPE_BF16) return 0;
-  return attention_partial_bytes(c->batch, c->head_dim, n_q, kPartPerHead * c->num_heads);
+  return attention_partial_bytes(c->batch, c->num_heads, c->head_dim, n_q, kPartPerHead * c->num_heads);
 }
 
 // Split partials of a planned launch: the schedule's p.sc.n_part slots (at
-// most kPartPerHead * H, what partial_ws_bytes provides for), the LSE
-// partials after the output partials.
+// most kPartPerHead * H, what partial_ws_bytes provides for), then the LSE
+// partials, then the arrival counters of the split query tiles.
 void set_partials(AttnParams& p, const hsa_config_t* c, int n_q, void* base) {
-  p.part_o = static_cast<float*>(base);
-  p.part_lse = reinterpret_cast<float*>(
-      static_cast<uint8_t*>(base) + attention_partial_o_bytes(c->batch, c->head_dim, n_q, p.sc.n_part));
+  uint8_t* b = static_cast<uint8_t*>(base);
+  const size_t o_bytes = attention_partial_o_bytes(c->batch, c->head_dim, n_q, p.sc.n_part);
+  p.part_o = reinterpret_cast<float*>(b);
+  p.part_lse = reinterpret_cast<float*>(b + o_bytes);
+  p.attn_ctr = reinterpret_cast<int32_t*>(b + o_bytes + attention_partial_lse_bytes(c->batch, n_q, p.sc.n_part));
 }
 
 // Bytes of split partials a planned launch writes.
 size_t planned_partial_bytes(const AttnParams& p, const hsa_config_t* c, int n_q) {
   if (c->dtype != HSA_DTYPE_BF16 || p.sc.n_part == 0) return 0;
-  return attention_partial_bytes(c->batch, c->head_dim, n_q, p.sc.n_part);
+  return attention_partial_bytes(c->batch, c->num_heads, c->head_dim, n_q, p.sc.n_part);
 }
 
 hsa_status_t from_hip(hipError_t e) { return e == hipSuccess ? HSA_OK : HSA_ERR_DEVICE; }

@@ -251,6 +251,78 @@ __device__ __forceinline__ void finish(const AttnParams& p, uint8_t* smem, int b
   }
 }
 
+// Split-KV merge without a launch of its own. Every split of a (b, h, query
+// tile) writes its normalised partial output and log-sum-exp (wave slot
+// cell0 + split * nq32), then counts itself in at the tile's counter; the
+// workgroup that arrives last reads all splits back and merges them in split
+// order, and returns true; the others return false. The merged sums of the
+// partials weighted by exp(lse_s - max), the reciprocal of the weight sum
+// and the merged LSE replace acc / inv_l / lse, as the epilogue expects. The
+// result does not depend on the order of arrival. Every thread of the
+// workgroup must call it.
+// The splits of a tile may run on different XCDs, whose L2 caches are not
+// coherent with each other. The partials therefore go through device-scope
+// (agent) atomic stores and loads, which write through to and read from the
+// device's point of coherence, instead of fences that would write back and
+// invalidate a whole L2: each split waits for its stores to complete before
+// it counts itself in, and the last one reads them after its count.
+template <int D>
+__device__ __forceinline__ bool last_split_merge(const AttnParams& p, size_t cell0, int split, int ns,
+                                                 size_t ctr, int lane, f32x16 (&acc)[D / 32],
+                                                 float& inv_l, float& lse, int& s_last) {
+  constexpr int NM = D / 32;
+  const size_t cstride = (size_t)p.sc.nq32;
+  // partial layout per wave slot: [accumulator register (NM x 16)][lane], so
+  // that every 4-byte access instruction covers 256 contiguous bytes
+  auto po = [&](int s) { return p.part_o + (cell0 + (size_t)s * cstride) * (NM * 16 * 64) + lane; };
+  auto pl = [&](int s) { return p.part_lse + (cell0 + (size_t)s * cstride) * 64 + lane; };
+  {
+    float* o = po(split);
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        __hip_atomic_store(o + (m * 16 + r) * 64, acc[m][r] * inv_l, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(pl(split), lse, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  wait_vmcnt<0>();  // this thread's partial has reached the point of coherence
+  __syncthreads();
+  if (threadIdx.x == 0)
+    s_last = __hip_atomic_fetch_add(p.attn_ctr + ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == ns - 1;
+  __syncthreads();
+  if (!s_last) return false;
+  auto ld = [](const float* q) { return __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); };
+  float lmax = -INFINITY;
+  for (int s = 0; s < ns; ++s) lmax = fmaxf(lmax, ld(pl(s)));
+  auto weight = [&](int s) {
+    const float ls = ld(pl(s));
+    return ls == -INFINITY ? 0.f : __expf(ls - lmax);
+  };
+  float wsum = 0.f;
+  for (int s = 0; s < ns; ++s) wsum += weight(s);
+  // one 32-dim output block at a time, each element summed over the splits
+  // in split order
+#pragma unroll
+  for (int m = 0; m < NM; ++m) {
+    acc[m] = f32x16{0};
+    for (int s = 0; s < ns; ++s) {
+      const float w = weight(s);
+      const float* o = po(s) + m * 16 * 64;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[m][r] = fmaf(w, ld(o + r * 64), acc[m][r]);
+    }
+  }
+  inv_l = wsum > 0.f ? 1.f / wsum : 0.f;
+  lse = wsum > 0.f ? lmax + __logf(wsum) : -INFINITY;
+  return true;
+}
+
+// Zeroes the arrival counters of a launch's split tiles.
+__global__ __launch_bounds__(256) void zero_counters_kernel(int32_t* ctr, int n) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < n) ctr[i] = 0;
+}
+
 // The tile-list walk (block-sparse mode): each (b, h, 128-query tile) walks
 // its own list of 64-key tiles; waves of a 64-query block that does not
 // keep a tile skip its MFMAs and softmax.
@@ -262,6 +334,7 @@ __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p
   constexpr int KK = D / 16;   // 16-wide d slices
   constexpr int NM = D / 32;   // 32-wide d blocks of the output
   __shared__ __attribute__((aligned(1024))) uint8_t smem[L::kBytes];
+  __shared__ int s_last;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
@@ -529,22 +602,13 @@ __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p
   wait_vmcnt<0>();  // the trailing re-reads
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
-  const float inv_l = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  const float lse = l_tot > 0.f ? m_run * p.sm_scale + __logf(l_tot) : -INFINITY;
+  float inv_l = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  float lse = l_tot > 0.f ? m_run * p.sm_scale + __logf(l_tot) : -INFINITY;
   if (ns > 1) {
-    // partial result of this split: normalised output and log-sum-exp, in the
-    // accumulator register layout (four registers of a lane contiguous, then
-    // lanes, then register groups: 16-byte accesses, coalesced)
-    const size_t cell = ((size_t)b * p.sc.n_part + p.sc.part_base[h] + split) * p.sc.nq32 + qtile * kW + wave;
-    f32x4* po = reinterpret_cast<f32x4*>(p.part_o + cell * (NM * 16 * 64)) + lane;
-#pragma unroll
-    for (int m = 0; m < NM; ++m)
-#pragma unroll
-      for (int g = 0; g < 4; ++g)
-        po[(m * 4 + g) * 64] = f32x4{acc[m][4 * g] * inv_l, acc[m][4 * g + 1] * inv_l,
-                                     acc[m][4 * g + 2] * inv_l, acc[m][4 * g + 3] * inv_l};
-    p.part_lse[cell * 64 + lane] = lse;
-    return;
+    const size_t cell0 = ((size_t)b * p.sc.n_part + p.sc.part_base[h]) * p.sc.nq32 + qtile * kW + wave;
+    if (!last_split_merge<D>(p, cell0, split, ns, ((size_t)b * H + h) * nqt + qtile, lane, acc,
+                             inv_l, lse, s_last))
+      return;
   }
   finish<D, 64 * kW>(p, smem, b, h, q_idx, qf, acc, inv_l, lse);
 }
@@ -571,6 +635,7 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
   constexpr int KK = D / 16;   // 16-wide d slices
   constexpr int NM = D / 32;   // 32-wide d blocks of the output
   __shared__ __attribute__((aligned(1024))) uint8_t smem[L::kBytes];
+  __shared__ int s_last;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -869,75 +934,15 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
-  const float inv_l = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  const float lse = l_tot > 0.f ? m_run * p.sm_scale + __logf(l_tot) : -INFINITY;
+  float inv_l = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  float lse = l_tot > 0.f ? m_run * p.sm_scale + __logf(l_tot) : -INFINITY;
   if (ns > 1) {
-    // partial result of this split (layout as in the tile-list walk)
-    const size_t cell = ((size_t)b * p.sc.n_part + p.sc.part_base[h] + split) * p.sc.nq32 + qtile * 8 + wave;
-    f32x4* po = reinterpret_cast<f32x4*>(p.part_o + cell * (NM * 16 * 64)) + lane;
-#pragma unroll
-    for (int m = 0; m < NM; ++m)
-#pragma unroll
-      for (int g = 0; g < 4; ++g)
-        po[(m * 4 + g) * 64] = f32x4{acc[m][4 * g] * inv_l, acc[m][4 * g + 1] * inv_l,
-                                     acc[m][4 * g + 2] * inv_l, acc[m][4 * g + 3] * inv_l};
-    p.part_lse[cell * 64 + lane] = lse;
-    return;
+    const size_t cell0 = ((size_t)b * p.sc.n_part + p.sc.part_base[h]) * p.sc.nq32 + qtile * 8 + wave;
+    if (!last_split_merge<D>(p, cell0, split, ns, ((size_t)b * H + h) * nqt + qtile, lane, acc,
+                             inv_l, lse, s_last))
+      return;
   }
   finish<D, 512>(p, smem, b, h, q_idx, qf, acc, inv_l, lse);
-}
-
-// Merge of the splits of one (head, 128 queries): weights exp(lse_s - max),
-// summed over the splits in order, then the same finish as an unsplit item.
-// Partials are kept per 32-query wave slot, so this works for attention
-// workgroups of any width.
-template <int D>
-__global__ __launch_bounds__(256, 2) void combine_bf16_kernel(AttnParams p) {
-  using L = AttnLayout<D>;
-  constexpr int KK = D / 16, NM = D / 32;
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[L::kLin];
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int l32 = lane & 31, half = lane >> 5;
-  const int b = blockIdx.y, nq32 = p.sc.nq32, cq = nq32 / 4;
-  const int ch = blockIdx.x / cq, q32 = (blockIdx.x % cq) * 4 + wave;
-  const int h = p.sc.c_head[ch], ns = p.sc.n_split[h];
-  const size_t cell0 = ((size_t)b * p.sc.n_part + p.sc.part_base[h]) * nq32 + q32;
-  const size_t cstride = (size_t)nq32;  // cells between consecutive splits
-  float lmax = -INFINITY;
-  for (int s = 0; s < ns; ++s) lmax = fmaxf(lmax, p.part_lse[(cell0 + s * cstride) * 64 + lane]);
-  f32x16 acc[NM];
-#pragma unroll
-  for (int m = 0; m < NM; ++m) acc[m] = f32x16{0};
-  float wsum = 0.f;
-  for (int s = 0; s < ns; ++s) {
-    const size_t cell = cell0 + s * cstride;
-    const float ls = p.part_lse[cell * 64 + lane];
-    const float w = ls == -INFINITY ? 0.f : __expf(ls - lmax);
-    wsum += w;
-    const f32x4* po = reinterpret_cast<const f32x4*>(p.part_o + cell * (NM * 16 * 64)) + lane;
-#pragma unroll
-    for (int m = 0; m < NM; ++m)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const f32x4 x = po[(m * 4 + g) * 64];
-        acc[m][4 * g] = fmaf(w, x.x, acc[m][4 * g]);
-        acc[m][4 * g + 1] = fmaf(w, x.y, acc[m][4 * g + 1]);
-        acc[m][4 * g + 2] = fmaf(w, x.z, acc[m][4 * g + 2]);
-        acc[m][4 * g + 3] = fmaf(w, x.w, acc[m][4 * g + 3]);
-      }
-  }
-  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-  const float lse = wsum > 0.f ? lmax + __logf(wsum) : -INFINITY;
-  const int q_idx = q32 * kWaveQ + l32;
-  u32x4 qf[KK];
-  {
-    const int q_ld = min(q_idx, p.n_q - 1);
-    const uint16_t* qrow = static_cast<const uint16_t*>(p.q) + (((size_t)b * p.n_q + q_ld) * p.H + h) * D + 8 * half;
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) qf[kk] = ld_global16(qrow + 16 * kk);
-  }
-  finish<D, 256>(p, smem, b, h, q_idx, qf, acc, inv, lse);
 }
 
 // fp32 inputs: VALU attention, 64 queries per workgroup, 4 lanes per query.
@@ -1070,18 +1075,25 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
 
 // Partials are kept per 32-query wave slot; the widest workgroup pads the
 // query count the most.
-static size_t partial_cells(int B, int n_q, int max_part) {
+static size_t partial_cells(int B, int n_q, int n_part) {
   const size_t nq32 = (size_t)((n_q + kWaveQ * kMaxWaves - 1) / (kWaveQ * kMaxWaves)) * kMaxWaves;
-  return (size_t)B * max_part * nq32;
+  return (size_t)B * n_part * nq32;
 }
 
-size_t attention_partial_o_bytes(int B, int d, int n_q, int max_part) {
-  return (partial_cells(B, n_q, max_part) * kWaveQ * d * 4 + 255) / 256 * 256;
+static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+size_t attention_partial_o_bytes(int B, int d, int n_q, int n_part) {
+  return align256(partial_cells(B, n_q, n_part) * kWaveQ * d * 4);
 }
 
-size_t attention_partial_bytes(int B, int d, int n_q, int max_part) {
-  return attention_partial_o_bytes(B, d, n_q, max_part) +
-         (partial_cells(B, n_q, max_part) * 64 * 4 + 255) / 256 * 256;
+size_t attention_partial_lse_bytes(int B, int n_q, int n_part) {
+  return align256(partial_cells(B, n_q, n_part) * 64 * 4);
+}
+
+size_t attention_partial_bytes(int B, int H, int d, int n_q, int n_part) {
+  // one counter per (b, h, query tile) of the narrowest workgroup (128 queries)
+  const size_t ctr = align256((size_t)B * H * ((n_q + 127) / 128) * 4);
+  return attention_partial_o_bytes(B, d, n_q, n_part) + attention_partial_lse_bytes(B, n_q, n_part) + ctr;
 }
 
 namespace {
@@ -1271,7 +1283,7 @@ bool plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_
     if (best_ns[h] > 1) {
       p.sc.part_base[h] = n_part;
       n_part += best_ns[h];
-      p.sc.c_head[n_chead++] = h;
+      ++n_chead;
     }
   }
   p.sc.n_part = n_part;
@@ -1300,6 +1312,12 @@ bool plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_
 
 hipError_t launch_attention(int dtype, int d, int B, const AttnParams& p, hipStream_t s) {
   if (dtype == HSA_DTYPE_BF16) {
+    if (p.sc.n_chead > 0) {
+      // arrival counters of the split tiles (a fill kernel, not a memset, so
+      // that the launch sequence can be captured into a graph)
+      const int n = B * p.H * p.sc.nqt;
+      zero_counters_kernel<<<(n + 255) / 256, 256, 0, s>>>(p.attn_ctr, n);
+    }
     const dim3 grid(8 * std::max(1, p.sc.xcd_items), B);
     const bool small = p.P < kBN, list = p.blist != nullptr;
     // tile lists (block-sparse mode) are built per 128-query tile and walked
@@ -1322,11 +1340,7 @@ hipError_t launch_attention(int dtype, int d, int B, const AttnParams& p, hipStr
         else attn_pp_kernel<64, false><<<grid, 512, 0, s>>>(p);
       }
     }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || p.sc.n_chead == 0) return e;
-    const dim3 cgrid(p.sc.n_chead * (p.sc.nq32 / 4), B);
-    if (d == 128) combine_bf16_kernel<128><<<cgrid, 256, 0, s>>>(p);
-    else combine_bf16_kernel<64><<<cgrid, 256, 0, s>>>(p);
+
   } else {
     const dim3 grid((p.n_q + 63) / 64, p.H, B);
     if (p.blist) {

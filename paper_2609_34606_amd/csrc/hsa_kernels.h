@@ -171,9 +171,8 @@ struct AttnSchedule {
   int32_t chunk_len[HSA_MAX_CHUNKS];
   int32_t xcd_chunk[9];
   int32_t xcd_items;                     // most items on one XCD
-  // combine items: n_chead heads with n_split > 1, nqt items each
+  // heads with n_split > 1 (their query tiles merge the splits at the end)
   int32_t n_chead;
-  int16_t c_head[HSA_MAX_HEADS];
 };
 
 struct AttnParams {
@@ -199,8 +198,10 @@ struct AttnParams {
   // sparse mode
   float* o_sp;              // [B, n_q, H, d]
   float* lse;               // [B, H, n_q] nullable
-  float* part_o;                         // [B, n_part, nq32, d/32 x 4 register groups, 64 lanes, 4 regs]
+  float* part_o;                         // [B, n_part, nq32, d/32 x 16 registers, 64 lanes]
   float* part_lse;                       // [B, n_part, nq32, 64 lanes]
+  int32_t* attn_ctr;                     // [B, H, nqt] arrivals of the splits of each query
+                                         // tile (zeroed by the launch)
   // block-sparse mode (blist != NULL): each (b, h, query tile) walks its own
   // list of 64-key tiles, entry {slot * H + h, (tile index << 2) | mask}; mask
   // bit w covers query block 2 * qtile + w (waves 2w, 2w + 1)
@@ -223,10 +224,11 @@ static_assert(HSA_MAX_LIST <= 32767 && 4 * HSA_MAX_HEADS <= 32767, "per-head sch
 // recent one costs a table lookup.
 bool plan_attention(AttnParams& p, int H, int d, int n_q, int P, const int* list_len,
                     int max_part, bool split, int waves);
-// Workspace bytes for max_part partial slots (any workgroup width), and
-// the offset of the LSE partials in it.
-size_t attention_partial_bytes(int B, int d, int n_q, int max_part);
-size_t attention_partial_o_bytes(int B, int d, int n_q, int max_part);
+// Workspace of split key lists for n_part partial slots (any workgroup
+// width): partial outputs, then partial LSEs, then the arrival counters.
+size_t attention_partial_bytes(int B, int H, int d, int n_q, int n_part);
+size_t attention_partial_o_bytes(int B, int d, int n_q, int n_part);
+size_t attention_partial_lse_bytes(int B, int n_q, int n_part);
 
 hipError_t launch_attention(int dtype, int d, int B, const AttnParams& p,
                             hipStream_t s);
