@@ -1188,11 +1188,10 @@ bool plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_
   const int tpp = (P + kBN - 1) / kBN;
   // Cost model (unit: one 64-key tile of one item with a full CU, i.e. two
   // 4-wave or one 8-wave workgroup): an item costs its tiles plus a fixed
-  // prologue/epilogue; splitting a
-  // head adds a combine pass whose time is dominated by writing and reading
-  // the partial outputs.
-  constexpr double kOverheadTiles = 3.0, kTileUs = 2.25;
-  constexpr double kCombineUsFixed = 8.0, kPartialBytesPerUs = 4.0e6;
+  // prologue/epilogue; an item of a split head also writes its partial
+  // output, and the last split of each query tile reads them all back and
+  // merges them.
+  constexpr double kOverheadTiles = 3.0, kTileUs = 2.25, kSplitTiles = 1.5;
   // Items of one batch entry are numbered head by head (heads in decreasing
   // split size), split-major, query tile fastest. The chunks of a (head,
   // split) group read the same pages, so each XCD should run few groups;
@@ -1216,7 +1215,8 @@ bool plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_
     for (int i = 0, it = 0; i < H; ++i) {
       const int h = order[i], base = list_len[h] / ns[h], rem = list_len[h] % ns[h];
       for (int sp = 0; sp < ns[h]; ++sp, it += nqt) {
-        const double c = (base + (sp < rem ? 1 : 0)) * (double)tpp + kOverheadTiles;
+        const double c = (base + (sp < rem ? 1 : 0)) * (double)tpp + kOverheadTiles +
+                         (ns[h] > 1 ? kSplitTiles : 0.0);
         for (int a = 0; a < nqt; a += len_c) {
           const int len = std::min(len_c, nqt - a);
           chunks.push_back({it + a, len, c * len});
@@ -1237,26 +1237,52 @@ bool plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_
       if (ns[h] > 1) n_part += ns[h];
     if (n_part > max_part) return kInfeasible;
     if (!build(ns, per_group, order, chunks)) return kInfeasible;
-    double us = deal_chunks(chunks, slots_per_xcd, xcd_of) * kTileUs * (waves / 4.0);
-    if (n_part > 0) us += kCombineUsFixed + 2.0 * n_part * nqt * (double)kBM * d * 4 / kPartialBytesPerUs;
-    return us;
+    return deal_chunks(chunks, slots_per_xcd, xcd_of) * kTileUs * (waves / 4.0);
   };
-  // Search the split (pages per split T) and the cut; a split or a finer cut
-  // has to win clearly, since both cost locality.
+  // Search. Start with every head whole; then, one key range at a time, split
+  // further the heads whose items are the longest, keeping the split counts
+  // of the best simulated launch (a split has to win clearly: it costs
+  // partial traffic). Each state tries whole (head, split) groups per XCD and
+  // groups cut into 2 or 4 chunks (finer cuts balance the XCDs better but
+  // make more XCDs fetch the same pages, so they too have to win clearly).
+  // The search stops three splits after the last improvement, or once the
+  // simulated launch is within 2% of the perfectly balanced one.
+  auto best_cut = [&](const int* ns, int& g_out) {
+    double b = kInfeasible;
+    for (int g : {1, 2, 4}) {
+      const double c = evaluate(ns, g) * (g == 1 ? 1.0 : g == 2 ? 1.01 : 1.03);
+      if (c < b) {
+        b = c;
+        g_out = g;
+      }
+    }
+    return b;
+  };
+  double total_tiles = 0.0;
+  for (int h = 0; h < H; ++h) total_tiles += (double)nqt * (list_len[h] * (double)tpp + kOverheadTiles);
+  const double bound = total_tiles / (8.0 * slots_per_xcd) * kTileUs * (waves / 4.0);
   int best_ns[HSA_MAX_HEADS], ns[HSA_MAX_HEADS];
-  for (int h = 0; h < H; ++h) best_ns[h] = 1;
-  int best_g = 2;
-  double best = evaluate(best_ns, 2);
-  for (int T : {0, 16, 12, 8, 6, 5, 4, 3, 2}) {
-    if (T > 0 && !split) break;
-    for (int h = 0; h < H; ++h) ns[h] = T > 0 ? std::max(1, (list_len[h] + T - 1) / T) : 1;
-    for (int g : {2, 4}) {
-      if (T == 0 && g == 2) continue;
-      const double c = evaluate(ns, g) * (T > 0 ? 1.03 : 1.0) * (g > 2 ? 1.02 : 1.0);
-      if (c < best) {
+  for (int h = 0; h < H; ++h) best_ns[h] = ns[h] = 1;
+  int best_g = 1, g = 1;
+  double best = best_cut(ns, best_g);
+  if (split) {
+    int misses = 0;
+    while (misses < 3 && best > 1.02 * bound) {
+      // the longest items: every head tied at the largest pages per split
+      int longest = 0;
+      for (int h = 0; h < H; ++h)
+        if (ns[h] < list_len[h]) longest = std::max(longest, (list_len[h] + ns[h] - 1) / ns[h]);
+      if (longest <= 1) break;
+      for (int h = 0; h < H; ++h)
+        if (ns[h] < list_len[h] && (list_len[h] + ns[h] - 1) / ns[h] == longest) ++ns[h];
+      const double c = best_cut(ns, g);
+      if (c < 0.99 * best) {
         best = c;
         best_g = g;
         std::copy(ns, ns + H, best_ns);
+        misses = 0;
+      } else {
+        ++misses;
       }
     }
   }
