@@ -166,6 +166,45 @@ hsa_status_t hsa_state_update(const hsa_config_t* cfg, const hsa_kv_pool_t* pool
                               size_t ws_bytes, void* stream);
 
 /*
+ * Page append (the page writer of row a1): copies the keys and values of
+ * n_pages new pages of every batch entry, token-major as a projection writes
+ * them, into their pool slots (logical pages [first_page, first_page +
+ * n_pages) through the page table) in the pool's layouts: key pages [P][d],
+ * value pages d-major [d][P]. The pool memory (pool->k, pool->v) is written.
+ * k_src, v_src: device [B, n_pages * P, H, d] of cfg->dtype, the tokens of
+ * each new page in raster order (frame, row, column). src_of: device int32
+ * [P] or NULL; stored position i of a page takes token src_of[i] of that
+ * page (entries are clamped into [0, P); a permutation is expected), NULL
+ * keeps the raster order. With the table of hsa_cube_order, every run of B
+ * stored tokens in the whole-cube prefix of a page is one cube, so the key
+ * blocks of the head-adaptive calls are cubes. Fold the pages with
+ * hsa_state_update afterwards. Errors: INVALID_ARG (NULL, bad range),
+ * OUT_OF_RANGE (range beyond max_pages), UNSUPPORTED (d, P).
+ */
+hsa_status_t hsa_page_write(const hsa_config_t* cfg, const hsa_kv_pool_t* pool, const void* k_src,
+                            const void* v_src, int32_t first_page, int32_t n_pages,
+                            const int32_t* src_of, void* stream);
+
+/*
+ * Cube order of a page of `frames` x `height` x `width` tokens (App. "Block
+ * Sparse Attention", the flattening index of (C_t, C_h, C_w) cubes; Sec. 3.3
+ * "Inter- and intra-chunk sparse granularity" uses (4, 8, 4) for retrieved
+ * history, B = 128, and (4, 4, 4) for the current chunk, B = 64). Host-only.
+ * Writes src_of[i] = raster index (t * height + h) * width + w of the token
+ * stored at position i, for i < frames * height * width (host int32 array of
+ * that length). Cubes that fit whole come first in the paper's order (cube
+ * index along t, then h, then w; tokens in (t, h, w) order inside a cube);
+ * when the cube does not divide the page (a 480p frame is 30 x 52 tokens:
+ * 30 is not a multiple of 8 or 4; a 3-frame chunk is shorter than C_t = 4)
+ * the cubes truncated along the far edges follow, in the same order. If the
+ * extents are multiples of the cube this is exactly the paper's index.
+ * Returns the number of positions covered by whole cubes (a multiple of
+ * ct * ch * cw), or -1 on invalid input (non-positive sizes, NULL).
+ */
+int32_t hsa_cube_order(int32_t frames, int32_t height, int32_t width, int32_t ct, int32_t ch,
+                       int32_t cw, int32_t* src_of);
+
+/*
  * hsa_page_select -- Stage-2 page-level retrieval (Sec. 3.2): per batch entry
  * and head h, with qbar the mean of the n_q queries of head h and kbar_p the
  * page's mean key,

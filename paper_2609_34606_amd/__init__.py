@@ -32,7 +32,9 @@ from .hsa import (  # noqa: F401
     hsa_forward,
     hsa_forward_selected,
     hsa_forward_workspace_size,
+    hsa_cube_order,
     hsa_page_select,
+    hsa_page_write,
     hsa_page_select_workspace_size,
     hsa_sparse_attn,
     hsa_sparse_attn_workspace_size,

@@ -17,7 +17,7 @@ LIBDIR = os.path.join(PKG, "lib")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(LIBDIR, "libhsa.so")
 SOURCES = ["hsa_api.hip", "hsa_state.hip", "hsa_select.hip", "hsa_blocks.hip", "hsa_linformer.hip",
-           "hsa_attn.hip", "hsa_tier.hip"]
+           "hsa_attn.hip", "hsa_tier.hip", "hsa_pages.hip"]
 ARCH = "gfx950"
 
 

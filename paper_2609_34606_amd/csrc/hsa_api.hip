@@ -530,6 +530,41 @@ hsa_status_t hsa_state_update(const hsa_config_t* cfg, const hsa_kv_pool_t* pool
   return from_hip(launch_state_update(cfg->dtype, cfg->head_dim, cfg->batch, p, r, s));
 }
 
+hsa_status_t hsa_page_write(const hsa_config_t* cfg, const hsa_kv_pool_t* pool, const void* k_src,
+                            const void* v_src, int32_t first_page, int32_t n_pages,
+                            const int32_t* src_of, void* stream) {
+  hsa_status_t st = check_cfg(cfg);
+  if (st != HSA_OK) return st;
+  if ((st = check_pool(pool)) != HSA_OK) return st;
+  if (!k_src || !v_src || first_page < 0 || n_pages < 0) return HSA_ERR_INVALID_ARG;
+  if ((long)first_page + n_pages > pool->max_pages) return HSA_ERR_OUT_OF_RANGE;
+  if (n_pages == 0) return HSA_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = validate_pages(cfg, pool, first_page, n_pages, s)) != HSA_OK) return st;
+  PageWriteParams p{};
+  // the pool is the caller's device memory; this call is the one that writes it
+  p.k = const_cast<void*>(pool->k);
+  p.v = const_cast<void*>(pool->v);
+  p.page_table = pool->page_table;
+  p.k_src = k_src;
+  p.v_src = v_src;
+  p.src_of = src_of;
+  p.H = cfg->num_heads;
+  p.P = cfg->page_size;
+  p.num_slots = pool->num_slots;
+  p.max_pages = pool->max_pages;
+  p.first_page = first_page;
+  p.n_pages = n_pages;
+  return from_hip(launch_page_write(cfg->dtype, cfg->head_dim, cfg->batch, p, s));
+}
+
+int32_t hsa_cube_order(int32_t frames, int32_t height, int32_t width, int32_t ct, int32_t ch,
+                       int32_t cw, int32_t* src_of) {
+  if (frames < 1 || height < 1 || width < 1 || ct < 1 || ch < 1 || cw < 1 || !src_of) return -1;
+  if ((long)frames * height * width > (1L << 30)) return -1;
+  return cube_order(frames, height, width, ct, ch, cw, src_of);
+}
+
 hsa_status_t hsa_page_select(const hsa_config_t* cfg, const void* q, int32_t n_q,
                              const double* page_kmean, int32_t max_pages, int32_t n_cand,
                              const int32_t* k_h, int32_t k_max, int32_t* sel, double* sel_score,

@@ -143,6 +143,24 @@ struct CompressParams {
 // entry (bf16: R in {32, 64, 128}; fp32: any R).
 hipError_t launch_compress(int dtype, int B, const CompressParams& p, hipStream_t s);
 
+// ------------------------------------------------------------ page append
+struct PageWriteParams {
+  void* k;                    // pool keys [num_slots, H, P, d]
+  void* v;                    // pool values [num_slots, H, d, P]
+  const int32_t* page_table;  // [B, max_pages]
+  const void* k_src;          // [B, n_pages * P, H, d] token-major
+  const void* v_src;          // [B, n_pages * P, H, d]
+  const int32_t* src_of;      // [P] stored position -> raster token, NULL: identity
+  int32_t H, P, num_slots, max_pages, first_page, n_pages;
+};
+
+hipError_t launch_page_write(int dtype, int d, int B, const PageWriteParams& p, hipStream_t s);
+
+// Cube order of a page of T x H x W tokens (see hsa_cube_order in hsa.h):
+// src_of[n] = raster index of the token stored at position n. Returns the
+// number of positions covered by whole cubes.
+int cube_order(int T, int H, int W, int ct, int ch, int cw, int32_t* src_of);
+
 // ------------------------------------------------------------ attention
 enum AttnMode : int32_t {
   ATTN_FINAL = 0,   // fused linear branch + gated merge, write o (dtype)

@@ -115,6 +115,10 @@ def lib():
     L.hsa_forward_noalloc.restype = ctypes.c_int
     L.hsa_forward_noalloc.argtypes = [P(HsaConfig), c_vp, c_i32, P(HsaKvPool), c_i32, c_i32, c_vp,
                                       c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp]
+    L.hsa_page_write.restype = ctypes.c_int
+    L.hsa_page_write.argtypes = [P(HsaConfig), P(HsaKvPool), c_vp, c_vp, c_i32, c_i32, c_vp, c_vp]
+    L.hsa_cube_order.restype = c_i32
+    L.hsa_cube_order.argtypes = [c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_vp]
     L.hsa_attention_plan.restype = ctypes.c_int
     L.hsa_attention_plan.argtypes = [P(HsaConfig), c_i32, c_vp, c_i32, c_vp, c_vp, c_vp]
     L.hsa_block_count.restype = c_i32
@@ -290,6 +294,40 @@ def hsa_state_update(cfg, pool, first_page, n_pages, kv_state, k_state, page_kme
     if check:
         _check("hsa_state_update", st)
     return st
+
+
+def hsa_page_write(cfg, pool, k_src, v_src, first_page, n_pages, src_of=None, stream=None,
+                   check=True) -> int:
+    """Append pages: k_src / v_src [B, n_pages * P, H, d] (raster order) into
+    the pool slots of logical pages [first_page, first_page + n_pages),
+    optionally permuted by src_of (device int32 [P], e.g. from
+    hsa_cube_order)."""
+    want = cfg.batch * n_pages * cfg.page_size * cfg.num_heads * cfg.head_dim
+    for name, t in (("k_src", k_src), ("v_src", v_src)):
+        if hasattr(t, "numel") and (t.numel() != want or str(t.dtype) != _elem_dtype(cfg)):
+            raise ValueError(f"{name} must hold {want} values of {_elem_dtype(cfg)} "
+                             f"([B, n_pages * P, H, d]), got {tuple(t.shape)} {t.dtype}")
+    if src_of is not None and hasattr(src_of, "numel"):
+        if src_of.numel() != cfg.page_size or str(src_of.dtype) != "torch.int32":
+            raise ValueError("src_of must be int32 [P]")
+    st = lib().hsa_page_write(ctypes.byref(cfg), ctypes.byref(pool), _ptr(k_src), _ptr(v_src),
+                              first_page, n_pages, _ptr(src_of), _stream(stream))
+    if check:
+        _check("hsa_page_write", st)
+    return st
+
+
+def hsa_cube_order(frames: int, height: int, width: int, cube=(4, 8, 4)):
+    """(src_of, whole): src_of[i] = raster index of the token stored at
+    position i of a page in cube order (int32 numpy array), and the number of
+    positions covered by whole cubes."""
+    n = frames * height * width
+    out = np.empty(n, np.int32)
+    whole = lib().hsa_cube_order(frames, height, width, int(cube[0]), int(cube[1]), int(cube[2]),
+                                 out.ctypes.data_as(c_vp))
+    if whole < 0:
+        raise ValueError("invalid cube order sizes")
+    return out, whole
 
 
 def hsa_page_select(cfg, q, n_q, page_kmean, max_pages, n_cand, k_h, k_max, sel,
