@@ -483,17 +483,24 @@ def bench_tier(args, wl, dev, main_layer, q, k_h, k_max, sel, n_slots=8, n_set=6
     sets = [np.arange(0, n_set, dtype=np.int32)[None], np.arange(n_set, 2 * n_set, dtype=np.int32)[None]]
     iters = max(10, args.steps)
 
-    def make(l2, l3, tmp):
-        host_k = torch.empty((l2, H, P, d), dtype=dt, pin_memory=True)
-        host_v = torch.empty((l2, H, d, P), dtype=dt, pin_memory=True)
+    def make(l2, l3, tmp, backup=False):
+        host_k = torch.empty((max(l2, 1), H, P, d), dtype=dt, pin_memory=True)
+        host_v = torch.empty((max(l2, 1), H, d, P), dtype=dt, pin_memory=True)
         tier = HsaTier(layer.cfg, layer.pool, l2, host_k, host_v, l3_dir=tmp if l3 else None,
-                       l3_slots=l3)
+                       l3_slots=l3, backup=backup)
+        t_commit = 0.0
         for p in range(npg):
             slot = tier.place(0, p)
             pool_k[slot] = dev["k_pool"][int(dev["page_table"][0, p])]
             pool_v[slot] = dev["v_pool"][int(dev["page_table"][0, p])]
+            if backup:
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                tier.commit()
+                t_commit += time.perf_counter() - t0
         tier.fetch(sets[1])
         torch.cuda.synchronize()
+        tier.commit_s = t_commit
         return tier, (host_k, host_v)
 
     def cycle(tier):
@@ -507,20 +514,37 @@ def bench_tier(args, wl, dev, main_layer, q, k_h, k_max, sel, n_slots=8, n_set=6
         moved = {k: (s1[k] - s0[k]) / iters for k in s1}
         per = moved["evictions"] + moved["fetches"]
         return {"pages_moved_per_fetch": per, "pages_to_file_per_fetch": moved["spills"],
-                "pages_from_file_per_fetch": moved["reloads"], "ms_per_fetch": round(dt_s * 1e3, 3),
+                "pages_from_file_per_fetch": moved["reloads"],
+                "file_writes_per_fetch": moved["backups"], "ms_per_fetch": round(dt_s * 1e3, 3),
                 "host_device_gbs": round(per * page_bytes / dt_s / 1e9, 1)}
 
     res = {"pool_slots": n_slots, "pages": npg, "pages_per_fetch": n_set,
            "page_bytes": page_bytes,
-           "note": "a page moved is one key block and one value block of every head"}
+           "note": "a page moved is one key block and one value block of every head; a fetch "
+                   "moves pages with one swap kernel per page (pool slot <-> pinned host "
+                   "memory, both directions at once), a prefetch with DMA copies"}
     # the link itself: one pinned copy of n_set pages' bytes each way
     hbuf = torch.empty(n_set * page_bytes, dtype=torch.uint8, pin_memory=True)
     dbuf = torch.empty(n_set * page_bytes, dtype=torch.uint8, device=cuda)
     ms_h2d = time_loop(lambda: dbuf.copy_(hbuf, non_blocking=True), iters, torch)
     ms_d2h = time_loop(lambda: hbuf.copy_(dbuf, non_blocking=True), iters, torch)
+    # both directions at once, each on its own stream
+    hbuf2 = torch.empty(n_set * page_bytes, dtype=torch.uint8, pin_memory=True)
+    dbuf2 = torch.empty_like(dbuf)
+    s_out = torch.cuda.Stream()
+
+    def both():
+        s_out.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s_out):
+            hbuf2.copy_(dbuf2, non_blocking=True)
+        dbuf.copy_(hbuf, non_blocking=True)
+        torch.cuda.current_stream().wait_stream(s_out)
+
+    ms_both = time_loop(both, iters, torch)
     res["link_gbs"] = {"h2d": round(n_set * page_bytes / ms_h2d / 1e6, 1),
-                       "d2h": round(n_set * page_bytes / ms_d2h / 1e6, 1)}
-    del hbuf, dbuf
+                       "d2h": round(n_set * page_bytes / ms_d2h / 1e6, 1),
+                       "both_directions": round(2 * n_set * page_bytes / ms_both / 1e6, 1)}
+    del hbuf, dbuf, hbuf2, dbuf2
     with tempfile.TemporaryDirectory() as tmp:
         tier, keep = make(npg - n_slots + 1, 0, tmp)
         res["host_tier"] = dict(host_slots=npg - n_slots + 1, **cycle(tier))
@@ -558,6 +582,17 @@ def bench_tier(args, wl, dev, main_layer, q, k_h, k_max, sel, n_slots=8, n_set=6
         tier, keep = make(n_l2, npg - n_slots - n_l2 + 1, tmp)
         res["file_tier"] = dict(host_slots=n_l2, file_slots=npg - n_slots - n_l2 + 1,
                                 file_dir=tmp.rsplit("/", 1)[0], **cycle(tier))
+        tier.close()
+        del keep
+        # backup mode: every page written to its own file slot by a commit
+        # right after it is placed; pages leaving the host tier then cost no
+        # file write
+        tier, keep = make(n_l2, npg, tmp, backup=True)
+        st = tier.stats()
+        res["file_backup_tier"] = dict(
+            host_slots=n_l2, file_slots=npg, pages_written=st["backups"],
+            commit_gbs=round(st["backups"] * page_bytes / tier.commit_s / 1e9, 2),
+            **cycle(tier))
         tier.close()
     return res
 

@@ -458,36 +458,53 @@ hsa_status_t hsa_forward_retrieval(const hsa_config_t* cfg, const void* q, int32
  *
  * Streams: place, fetch and the kernels that read the pool go on one
  * "compute" stream; a prefetch may go on another stream and then overlaps
- * them. Host-to-device copies run on the calling stream, device-to-host
- * copies on a stream of the tier's own (so the two directions overlap); the
- * tier orders them with events and makes the calling stream wait for its
- * own copies before returning. A move from L2 to L3 or from L3 waits on the
- * host for the copies it depends on (so that call blocks). A tier is not
+ * them. A fetch moves each page with one swap kernel on the calling stream:
+ * the page it brings in from pinned host memory and the page it displaces,
+ * which goes to the host slot the first one leaves, cross the link in both
+ * directions at once, in place. A prefetch (which overlaps compute, so
+ * takes no compute units) and place use DMA copies: host-to-device on the
+ * calling stream, device-to-host on a stream of the tier's own, the page
+ * going out taking the free host slot freed first. The tier orders all of
+ * them with events and makes the calling stream wait for its own copies
+ * before returning. A move from L2 to L3 or from L3 waits on the host for
+ * the copies it depends on (so that call blocks). A tier is not
  * thread-safe.
+ *
+ * Backup mode (l3_backup != 0): the file holds a copy of every page. Each
+ * page owns file slot i from its placement on (i-th page placed), written by
+ * the first hsa_tier_commit after the caller has written the page, or when
+ * the page leaves L1 and L2 before that; the copy stays. Pages leaving L2
+ * then cost no file write, a read from L3 keeps the file copy, and
+ * hsa_tier_drop can release every L1 and L2 copy, each page staying
+ * restorable from the file.
  */
 typedef struct hsa_tier hsa_tier_t;
 
 typedef struct hsa_tier_stats {
-  int64_t evictions;  /* pages moved L1 -> L2 */
+  int64_t evictions;  /* pages moved out of L1 (to L2, or to L3 when no L2 slot can take them) */
   int64_t fetches;    /* pages moved into L1 from L2 or L3 (prefetched ones included) */
-  int64_t spills;     /* pages moved L2 -> L3 */
+  int64_t spills;     /* pages moved to L3 from L2 (or from L1 directly) */
   int64_t reloads;    /* pages moved L3 -> L1 */
   int64_t prefetched; /* pages moved into L1 by hsa_tier_prefetch */
+  int64_t backups;    /* backup mode: pages written to their own file slot */
 } hsa_tier_stats_t;
 
 /* Creates a tier for pool (device k, v, page_table; num_slots L1 slots,
  * max_pages logical pages per batch entry) on the current device.
- * host_k, host_v: pinned host memory of l2_slots slots in the pool layout
- * ([l2_slots, H, P, d] and [l2_slots, H, d, P], cfg->dtype), owned by the
- * caller. l3_dir: a directory on the drive where the tier keeps an unnamed
- * file of l3_slots slots (gone when the tier is destroyed); l3_slots > 0
- * needs l2_slots >= 1. The tier allocates two pinned staging pages for L3
- * reads, an internal stream and its events. pool->k == NULL makes a
+ * host_k, host_v: pinned host memory (hipHostMalloc; the swap kernel reads
+ * and writes it) of l2_slots slots in the pool layout ([l2_slots, H, P, d]
+ * and [l2_slots, H, d, P], cfg->dtype), owned by the caller; INVALID_ARG if
+ * the device cannot address it. pool->k, pool->v, host_k and host_v 16-byte
+ * aligned, else UNSUPPORTED. l3_dir: a directory on the drive where the tier keeps an unnamed
+ * file of l3_slots slots (gone when the tier is destroyed); without backup
+ * mode l3_slots > 0 needs l2_slots >= 1, with it l3_slots >= 1 (l2_slots may
+ * be 0). The tier allocates two pinned staging pages for file reads and
+ * writes, an internal stream and its events. pool->k == NULL makes a
  * plan-only tier that issues no copy and touches no file (policy
  * inspection). HSA_ERR_IO if the file cannot be created. */
 hsa_status_t hsa_tier_create(const hsa_config_t* cfg, const hsa_kv_pool_t* pool, void* host_k,
                              void* host_v, int32_t l2_slots, const char* l3_dir,
-                             int32_t l3_slots, hsa_tier_t** tier);
+                             int32_t l3_slots, int32_t l3_backup, hsa_tier_t** tier);
 
 /* Waits for the tier's own copies, then frees it. Call it once the kernels
  * that read its pages have finished. */
@@ -497,8 +514,9 @@ void hsa_tier_destroy(hsa_tier_t* tier);
  * the caller on the same stream); if none is free, the least recently used
  * page moves down a tier. A tier holds at most
  * num_slots + l2_slots + l3_slots - 1 pages (num_slots without lower tiers):
- * one lower-tier slot stays free so that a fetch can always swap.
- * UNSUPPORTED beyond that. Sets the page-table entry. */
+ * one lower-tier slot stays free so that a fetch can always swap; in backup
+ * mode at most l3_slots pages. UNSUPPORTED beyond that. Sets the page-table
+ * entry. */
 hsa_status_t hsa_tier_place(hsa_tier_t* tier, int32_t b, int32_t page, int32_t* slot,
                             void* stream);
 
@@ -518,6 +536,22 @@ hsa_status_t hsa_tier_fetch(hsa_tier_t* tier, const int32_t* pages, int32_t n_pe
  * and the listed ones do not fit in the pool together. */
 hsa_status_t hsa_tier_prefetch(hsa_tier_t* tier, const int32_t* pages, int32_t n_per_batch,
                                void* stream);
+
+/* Backup mode: writes every placed page whose file copy is not written yet
+ * to its file slot, after the work already on `stream` (the caller's writes
+ * of the pages placed since the last commit). The device-to-host copy of one
+ * page overlaps the file write of the one before; the call blocks until the
+ * writes are done. INVALID_ARG for a tier without backup mode, IO if a
+ * write fails. */
+hsa_status_t hsa_tier_commit(hsa_tier_t* tier, void* stream);
+
+/* Backup mode: commits, then releases every L1 and L2 copy once the work
+ * already on `stream` is done: each page then lives in its file slot only
+ * (hsa_tier_locate gives its L3 code), its page-table entry becomes -1, and
+ * the next fetch restores it from the file. For a sequence that is paused
+ * (its pool and host slots are free for others) and resumed later.
+ * INVALID_ARG for a tier without backup mode. */
+hsa_status_t hsa_tier_drop(hsa_tier_t* tier, void* stream);
 
 /* Where a page lives: its pool slot (>= 0), -(i + 2) in L2 slot i,
  * -(l2_slots + i + 2) in L3 slot i, -1 never placed. */

@@ -33,7 +33,7 @@ class HsaConfig(ctypes.Structure):
 class HsaTierStats(ctypes.Structure):
     _fields_ = [("evictions", ctypes.c_int64), ("fetches", ctypes.c_int64),
                 ("spills", ctypes.c_int64), ("reloads", ctypes.c_int64),
-                ("prefetched", ctypes.c_int64)]
+                ("prefetched", ctypes.c_int64), ("backups", ctypes.c_int64)]
 
 
 class HsaKvPool(ctypes.Structure):
@@ -97,7 +97,7 @@ def lib():
                                         c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]
     L.hsa_tier_create.restype = ctypes.c_int
     L.hsa_tier_create.argtypes = [P(HsaConfig), P(HsaKvPool), c_vp, c_vp, c_i32, ctypes.c_char_p,
-                                  c_i32, P(c_vp)]
+                                  c_i32, c_i32, P(c_vp)]
     L.hsa_tier_destroy.restype = None
     L.hsa_tier_destroy.argtypes = [c_vp]
     L.hsa_tier_place.restype = ctypes.c_int
@@ -106,6 +106,10 @@ def lib():
     L.hsa_tier_fetch.argtypes = [c_vp, c_vp, c_i32, c_vp]
     L.hsa_tier_prefetch.restype = ctypes.c_int
     L.hsa_tier_prefetch.argtypes = [c_vp, c_vp, c_i32, c_vp]
+    L.hsa_tier_commit.restype = ctypes.c_int
+    L.hsa_tier_commit.argtypes = [c_vp, c_vp]
+    L.hsa_tier_drop.restype = ctypes.c_int
+    L.hsa_tier_drop.argtypes = [c_vp, c_vp]
     L.hsa_tier_locate.restype = c_i32
     L.hsa_tier_locate.argtypes = [c_vp, c_i32, c_i32]
     L.hsa_tier_stats.restype = None
@@ -542,18 +546,21 @@ class HsaTier:
     """Host-managed tiers of a layer's KV pool (include/hsa.h, hsa_tier_*):
     logical pages live in the pool's slots (L1), in pinned host slots (L2) or
     in slots of an unnamed file under ``l3_dir`` (L3). ``pool`` None makes a
-    plan-only tier (bookkeeping without copies)."""
+    plan-only tier (bookkeeping without copies). ``backup`` keeps a copy of
+    every page in the file (``commit`` writes new pages, ``drop`` releases
+    the pool and host copies)."""
 
     def __init__(self, cfg: HsaConfig, pool: Optional[HsaKvPool], l2_slots: int, host_k=None,
                  host_v=None, num_slots: int = 0, max_pages: int = 0, l3_dir: Optional[str] = None,
-                 l3_slots: int = 0):
+                 l3_slots: int = 0, backup: bool = False):
         if pool is None:
             pool = HsaKvPool(None, None, None, num_slots, max_pages)
         self._keep = (cfg, pool, host_k, host_v)
         h = c_vp()
         _check("hsa_tier_create", lib().hsa_tier_create(
             ctypes.byref(cfg), ctypes.byref(pool), _ptr(host_k), _ptr(host_v), l2_slots,
-            None if l3_dir is None else str(l3_dir).encode(), l3_slots, ctypes.byref(h)))
+            None if l3_dir is None else str(l3_dir).encode(), l3_slots, int(bool(backup)),
+            ctypes.byref(h)))
         self._h = h
 
     def close(self):
@@ -591,6 +598,18 @@ class HsaTier:
 
     def prefetch(self, pages, stream=None, check=True) -> int:
         return self._move("hsa_tier_prefetch", pages, stream, check)
+
+    def commit(self, stream=None, check=True) -> int:
+        st = lib().hsa_tier_commit(self._h, self._stream(stream))
+        if check:
+            _check("hsa_tier_commit", st)
+        return st
+
+    def drop(self, stream=None, check=True) -> int:
+        st = lib().hsa_tier_drop(self._h, self._stream(stream))
+        if check:
+            _check("hsa_tier_drop", st)
+        return st
 
     def locate(self, b: int, page: int) -> int:
         return lib().hsa_tier_locate(self._h, b, page)

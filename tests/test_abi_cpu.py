@@ -179,24 +179,96 @@ def test_tier_three_levels_and_prefetch_plan_only():
         t.place(0, p)
     assert t.place(0, 6, check=False)[0] == 2
     assert [t.locate(0, p) for p in range(6)] == [L3(0), L3(1), L2(0), L2(1), 0, 1]
-    assert t.stats() == dict(evictions=4, fetches=0, spills=2, reloads=0, prefetched=0)
+    assert t.stats() == dict(evictions=4, fetches=0, spills=2, reloads=0, prefetched=0, backups=0)
     t.fetch([[0]])                 # p0: L3 -> L1; p4 -> L2; p2 -> L3 (the freed slot)
     assert [t.locate(0, p) for p in range(6)] == [0, L3(1), L3(0), L2(1), L2(0), 1]
     # a prefetch leaves the fetched page where it is and moves the other
     t.prefetch([[1]])
     assert [t.locate(0, p) for p in range(6)] == [0, 1, L3(0), L3(1), L2(0), L2(1)]
-    assert t.stats() == dict(evictions=6, fetches=2, spills=4, reloads=2, prefetched=1)
+    assert t.stats() == dict(evictions=6, fetches=2, spills=4, reloads=2, prefetched=1, backups=0)
     # the fetched page plus two more do not fit in two slots
     assert t.prefetch([[2, 3]], check=False) == 2
     # a fetch may move anything it does not list
     t.fetch([[2, 3]])
     assert [t.locate(0, p) for p in range(6)] == [L2(0), L2(1), 0, 1, L3(0), L3(1)]
-    assert t.stats() == dict(evictions=8, fetches=4, spills=6, reloads=4, prefetched=1)
-    # both listed pages wait in L2, so no L2 page can make room: the pool's
-    # least recently used page goes straight to the free file slot
+    assert t.stats() == dict(evictions=8, fetches=4, spills=6, reloads=4, prefetched=1, backups=0)
+    # a fetch swaps: each page it brings from L2 trades places with the page
+    # it displaces, which takes its host slot
     t.fetch([[0, 1]])
-    assert [t.locate(0, p) for p in range(6)] == [0, 1, L3(2), L2(0), L3(0), L3(1)]
-    assert t.stats() == dict(evictions=10, fetches=6, spills=7, reloads=4, prefetched=1)
+    assert [t.locate(0, p) for p in range(6)] == [0, 1, L2(0), L2(1), L3(0), L3(1)]
+    assert t.stats() == dict(evictions=10, fetches=6, spills=6, reloads=4, prefetched=1, backups=0)
+    t.close()
+    # one host slot, holding a page the fetch lists: the pool's least
+    # recently used page goes straight to a free file slot
+    t = P.HsaTier(cfg, None, 1, num_slots=2, max_pages=10, l3_slots=3)
+    L3 = lambda i: -(2 + 1 + i)
+    for p in range(5):
+        t.place(0, p)
+    assert [t.locate(0, p) for p in range(5)] == [L3(0), L3(1), L2(0), 1, 0]
+    t.fetch([[0, 2]])
+    assert [t.locate(0, p) for p in range(5)] == [1, L3(1), 0, L3(0), L2(0)]
+    assert t.stats() == dict(evictions=5, fetches=2, spills=3, reloads=1, prefetched=0, backups=0)
+    t.close()
+
+
+def test_tier_backup_plan_only():
+    # backup mode: 2 pool slots, 1 host slot, 5 file slots, one per page
+    cfg = P.config(1, 2, 64, 256, "bf16")
+    with pytest.raises(P.HsaError):
+        P.HsaTier(cfg, None, 1, num_slots=2, max_pages=10, backup=True)   # needs file slots
+    t = P.HsaTier(cfg, None, 1, num_slots=2, max_pages=10, l3_slots=5, backup=True)
+    L2 = lambda i: -(i + 2)
+    L3 = lambda i: -(2 + 1 + i)
+    for p in range(5):
+        t.place(0, p)
+    assert t.place(0, 5, check=False)[0] == 2           # one file slot per page
+    # p0 and p1 left L2 before any commit: written to their own slots then
+    assert [t.locate(0, p) for p in range(5)] == [L3(0), L3(1), L2(0), 1, 0]
+    assert t.stats() == dict(evictions=3, fetches=0, spills=2, reloads=0, prefetched=0, backups=2)
+    t.commit()                          # the other three: p2 from L2, p3 and p4 from the pool
+    assert t.stats()["backups"] == 5
+    t.commit()                          # nothing left to write
+    assert t.stats()["backups"] == 5
+    # p0 back from its file slot (the copy stays there); p3 -> L2, and p2
+    # leaves L2 for its own file slot without a write
+    t.fetch([[0]])
+    assert [t.locate(0, p) for p in range(5)] == [1, L3(1), L3(2), L2(0), 0]
+    assert t.stats() == dict(evictions=4, fetches=1, spills=3, reloads=1, prefetched=0, backups=5)
+    # drop every pool and host copy: each page in its own file slot only
+    t.drop()
+    assert [t.locate(0, p) for p in range(5)] == [L3(p) for p in range(5)]
+    t.fetch([[3, 4]])                   # both restored from the file
+    assert t.locate(0, 3) >= 0 and t.locate(0, 4) >= 0
+    assert t.stats() == dict(evictions=4, fetches=3, spills=3, reloads=3, prefetched=0, backups=5)
+    # without a host tier the pool's page goes straight to its file slot
+    t2 = P.HsaTier(cfg, None, 0, num_slots=2, max_pages=10, l3_slots=3, backup=True)
+    t2.place(0, 0), t2.place(0, 1), t2.place(0, 2)
+    assert t2.locate(0, 0) == -2 and t2.stats()["backups"] == 1 and t2.stats()["spills"] == 1
+    t2.fetch([[0, 2]])                  # p1 leaves for its slot, p0 comes back
+    assert t2.locate(0, 1) == -3 and t2.stats()["backups"] == 2 and t2.stats()["reloads"] == 1
+    # commit and drop need backup mode
+    t3 = P.HsaTier(cfg, None, 2, num_slots=2, max_pages=10)
+    assert t3.commit(check=False) == 1 and t3.drop(check=False) == 1
+    t.close(), t2.close(), t3.close()
+
+
+def test_tier_fetch_swaps_and_prefetch_reuses_the_slot_freed_first_plan_only():
+    # a fetch swaps the page it brings from L2 with the page it displaces (one
+    # host slot, in place); a prefetch copies the displaced page to the free
+    # host slot freed longest ago, not the one its incoming page just left
+    cfg = P.config(1, 2, 64, 256, "bf16")
+    t = P.HsaTier(cfg, None, 4, num_slots=2, max_pages=10)
+    for p in range(4):
+        t.place(0, p)                   # p0 -> host 0, p1 -> host 1
+    assert t.locate(0, 0) == -2 and t.locate(0, 1) == -3
+    t.fetch([[0]])                      # p0 <-> p2: p2 takes host 0
+    assert t.locate(0, 0) >= 0 and t.locate(0, 2) == -2
+    t.prefetch([[1]])                   # p3 -> host 2 (free, never used); host 1 freed
+    assert t.locate(0, 3) == -4
+    t.prefetch([[2]])                   # p1 -> host 3 (never used), not host 1; host 0 freed
+    assert t.locate(0, 1) == -5
+    t.prefetch([[3]])                   # p2 -> host 1 (freed before host 0)
+    assert t.locate(0, 2) == -3
     t.close()
 
 
