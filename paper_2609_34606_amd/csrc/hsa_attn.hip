@@ -269,7 +269,7 @@ __device__ __forceinline__ void finish(const AttnParams& p, uint8_t* smem, int b
 template <int D>
 __device__ __forceinline__ bool last_split_merge(const AttnParams& p, size_t cell0, int split, int ns,
                                                  size_t ctr, int lane, f32x16 (&acc)[D / 32],
-                                                 float& inv_l, float& lse, int& s_last) {
+                                                 float& inv_l, float& lse, uint8_t* smem) {
   constexpr int NM = D / 32;
   const size_t cstride = (size_t)p.sc.nq32;
   // partial layout per wave slot: [accumulator register (NM x 16)][lane], so
@@ -286,11 +286,15 @@ __device__ __forceinline__ bool last_split_merge(const AttnParams& p, size_t cel
     __hip_atomic_store(pl(split), lse, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   wait_vmcnt<0>();  // this thread's partial has reached the point of coherence
+  // the walk's LDS is free once every wave is here: its first word carries
+  // the arrival verdict (a separate shared variable would push the 80 KB
+  // tile-list kernel past two workgroups per CU)
   __syncthreads();
+  int* s_last = reinterpret_cast<int*>(smem);
   if (threadIdx.x == 0)
-    s_last = __hip_atomic_fetch_add(p.attn_ctr + ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == ns - 1;
+    *s_last = __hip_atomic_fetch_add(p.attn_ctr + ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == ns - 1;
   __syncthreads();
-  if (!s_last) return false;
+  if (!*s_last) return false;
   auto ld = [](const float* q) { return __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); };
   float lmax = -INFINITY;
   for (int s = 0; s < ns; ++s) lmax = fmaxf(lmax, ld(pl(s)));
@@ -330,11 +334,13 @@ template <int D, bool kSmallP, int kW>
 __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p) {
   static_assert(kW == 4, "tile lists mark two 64-query blocks per workgroup");
   using L = AttnLayout<D, kW>;
+  // the kernel's only LDS: two workgroups per CU (160 KB) must fit, or the
+  // compiler targets one wave per SIMD and spreads into the AGPRs
+  static_assert(2 * L::kBytes <= 160 * 1024, "two tile-list workgroups per CU");
   constexpr int kBM = kWaveQ * kW;
   constexpr int KK = D / 16;   // 16-wide d slices
   constexpr int NM = D / 32;   // 32-wide d blocks of the output
   __shared__ __attribute__((aligned(1024))) uint8_t smem[L::kBytes];
-  __shared__ int s_last;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
@@ -607,7 +613,7 @@ __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p
   if (ns > 1) {
     const size_t cell0 = ((size_t)b * p.sc.n_part + p.sc.part_base[h]) * p.sc.nq32 + qtile * kW + wave;
     if (!last_split_merge<D>(p, cell0, split, ns, ((size_t)b * H + h) * nqt + qtile, lane, acc,
-                             inv_l, lse, s_last))
+                             inv_l, lse, smem))
       return;
   }
   finish<D, 64 * kW>(p, smem, b, h, q_idx, qf, acc, inv_l, lse);
@@ -635,7 +641,6 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
   constexpr int KK = D / 16;   // 16-wide d slices
   constexpr int NM = D / 32;   // 32-wide d blocks of the output
   __shared__ __attribute__((aligned(1024))) uint8_t smem[L::kBytes];
-  __shared__ int s_last;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -939,7 +944,7 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
   if (ns > 1) {
     const size_t cell0 = ((size_t)b * p.sc.n_part + p.sc.part_base[h]) * p.sc.nq32 + qtile * 8 + wave;
     if (!last_split_merge<D>(p, cell0, split, ns, ((size_t)b * H + h) * nqt + qtile, lane, acc,
-                             inv_l, lse, s_last))
+                             inv_l, lse, smem))
       return;
   }
   finish<D, 512>(p, smem, b, h, q_idx, qf, acc, inv_l, lse);
