@@ -70,9 +70,10 @@ def time_loop(fn, iters, torch):
     return s.elapsed_time(e) / iters
 
 
-def time_each(fn, iters, torch):
+def time_each(fn, iters, torch, keep=False):
     """Per-call ms of fn: one event pair around each call, on torch's current
-    stream (the stream the library launches on). Returns the sorted times."""
+    stream (the stream the library launches on). Returns the sorted times
+    (and, with keep, the event pairs in call order)."""
     import numpy as np
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(iters)]
@@ -82,7 +83,8 @@ def time_each(fn, iters, torch):
         fn()
         b.record()
     torch.cuda.synchronize()
-    return np.sort(np.array([a.elapsed_time(b) for a, b in evs]))
+    t = np.sort(np.array([a.elapsed_time(b) for a, b in evs]))
+    return (t, evs) if keep else t
 
 
 def time_med(fn, iters, torch):
@@ -189,8 +191,17 @@ def bench_core(args, wl, dev=None):
     out = torch.empty_like(q)
     sel = torch.empty((wl.batch, wl.heads, k_max), dtype=torch.int32, device=q.device)
 
-    def step():
+    # one event between the fold and the forward of each step, so that the
+    # step's two parts are also timed where they run (the fold right after
+    # the previous step's attention launch)
+    mids = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    k_step = [0]
+
+    def step(mark=False):
         layer.fold(0, n_pages)
+        if mark:
+            mids[k_step[0]].record()
+            k_step[0] += 1
         layer.forward(q, wl.n_cand, wl.n_cur, k_h, k_max=k_max, out=out)
 
     for _ in range(args.warmup):
@@ -199,8 +210,10 @@ def bench_core(args, wl, dev=None):
     # each step bracketed by its own event pair
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    t_step = time_each(step, args.steps, torch)
+    t_step, step_evs = time_each(lambda: step(True), args.steps, torch, keep=True)
     wall_ms = (time.perf_counter() - t0) * 1e3
+    t_fold_in = np.array([a.elapsed_time(m) for (a, _), m in zip(step_evs, mids)])
+    t_fwd_in = np.array([m.elapsed_time(b) for (_, b), m in zip(step_evs, mids)])
     log(f"{wl.name}: step median {np.median(t_step):.4f} ms")
     n = args.steps
     t_state = time_each(lambda: layer.fold(0, n_pages), n, torch)
@@ -233,12 +246,17 @@ def bench_core(args, wl, dev=None):
                    "head_dim": wl.head_dim, "n_q": n_q, "page_size": wl.page_size,
                    "history_pages": wl.n_cand, "current_pages": wl.n_cur, "k_h": k_h,
                    "state": "cold (all pages folded every step)", "parallelism": "single GPU"},
+        "step_parts_ms": {"state_update_cold": stats(t_fold_in), "forward": stats(t_fwd_in),
+                          "note": "the two parts of the timed steps (an event between them); "
+                                  "phases_ms times each part alone, back to back"},
         "phases_ms": {"state_update_cold": stats(t_state),
                       "state_update_warm_current_pages": stats(t_warm),
                       "page_select": stats(t_sel), "forward": stats(t_fwd),
                       "attention_launch": stats(t_attn)},
         "state_update_hbm_gbs": round(bs / (ms_state * 1e-3) / 1e9, 1),
         "state_update_hbm_frac": round(bs / (ms_state * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "state_update_in_step_hbm_frac": round(bs / (float(np.median(t_fold_in)) * 1e-3) / 1e9
+                                               / PEAK_HBM_GBS, 4),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
                      "traffic": measured_traffic(wl.name),
