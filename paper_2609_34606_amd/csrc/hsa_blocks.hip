@@ -18,8 +18,9 @@
 //   1. block_kmean: one workgroup per (b, h, key block) sums the block's keys
 //      (exact in fp64 for bf16 keys) and writes the mean, d-major.
 //   2. pooled_rows: one workgroup per (b, h, 4 query blocks) scores the
-//      blocks, then each wave takes one query block: softmax, a bitonic sort
-//      in LDS, the Gini term and the running weight in sorted order.
+//      blocks (a thread per key block), then each of four waves takes one
+//      query block: softmax, a bitonic sort (in registers up to 1024 blocks,
+//      else in LDS), the Gini term and the running weight in sorted order.
 //   3. block_lists: one workgroup per (b, h, 128-query tile) forms the
 //      threshold from every query block's Gini term (same order in every
 //      workgroup), cuts the two prefixes of its query blocks and writes the
@@ -35,6 +36,10 @@
 
 namespace hsa {
 namespace {
+
+// threads of a pooled_rows workgroup: one key block per thread in the score
+// loop (up to 512 blocks), then one wave per query block
+constexpr int kRowsThreads = 512;
 
 template <typename T>
 __device__ __forceinline__ void load8(const T* p, double (&x)[8]);
@@ -205,11 +210,69 @@ __device__ void bitonic_sort_wave(double* rp, int32_t* ri, int n_pad, int lane) 
   }
 }
 
+// The same order for n_pad = 64 E <= 1024 entries, sorted in registers: lane
+// l holds entries l E .. l E + E - 1, so compare-exchanges at distances below
+// E stay inside a lane and the others pair lane l with lane l ^ (distance / E)
+// through cross-lane shuffles (no LDS round trip and wave barrier per stage).
+template <int E>
+__device__ void bitonic_sort_regs(double* rp, int32_t* ri, int n_pad, int lane) {
+  double w[E];
+  int id[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    w[e] = rp[lane * E + e];
+    id[e] = ri[lane * E + e];
+  }
+  for (int k = 2; k <= n_pad; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      if (j >= E) {
+        const int m = j / E;
+        const bool lower = (lane & m) == 0;  // this lane holds the lower position of each pair
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const double tw = __shfl_xor(w[e], m);
+          const int ti = __shfl_xor(id[e], m);
+          // selects, not branches: every lane takes the same path
+          const bool mine_first = (w[e] > tw) | ((w[e] == tw) & (id[e] < ti));
+          const bool desc = ((lane * E + e) & k) == 0;
+          const bool take = (desc != mine_first) == lower;
+          w[e] = take ? tw : w[e];
+          id[e] = take ? ti : id[e];
+        }
+      } else {
+#pragma unroll
+        for (int jj = 1; jj < E; jj <<= 1) {
+          if (j != jj) continue;
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            if (e & jj) continue;
+            const double wa = w[e], wb = w[e + jj];
+            const int ia = id[e], ib = id[e + jj];
+            const bool a_first = (wa > wb) | ((wa == wb) & (ia < ib));
+            const bool sw = a_first != (((lane * E + e) & k) == 0);
+            w[e] = sw ? wb : wa;
+            w[e + jj] = sw ? wa : wb;
+            id[e] = sw ? ib : ia;
+            id[e + jj] = sw ? ia : ib;
+          }
+        }
+      }
+    }
+  }
+  wave_sync();
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    rp[lane * E + e] = w[e];
+    ri[lane * E + e] = id[e];
+  }
+  wave_sync();
+}
+
 // ---------------------------------------------------------------- 2. pooled rows
-// p.rpg query blocks per workgroup (1..4, one per wave; fewer for long lists
-// so that the rows fit in LDS).
+// p.rpg query blocks per workgroup (1..4, one per wave of the first four;
+// fewer for long lists so that the rows fit in LDS).
 template <int D>
-__global__ __launch_bounds__(256) void pooled_rows_kernel(BlockSelParams p) {
+__global__ __launch_bounds__(kRowsThreads) void pooled_rows_kernel(BlockSelParams p) {
   extern __shared__ __attribute__((aligned(16))) uint8_t dsm[];
   const int rpg = p.rpg;
   double* qbar = reinterpret_cast<double*>(dsm);                   // [rpg][D]
@@ -225,7 +288,7 @@ __global__ __launch_bounds__(256) void pooled_rows_kernel(BlockSelParams p) {
 
   // query block means from the column sums of its two halves
   const int HD = p.H * D;
-  for (int x = tid; x < rpg * D; x += 256) {
+  for (int x = tid; x < rpg * D; x += kRowsThreads) {
     const int i = x / D, dd = x % D, qb = qb0 + i;
     double v = 0.0;
     if (qb < p.n_qb) {
@@ -243,13 +306,18 @@ __global__ __launch_bounds__(256) void pooled_rows_kernel(BlockSelParams p) {
   int qi[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) qi[i] = (i < rpg ? i : 0) * D;
-  for (int j = tid; j < N; j += 256) {
+  for (int j = tid; j < N; j += kRowsThreads) {
     double a[4] = {0, 0, 0, 0};
-#pragma unroll 16
-    for (int dd = 0; dd < D; ++dd) {
-      const double kv = kb[(size_t)dd * p.n_blk_max + j];
+    // 32 block-mean loads in flight before their FMAs (the sums keep the
+    // order dd = 0, 1, ...)
+    for (int d0 = 0; d0 < D; d0 += 32) {
+      double kv[32];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = fma(qbar[qi[i] + dd], kv, a[i]);
+      for (int u = 0; u < 32; ++u) kv[u] = kb[(size_t)(d0 + u) * p.n_blk_max + j];
+#pragma unroll
+      for (int u = 0; u < 32; ++u)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) a[i] = fma(qbar[qi[i] + d0 + u], kv[u], a[i]);
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -293,10 +361,14 @@ __global__ __launch_bounds__(256) void pooled_rows_kernel(BlockSelParams p) {
     for (int j = lane; j < p.kept_len; j += 64) p.pooled[row * p.kept_len + j] = j < N ? rp[j] : 0.0;
   wave_sync();
   // sort: weight descending, block id ascending
-  if (p.n_pad <= 128) bitonic_sort_wave<1>(rp, ri, p.n_pad, lane);
-  else if (p.n_pad == 256) bitonic_sort_wave<2>(rp, ri, p.n_pad, lane);
-  else if (p.n_pad == 512) bitonic_sort_wave<4>(rp, ri, p.n_pad, lane);
-  else bitonic_sort_wave<8>(rp, ri, p.n_pad, lane);
+  switch (p.n_pad) {
+    case 64: bitonic_sort_regs<1>(rp, ri, p.n_pad, lane); break;
+    case 128: bitonic_sort_regs<2>(rp, ri, p.n_pad, lane); break;
+    case 256: bitonic_sort_regs<4>(rp, ri, p.n_pad, lane); break;
+    case 512: bitonic_sort_regs<8>(rp, ri, p.n_pad, lane); break;
+    case 1024: bitonic_sort_regs<16>(rp, ri, p.n_pad, lane); break;
+    default: bitonic_sort_wave<8>(rp, ri, p.n_pad, lane);
+  }
   // Gini term: (1/N) sum over sorted positions m = pos + 1 of (N - 2m + 1) p
   double gs = 0.0;
   for (int pos = lane; pos < N; pos += 64) gs += ((double)(N - 2 * pos - 1) / (double)N) * rp[pos];
@@ -428,8 +500,8 @@ hipError_t launch_block_select(int dtype, int d, int B, const BlockSelParams& p,
   if (e != hipSuccess) return e;
   const dim3 g2((p.n_qb + p.rpg - 1) / p.rpg, p.H, B);
   const size_t lds = block_rows_lds_bytes(d, p.n_pad, p.rpg);
-  if (d == 128) pooled_rows_kernel<128><<<g2, 256, lds, s>>>(p);
-  else pooled_rows_kernel<64><<<g2, 256, lds, s>>>(p);
+  if (d == 128) pooled_rows_kernel<128><<<g2, kRowsThreads, lds, s>>>(p);
+  else pooled_rows_kernel<64><<<g2, kRowsThreads, lds, s>>>(p);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const dim3 g3(p.n_qt, p.H, B);
   block_lists_kernel<<<g3, 256, 0, s>>>(p);
