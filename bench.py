@@ -287,7 +287,9 @@ def bench_single(args, wl):
             line["retrieval"] = bench_retrieval(args, wl, layer, q, k_h, k_max)
             line["tier"] = bench_tier(args, wl, dev, layer, q, k_h, k_max, sel)
     if not args.no_cpu_baseline:
-        heads = list(range(wl.heads)) if wl.heads * wl.n_pages <= 12 * 24 else [0, 1]
+        # every head up to the c3 history (about 10 s of oracle work on 16
+        # threads), two heads of longer ones
+        heads = list(range(wl.heads)) if wl.heads * wl.n_pages <= 12 * 130 else [0, 1]
         log("timing the oracle on the host ...")
         line["cpu_baseline"] = cpu_baseline(wl, dev, k_h, heads)
     del layer, dev, sel
