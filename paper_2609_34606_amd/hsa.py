@@ -61,6 +61,11 @@ def lib():
         return _lib
     if not os.path.exists(LIB_PATH):
         raise LibraryNotBuilt(f"{LIB_PATH} missing: build it with `python -m paper_2609_34606_amd.build`")
+    # torch's HIP runtime first: the library's libamdhip64.so.7 then binds to
+    # that copy (same soname). Loaded the other way round, torch loads its own
+    # copy beside the system one, and memory and streams of one runtime are
+    # not valid in the other (the library's launches then fail).
+    import torch  # noqa: F401
     L = ctypes.CDLL(LIB_PATH)
     P = ctypes.POINTER
     L.hsa_status_string.restype = ctypes.c_char_p

@@ -137,6 +137,20 @@ def test_adaptive_entry_points_validate_before_launch():
                                         1.0, fake, None, fake, 1024, None) == 4
 
 
+def test_library_shares_torchs_hip_runtime():
+    # loading the library first (before any torch call) must not leave two
+    # HIP runtimes in the process: the binding imports torch before it
+    import subprocess
+    import sys
+    code = ("import paper_2609_34606_amd.hsa as H; H.lib(); "
+            "m = open('/proc/self/maps').read(); "
+            "print(len({l.split()[-1] for l in m.splitlines() if 'libamdhip64' in l}))")
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True,
+                         cwd=os.path.dirname(os.path.dirname(os.path.abspath(__file__))), timeout=300)
+    assert out.returncode == 0, out.stderr[-2000:]
+    assert out.stdout.strip().splitlines()[-1] == "1"
+
+
 def test_tier_policy_plan_only():
     # 4 pool slots, 6 host slots, 10 logical pages: pages leave the pool least
     # recently used first; a fetch brings listed pages back and pins them
