@@ -114,20 +114,22 @@ def _rows(n_q, k=192, seed=0):
     return np.unique(np.concatenate([r, [t for t in tail if 0 <= t < n_q]]))
 
 
-@pytest.mark.parametrize("H,n_q,P,long_k,short_k", [(17, 2560, 64, 48, 4), (32, 1200, 128, 40, 4)])
-def test_many_heads_split_schedule(H, n_q, P, long_k, short_k):
-    # More heads than the workloads have, every third with a long list: the
-    # planner splits those lists (and deals more chunks than there are
-    # heads), so the schedule table, the split merge and the per-head
-    # schedule fields are exercised beyond H = 12. Every output element is
-    # compared.
+@pytest.mark.parametrize("B,H,n_q,P,long_k,short_k", [(1, 17, 2560, 64, 48, 4), (1, 32, 1200, 128, 40, 4),
+                                                     (2, 64, 600, 64, 24, 2)])
+def test_many_heads_split_schedule(B, H, n_q, P, long_k, short_k):
+    # More heads than the workloads have (up to the 64 the library takes,
+    # with two batch entries), every third with a long list: the planner
+    # splits those lists (and deals more chunks than there are heads), so the
+    # schedule table, the split merge and the per-head schedule fields are
+    # exercised beyond H = 12. Every output element is compared.
     import ctypes
     from paper_2609_34606_amd import config, lib
     k_h = tuple(long_k if h % 3 == 0 else short_k for h in range(H))
-    wl = SMALL.replace(heads=H, n_q=n_q, page_size=P, n_cand=long_k + 4, n_cur=2, k_h=k_h, seed=61 + H)
+    wl = SMALL.replace(batch=B, heads=H, n_q=n_q, page_size=P, n_cand=long_k + 4, n_cur=2, k_h=k_h,
+                       seed=61 + H)
     lens = (ctypes.c_int32 * H)(*[k + 2 for k in k_h])
     items, chunks, widest = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
-    cfg = config(1, H, wl.head_dim, P, "bf16")
+    cfg = config(B, H, wl.head_dim, P, "bf16")
     assert lib().hsa_attention_plan(ctypes.byref(cfg), n_q, lens, 0, ctypes.byref(items),
                                     ctypes.byref(chunks), ctypes.byref(widest)) == 0
     say(f"[case] {H} heads: {items.value} work items, {chunks.value} chunks, widest split {widest.value}")
