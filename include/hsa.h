@@ -124,8 +124,12 @@ size_t hsa_adaptive_workspace_size(const hsa_config_t* cfg, int32_t n_q,
  * list_len[h] (selected pages + current pages, host array of H entries, each
  * in [1, HSA_MAX_LIST]) and n_q queries it runs the planner that
  * hsa_forward (adaptive = 0) or the tile-list walk of the adaptive calls
- * (adaptive = 1) use, and writes the number of work items (query tile x key
- * split), of chunks in the launch's schedule table (at most
+ * (adaptive = 1) use, for cfg->batch batch entries. Page walk: writes the
+ * work items of one batch entry (256-query tiles x heads), the workgroups
+ * of the launch (each walks one of that many equal ranges of the launch's
+ * 64-key tiles, at most HSA_PLAN_MAX_CHUNKS) and the most pieces the ranges
+ * cut an item into. Tile-list walk: the work items (128-query tile x key
+ * split), the chunks of the launch's schedule table (at most
  * HSA_PLAN_MAX_CHUNKS) and the largest key split of a head. Each output
  * pointer is nullable. Errors: INVALID_ARG, UNSUPPORTED (no schedule fits;
  * the attention calls then return the same). */

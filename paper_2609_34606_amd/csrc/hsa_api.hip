@@ -431,7 +431,7 @@ hsa_status_t run_sparse(const hsa_config_t* cfg, const void* q, int32_t n_q,
   int list_len[HSA_MAX_HEADS];
   for (int h = 0; h < cfg->num_heads; ++h)
     list_len[h] = std::min(k_h ? k_h[h] : k_max, pool->max_pages) + n_cur_pages;
-  if (!plan_attention(p, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
+  if (!plan_attention(p, cfg->batch, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
                       kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16, w ? 4 : kPageWaves))
     return HSA_ERR_UNSUPPORTED;
   if (cfg->dtype == HSA_DTYPE_BF16) set_partials(p, cfg, n_q, partials);
@@ -612,7 +612,7 @@ hsa_status_t hsa_attention_plan(const hsa_config_t* cfg, int32_t n_q, const int3
   for (int h = 0; h < cfg->num_heads; ++h)
     if (list_len[h] < 1 || list_len[h] > HSA_MAX_LIST) return HSA_ERR_INVALID_ARG;
   AttnParams p{};
-  if (!plan_attention(p, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
+  if (!plan_attention(p, cfg->batch, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
                       kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16,
                       adaptive ? 4 : kPageWaves))
     return HSA_ERR_UNSUPPORTED;
@@ -717,7 +717,7 @@ bool plan_attend(AttnParams& p, const hsa_config_t* cfg, int n_q, const int32_t*
                  int n_cur_pages, bool tile_lists) {
   int list_len[HSA_MAX_HEADS];
   for (int h = 0; h < cfg->num_heads; ++h) list_len[h] = std::min(k_h[h], n_cand) + n_cur_pages;
-  return plan_attention(p, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
+  return plan_attention(p, cfg->batch, cfg->num_heads, cfg->head_dim, n_q, cfg->page_size, list_len,
                         kPartPerHead * cfg->num_heads, cfg->dtype == HSA_DTYPE_BF16,
                         tile_lists ? 4 : kPageWaves);
 }

@@ -105,14 +105,15 @@ __device__ __forceinline__ float gate_w(const float* g, size_t i) {
 //   parts (~16 bits kept) and staged through LDS in two halves of its rows;
 //   o = sigmoid(g_lin) O_lin + sigmoid(g_sp) O_sp, rounded to bf16, with one
 //   gate logit per (query, head) or, with gate_elem, per (query, head, dim).
-// Every thread of the workgroup must call it (it synchronises).
+// Every thread of the workgroup must call it (it synchronises); tid is
+// threadIdx.x.
 template <int D, int NT>
 __device__ __forceinline__ void finish(const AttnParams& p, uint8_t* smem, int b, int h, int q_idx,
                                        const u32x4 (&qf)[D / 16], const f32x16 (&acc)[D / 32],
-                                       float inv_l, float lse) {
+                                       float inv_l, float lse, int tid) {
   using L = AttnLayout<D>;
   constexpr int KK = D / 16, NM = D / 32;
-  const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, half = lane >> 5;
+  const int lane = tid & 63, l32 = lane & 31, half = lane >> 5;
   const int H = p.H;
   const bool q_ok = q_idx < p.n_q;
   if (p.mode == ATTN_SPARSE) {
@@ -259,23 +260,24 @@ __device__ __forceinline__ void finish(const AttnParams& p, uint8_t* smem, int b
 // partials weighted by exp(lse_s - max), the reciprocal of the weight sum
 // and the merged LSE replace acc / inv_l / lse, as the epilogue expects. The
 // result does not depend on the order of arrival. Every thread of the
-// workgroup must call it.
+// workgroup must call it; tid is threadIdx.x.
 // The splits of a tile may run on different XCDs, whose L2 caches are not
 // coherent with each other. The partials therefore go through device-scope
 // (agent) atomic stores and loads, which write through to and read from the
 // device's point of coherence, instead of fences that would write back and
 // invalidate a whole L2: each split waits for its stores to complete before
 // it counts itself in, and the last one reads them after its count.
-template <int D>
-__device__ __forceinline__ bool last_split_merge(const AttnParams& p, size_t cell0, int split, int ns,
-                                                 size_t ctr, int lane, f32x16 (&acc)[D / 32],
+template <int D, typename CellOf>
+__device__ __forceinline__ bool last_split_merge(const AttnParams& p, CellOf cell_of, int split, int ns,
+                                                 size_t ctr, int tid, f32x16 (&acc)[D / 32],
                                                  float& inv_l, float& lse, uint8_t* smem) {
+  const int lane = tid & 63;
   constexpr int NM = D / 32;
-  const size_t cstride = (size_t)p.sc.nq32;
-  // partial layout per wave slot: [accumulator register (NM x 16)][lane], so
-  // that every 4-byte access instruction covers 256 contiguous bytes
-  auto po = [&](int s) { return p.part_o + (cell0 + (size_t)s * cstride) * (NM * 16 * 64) + lane; };
-  auto pl = [&](int s) { return p.part_lse + (cell0 + (size_t)s * cstride) * 64 + lane; };
+  // partial layout per wave slot (cell_of(s): the slot of split s):
+  // [accumulator register (NM x 16)][lane], so that every 4-byte access
+  // instruction covers 256 contiguous bytes
+  auto po = [&](int s) { return p.part_o + cell_of(s) * (NM * 16 * 64) + lane; };
+  auto pl = [&](int s) { return p.part_lse + cell_of(s) * 64 + lane; };
   {
     float* o = po(split);
 #pragma unroll
@@ -291,31 +293,53 @@ __device__ __forceinline__ bool last_split_merge(const AttnParams& p, size_t cel
   // tile-list kernel past two workgroups per CU)
   __syncthreads();
   int* s_last = reinterpret_cast<int*>(smem);
-  if (threadIdx.x == 0)
+  if (tid == 0)
     *s_last = __hip_atomic_fetch_add(p.attn_ctr + ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == ns - 1;
   __syncthreads();
   if (!*s_last) return false;
   auto ld = [](const float* q) { return __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); };
+  // the largest split LSE, four loads in flight at a time
   float lmax = -INFINITY;
-  for (int s = 0; s < ns; ++s) lmax = fmaxf(lmax, ld(pl(s)));
-  auto weight = [&](int s) {
-    const float ls = ld(pl(s));
-    return ls == -INFINITY ? 0.f : __expf(ls - lmax);
-  };
-  float wsum = 0.f;
-  for (int s = 0; s < ns; ++s) wsum += weight(s);
-  // one 32-dim output block at a time, each element summed over the splits
-  // in split order
+  for (int s0 = 0; s0 < ns; s0 += 4) {
+    float l4[4];
 #pragma unroll
-  for (int m = 0; m < NM; ++m) {
-    acc[m] = f32x16{0};
-    for (int s = 0; s < ns; ++s) {
-      const float w = weight(s);
-      const float* o = po(s) + m * 16 * 64;
+    for (int j = 0; j < 4; ++j) l4[j] = ld(pl(min(s0 + j, ns - 1)));
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[m][r] = fmaf(w, ld(o + r * 64), acc[m][r]);
-    }
+    for (int j = 0; j < 4; ++j) lmax = fmaxf(lmax, l4[j]);
   }
+  auto weight = [&](float ls) { return ls == -INFINITY ? 0.f : __expf(ls - lmax); };
+  // sum over the splits in split order of weight x partial, each split's
+  // partial and LSE loaded in one batch; this split's partial is taken from
+  // its registers, rounded as it was stored, so that the sum does not depend
+  // on which split arrives last
+  float wsum = 0.f;
+  f32x16 before[NM];
+#pragma unroll
+  for (int m = 0; m < NM; ++m) before[m] = f32x16{0};
+  auto add_split = [&](int s, f32x16 (&into)[NM]) {
+    const float ls = ld(pl(s));
+    f32x16 o[NM];
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[m][r] = ld(po(s) + (m * 16 + r) * 64);
+    const float w = weight(ls);
+    wsum += w;
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) into[m][r] = fmaf(w, o[m][r], into[m][r]);
+  };
+  for (int s = 0; s < split; ++s) add_split(s, before);
+  {
+    const float w = weight(lse);
+    wsum += w;
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[m][r] = fmaf(w, acc[m][r] * inv_l, before[m][r]);
+  }
+  for (int s = split + 1; s < ns; ++s) add_split(s, acc);
   inv_l = wsum > 0.f ? 1.f / wsum : 0.f;
   lse = wsum > 0.f ? lmax + __logf(wsum) : -INFINITY;
   return true;
@@ -612,11 +636,12 @@ __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p
   float lse = l_tot > 0.f ? m_run * p.sm_scale + __logf(l_tot) : -INFINITY;
   if (ns > 1) {
     const size_t cell0 = ((size_t)b * p.sc.n_part + p.sc.part_base[h]) * p.sc.nq32 + qtile * kW + wave;
-    if (!last_split_merge<D>(p, cell0, split, ns, ((size_t)b * H + h) * nqt + qtile, lane, acc,
-                             inv_l, lse, smem))
+    const size_t cstride = (size_t)p.sc.nq32;
+    if (!last_split_merge<D>(p, [&](int s) { return cell0 + (size_t)s * cstride; }, split, ns,
+                             ((size_t)b * H + h) * nqt + qtile, (int)threadIdx.x, acc, inv_l, lse, smem))
       return;
   }
-  finish<D, 64 * kW>(p, smem, b, h, q_idx, qf, acc, inv_l, lse);
+  finish<D, 64 * kW>(p, smem, b, h, q_idx, qf, acc, inv_l, lse, (int)threadIdx.x);
 }
 
 // Page walk of the selected pages plus the current pages: 256 queries of one
@@ -634,65 +659,114 @@ __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p
 // waves alone return a fraction of its bandwidth). Key and value tiles sit in
 // 4-slot rings (128 KB at d = 128) filled by global-to-LDS copies that every
 // wave issues for its share right after a barrier.
+//
+// Stream-K schedule: the tiles of all items of the launch (item = one
+// (b, h, 256-query tile), ordered b, h, query tile; list pages x tiles per
+// page each) are cut into sk_g equal contiguous ranges, one per workgroup,
+// consecutive ranges on one XCD. A workgroup walks the item segments of its
+// range in order; an item cut by range boundaries is finished by the last of
+// its pieces to arrive, which merges the pieces' partials in piece order.
+// A workgroup's first and last segments are the only ones that can be
+// pieces; their partials go to its two slots (first: 0, last: 1).
 template <int D, bool kSmallP>
-__global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
+__global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p_arg) {
   using L = AttnLayout<D, 8>;
   constexpr int kBM = 256;
   constexpr int KK = D / 16;   // 16-wide d slices
   constexpr int NM = D / 32;   // 32-wide d blocks of the output
   __shared__ __attribute__((aligned(1024))) uint8_t smem[L::kBytes];
+  using ArgParams = const __attribute__((address_space(4))) AttnParams;
 
-  const int tid = threadIdx.x, lane = tid & 63;
+  // workgroup blockIdx.x runs on XCD x = blockIdx.x % 8, which holds
+  // G / 8 workgroups (one more for x < G % 8); the ranges of an XCD are
+  // contiguous
+  auto range_id = [](const AttnSchedule& sc) {
+    const int G = sc.sk_g, x = (int)(blockIdx.x & 7);
+    return x * (G >> 3) + min(x, G & 7) + (int)(blockIdx.x >> 3);
+  };
+  // ranges [0, sk_rm) hold sk_q + 1 tiles, the others sk_q
+  auto range_start = [](const AttnSchedule& sc, int i) { return i * sc.sk_q + min(i, sc.sk_rm); };
+  auto range_of = [](const AttnSchedule& sc, int t) {
+    const int big = sc.sk_rm * (sc.sk_q + 1);
+    return t < big ? t / (sc.sk_q + 1) : sc.sk_rm + (t - big) / sc.sk_q;
+  };
+  int t_seg = range_start(p_arg.sc, range_id(p_arg.sc));
+  const int t_end = range_start(p_arg.sc, range_id(p_arg.sc) + 1);
+  for (; t_seg < t_end;) {
+  __syncthreads();  // the previous segment is done with the LDS
+  // The segment reads the parameters (through the kernel-argument segment)
+  // and the lane's index through values the compiler cannot see through:
+  // otherwise it hoists out of the loop the loads and offsets that only the
+  // epilogue needs and keeps them live across the walk, which has no scalar
+  // or vector registers to spare for them.
+  ArgParams* pa = (ArgParams*)__builtin_amdgcn_kernarg_segment_ptr();
+  asm volatile("" : "+s"(pa));
+  const AttnParams& p = *(const AttnParams*)pa;
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));
+  const int lane = tid & 63, l32 = lane & 31, half = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const bool first = wave < 4;  // matrix phase in even slots
-  const int l32 = lane & 31, half = lane >> 5;
   const int H = p.H, P = p.P;
   const int nqt = p.sc.nqt;
-  const int b = blockIdx.y;
-  int qtile, h, split;
-  {
-    const int w = blockIdx.x, x = w & 7;
-    int k = w >> 3, c = p.sc.xcd_chunk[x];
-    const int c_end = p.sc.xcd_chunk[x + 1];
-    while (c < c_end && k >= p.sc.chunk_len[c]) {
-      k -= p.sc.chunk_len[c];
-      ++c;
-    }
-    if (c >= c_end) return;
-    const int item = p.sc.chunk_start[c] + k;
-    int oh = 0;
-    while (oh + 1 < p.sc.n_order && p.sc.item_off[oh + 1] <= item) ++oh;
-    h = p.sc.head_order[oh];
-    const int local = item - p.sc.item_off[oh];
-    split = local / nqt;
-    qtile = local % nqt;
-  }
-  const int ns = p.sc.n_split[h];
   const int tpp = (P + kBN - 1) / kBN;
+  const int per_b = p.sc.sk_head_off[H];
+  const int b = t_seg / per_b;
+  const int tb = t_seg - b * per_b;
+  int h = 0;
+  while (h + 1 < H && p.sc.sk_head_off[h + 1] <= tb) ++h;
+  // (an empty list still takes one tile of the range: its item writes zeros)
+  const int n_tiles_item = std::max(1, (int)p.sc.list_len[h]) * tpp;
+  const int ih = tb - p.sc.sk_head_off[h];
+  const int qtile = ih / n_tiles_item;
+  const int a = ih % n_tiles_item;   // this segment: tiles [a, e) of the item
+  const int item0 = t_seg - a;
+  const int e = std::min(n_tiles_item, t_end - item0);
+  t_seg = item0 + e;
+  // Tile v of the item is key tile (v + sigma) mod n_tiles_item of its list.
+  // sigma puts the item's largest piece in step with its range: there key
+  // tile = tiles since the range start (mod the item's tiles), as for every
+  // item that a range holds whole. So the workgroups of one head walk about
+  // the same key tiles at the same time and find them in the L2 cache, where
+  // unrotated pieces would start anywhere in the list.
+  int sigma;
+  {
+    const int r0 = range_of(p.sc, item0), s1 = range_start(p.sc, r0 + 1);
+    const int n = n_tiles_item;
+    int rs = s1;  // the second piece: larger than the first, or a whole range
+    if (item0 + n <= s1 || (item0 + n <= range_start(p.sc, r0 + 2) && s1 - item0 >= item0 + n - s1))
+      rs = range_start(p.sc, r0);
+    sigma = (item0 - rs) % n;
+    if (sigma < 0) sigma += n;
+  }
 
   const int32_t* selrow = p.sel + ((size_t)b * H + h) * p.k_max;
   const int32_t* ptrow = p.page_table + (size_t)b * p.max_pages;
   int n_sel = 0;
-  while (n_sel < p.k_max) {
-    const int e = ld_const(selrow + n_sel);
-    if (e < 0 || e >= p.max_pages) break;
+  while (n_sel < p.k_max && n_sel + p.n_cur < p.sc.list_len[h]) {
+    const int e2 = ld_const(selrow + n_sel);
+    if (e2 < 0 || e2 >= p.max_pages) break;
     ++n_sel;
   }
   auto head_of = [&](int li) -> size_t {
     const int lp = li < n_sel ? ld_const(selrow + li) : p.cur_first + (li - n_sel);
     return (size_t)clampi(ld_const(ptrow + lp), 0, p.num_slots - 1) * H + h;
   };
-  int pg0 = 0, pg1;
+  // The segment's key tiles: [S, S + e - a) mod n_tiles_item, less those
+  // beyond the real list's n_real tiles (a selection row may hold fewer
+  // pages than the bound the ranges were cut from). The walk starts at k0
+  // and wraps from the real list's last tile to its first.
+  const int n_list = n_sel + p.n_cur;
+  int ntiles, k0;
   {
-    const int n_list = n_sel + p.n_cur;
-    pg1 = n_list;
-    if (ns > 1) {
-      const int len = p.sc.list_len[h], base = len / ns, rem = len % ns;
-      pg0 = min(n_list, split * base + min(split, rem));
-      pg1 = split == ns - 1 ? n_list : min(n_list, pg0 + base + (split < rem ? 1 : 0));
-    }
+    const int n = n_tiles_item, n_real = n_list * tpp, len = e - a;
+    const int S = a + sigma < n ? a + sigma : a + sigma - n;
+    const int c1 = std::max(0, std::min(S + len, n_real) - S);
+    const int c2 = S + len > n ? std::min(S + len - n, n_real) : 0;
+    ntiles = c1 + c2;
+    k0 = c1 > 0 ? S : 0;
   }
-  const int ntiles = (pg1 - pg0) * tpp;
+  const int pg0 = ntiles > 0 ? k0 / tpp : 0;
 
   const uint16_t* qb = static_cast<const uint16_t*>(p.q);
   const int q_idx = qtile * kBM + wave * kWaveQ + l32;
@@ -719,11 +793,11 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
   for (int n = 0; n < L::kInstV; ++n) v_off[n] = (uint32_t)(v_row(n) * P + v_col(n)) * 2u;
 
   auto window = [&](int t) { return kSmallP ? t * kBN : min(t * kBN, P - kBN); };
-  int kli = pg0, kt = 0, vli = pg0, vt = 0;
+  int kli = pg0, kt = ntiles > 0 ? k0 % tpp : 0, vli = pg0, vt = kt;
   const char* kbase =
-      reinterpret_cast<const char*>(kpool) + (pg0 < pg1 ? head_of(pg0) : 0) * (size_t)P * D * 2;
+      reinterpret_cast<const char*>(kpool) + (ntiles > 0 ? head_of(pg0) : 0) * (size_t)P * D * 2;
   const char* vbase =
-      reinterpret_cast<const char*>(vpool) + (pg0 < pg1 ? head_of(pg0) : 0) * (size_t)D * P * 2;
+      reinterpret_cast<const char*>(vpool) + (ntiles > 0 ? head_of(pg0) : 0) * (size_t)D * P * 2;
   auto load_k = [&](int buf, const char* src) {
     uint8_t* dst = smem + buf * L::kKTile + wave * L::kInstK * 1024;
 #pragma unroll
@@ -746,9 +820,9 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
     load_k(buf, kbase + (size_t)window(kt) * D * 2);
     if (kt + 1 < tpp) {
       ++kt;
-    } else if (kli + 1 < pg1) {
+    } else {
       kt = 0;
-      ++kli;
+      kli = kli + 1 < n_list ? kli + 1 : 0;
       kbase = reinterpret_cast<const char*>(kpool) + head_of(kli) * (size_t)P * D * 2;
     }
   };
@@ -756,9 +830,9 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
     load_v(buf, vbase + (size_t)window(vt) * 2);
     if (vt + 1 < tpp) {
       ++vt;
-    } else if (vli + 1 < pg1) {
+    } else {
       vt = 0;
-      ++vli;
+      vli = vli + 1 < n_list ? vli + 1 : 0;
       vbase = reinterpret_cast<const char*>(vpool) + head_of(vli) * (size_t)D * P * 2;
     }
   };
@@ -784,7 +858,7 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
   auto v_tile = [&](int t) { return smem + L::kVBase + ((t + 4) & 3) * L::kVTile; };
 
   f32x16 s[2];
-  int tcs = 0;  // tile within its page of the next value phase
+  int tcs = kt;  // tile within its page of the next value phase
 
   // X(t): the scores of tile t, S^T = K(t) Q^T (two chains, key halves 0 and
   // 1), key fragments read kAheadX MFMAs ahead.
@@ -891,6 +965,12 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
     issue_k(2);
     issue_v(2);
     wait_vmcnt<0>();
+    // Nothing may be left in flight on the LDS/scalar counter either: a
+    // scalar load the compiler issued early for the epilogue would make its
+    // wait-count pass assume one pending through the walk, and it then waits
+    // for all eight operand reads before the first score MFMA of every phase
+    // instead of for one.
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) asm volatile("" : "+v"(qf[kk]));
     // Slot j opens with a barrier. Waves 0-3 run X(t) in slot 2t and Y(t) in
@@ -941,13 +1021,22 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   float inv_l = l_tot > 0.f ? 1.f / l_tot : 0.f;
   float lse = l_tot > 0.f ? m_run * p.sm_scale + __logf(l_tot) : -INFINITY;
-  if (ns > 1) {
-    const size_t cell0 = ((size_t)b * p.sc.n_part + p.sc.part_base[h]) * p.sc.nq32 + qtile * 8 + wave;
-    if (!last_split_merge<D>(p, cell0, split, ns, ((size_t)b * H + h) * nqt + qtile, lane, acc,
-                             inv_l, lse, smem))
-      return;
+  const int r_first = range_of(p.sc, item0);
+  const int n_pieces = range_of(p.sc, item0 + n_tiles_item - 1) - r_first + 1;
+  if (n_pieces > 1) {
+    // piece k of the item is range r_first + k's first segment (slot 0),
+    // except for k = 0 when the item starts inside that range (its last
+    // segment, slot 1)
+    const int slot0 = item0 != range_start(p.sc, r_first) ? 1 : 0;
+    auto cell_of = [&](int k) {
+      return ((size_t)(r_first + k) * 2 + (k == 0 ? slot0 : 0)) * 8 + wave;
+    };
+    if (!last_split_merge<D>(p, cell_of, range_id(p.sc) - r_first, n_pieces, ((size_t)b * H + h) * nqt + qtile,
+                             tid, acc, inv_l, lse, smem))
+      continue;
   }
-  finish<D, 512>(p, smem, b, h, q_idx, qf, acc, inv_l, lse);
+  finish<D, 512>(p, smem, b, h, q_idx, qf, acc, inv_l, lse, tid);
+  }  // segments
 }
 
 // fp32 inputs: VALU attention, 64 queries per workgroup, 4 lanes per query.
@@ -1144,27 +1233,29 @@ double deal_chunks(const std::vector<Chunk>& chunks, int kSlotsPerXcd, std::vect
 
 // Inputs of a schedule, the key of the schedule cache.
 struct PlanKey {
-  int H, d, n_q, P, max_part, split, waves;
+  int B, H, d, n_q, P, max_part, split, waves;
   int list_len[HSA_MAX_HEADS];
   bool operator==(const PlanKey& o) const {
-    return H == o.H && d == o.d && n_q == o.n_q && P == o.P && max_part == o.max_part &&
+    return B == o.B && H == o.H && d == o.d && n_q == o.n_q && P == o.P && max_part == o.max_part &&
            split == o.split && waves == o.waves && std::equal(list_len, list_len + H, o.list_len);
   }
 };
 
 bool plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_len, int max_part,
                    bool split, int waves);
+bool plan_stream_k(AttnParams& p, int B, int H, int n_q, int P, const int* list_len, int max_part,
+                   bool split);
 
 }  // namespace
 
-bool plan_attention(AttnParams& p, int H, int d, int n_q, int P, const int* list_len, int max_part,
-                    bool split, int waves) {
+bool plan_attention(AttnParams& p, int B, int H, int d, int n_q, int P, const int* list_len,
+                    int max_part, bool split, int waves) {
   constexpr int kCache = 8;
   static std::mutex mu;
   static PlanKey keys[kCache];
   static AttnSchedule scheds[kCache];
   static int n_cached = 0, next = 0;
-  PlanKey key{H, d, n_q, P, max_part, split ? 1 : 0, waves, {}};
+  PlanKey key{B, H, d, n_q, P, max_part, split ? 1 : 0, waves, {}};
   std::copy(list_len, list_len + H, key.list_len);
   {
     std::lock_guard<std::mutex> lock(mu);
@@ -1174,7 +1265,9 @@ bool plan_attention(AttnParams& p, int H, int d, int n_q, int P, const int* list
         return true;
       }
   }
-  if (!plan_schedule(p, H, d, n_q, P, list_len, max_part, split, waves)) return false;
+  if (waves == 8 ? !plan_stream_k(p, B, H, n_q, P, list_len, max_part, split)
+                 : !plan_schedule(p, H, d, n_q, P, list_len, max_part, split, waves))
+    return false;
   std::lock_guard<std::mutex> lock(mu);
   keys[next] = key;
   scheds[next] = p.sc;
@@ -1184,6 +1277,82 @@ bool plan_attention(AttnParams& p, int H, int d, int n_q, int P, const int* list
 }
 
 namespace {
+
+// Stream-K ranges of the page walk. The launch's items (b, h, 256-query
+// tile; a head's items all cost its list's tiles) are laid end to end, tile
+// by tile, and cut into G equal ranges of consecutive tiles, one workgroup
+// each: G = 256 (one per CU) unless the launch has fewer than 16 tiles per
+// range or two ranges per item (the partial slots: each range holds at most
+// two pieces of cut items, its first and last segments). Items of equal
+// length that fill at least 7/8 of the CUs whole (one or more per range)
+// are not cut: the partial outputs, merges and second prologues of cut
+// items cost more there than the idle CUs. split = false (fp32, whose
+// kernel does not read the schedule) takes one range.
+bool plan_stream_k(AttnParams& p, int B, int H, int n_q, int P, const int* list_len, int max_part,
+                   bool split) {
+  constexpr int kMaxRanges = 256, kMinTiles = 16;
+  const int nqt = (n_q + 255) / 256, tpp = (P + kBN - 1) / kBN;
+  int64_t per_b = 0;
+  for (int h = 0; h < H; ++h) {
+    p.sc.sk_head_off[h] = (int32_t)per_b;
+    per_b += (int64_t)nqt * std::max(1, list_len[h]) * tpp;
+  }
+  const int64_t T = (int64_t)B * per_b, items = (int64_t)B * H * nqt;
+  if (T > INT32_MAX / 2) return false;  // the kernel indexes tiles in 32 bits
+  int64_t G = std::max<int64_t>(1, std::min<int64_t>({kMaxRanges, T / kMinTiles, 2 * items}));
+  bool equal = true;
+  for (int h = 1; h < H; ++h) equal = equal && std::max(1, list_len[h]) == std::max(1, list_len[0]);
+  if (equal) {
+    const int64_t k = (items + kMaxRanges - 1) / kMaxRanges;  // items per range
+    if (items % k == 0 && 8 * (items / k) >= 7 * kMaxRanges) G = items / k;
+  }
+  if (!split) G = 1;
+  // ranges [0, rm) hold q + 1 tiles, the others q
+  const int64_t q = T / G, rm = T % G;
+  auto range_of = [&](int64_t t) {
+    return (int)(t < rm * (q + 1) ? t / (q + 1) : rm + (t - rm * (q + 1)) / q);
+  };
+  // the most pieces an item of head h is cut into
+  int pieces[HSA_MAX_HEADS];
+  bool cut = false;
+  for (int h = 0; h < H; ++h) {
+    pieces[h] = 1;
+    const int64_t len = (int64_t)std::max(1, list_len[h]) * tpp;
+    for (int b = 0; b < B; ++b)
+      for (int qt = 0; qt < nqt; ++qt) {
+        const int64_t t0 = b * per_b + p.sc.sk_head_off[h] + qt * len;
+        pieces[h] = std::max(pieces[h], range_of(t0 + len - 1) - range_of(t0) + 1);
+      }
+    cut = cut || pieces[h] > 1;
+  }
+  // partial slots: two per range and wave, in units of a batch entry's
+  // 32-query wave slots (G <= 2 items keeps this within 4 per head)
+  const int nq32 = nqt * 8;
+  const int n_part = cut ? (int)((16 * G + (int64_t)B * nq32 - 1) / ((int64_t)B * nq32)) : 0;
+  if (n_part > max_part) return false;
+  p.sc.nqt = nqt;
+  p.sc.nq32 = nq32;
+  p.sc.waves = 8;
+  p.sc.n_items = H * nqt;
+  p.sc.n_order = H;
+  for (int h = 0; h < H; ++h) {
+    p.sc.head_order[h] = h;
+    p.sc.item_off[h] = h * nqt;
+    p.sc.n_split[h] = pieces[h];
+    p.sc.list_len[h] = list_len[h];
+    p.sc.part_base[h] = 0;
+  }
+  p.sc.item_off[H] = H * nqt;
+  p.sc.n_part = n_part;
+  p.sc.n_chunks = (int)G;
+  p.sc.xcd_items = (int)((G + 7) / 8);
+  p.sc.n_chead = cut ? 1 : 0;
+  p.sc.sk_g = (int)G;
+  p.sc.sk_q = (int)q;
+  p.sc.sk_rm = (int)rm;
+  p.sc.sk_head_off[H] = (int32_t)per_b;
+  return true;
+}
 
 bool plan_schedule(AttnParams& p, int H, int d, int n_q, int P, const int* list_len, int max_part,
                    bool split, int waves) {
@@ -1349,11 +1518,11 @@ hipError_t launch_attention(int dtype, int d, int B, const AttnParams& p, hipStr
       const int n = B * p.H * p.sc.nqt;
       zero_counters_kernel<<<(n + 255) / 256, 256, 0, s>>>(p.attn_ctr, n);
     }
-    const dim3 grid(8 * std::max(1, p.sc.xcd_items), B);
     const bool small = p.P < kBN, list = p.blist != nullptr;
     // tile lists (block-sparse mode) are built per 128-query tile and walked
-    // by 4-wave workgroups; the page walk takes 8-wave ones
+    // by 4-wave workgroups; the page walk takes 8-wave ones, one per range
     if (p.sc.waves != (list ? 4 : 8)) return hipErrorInvalidValue;
+    const dim3 grid = list ? dim3(8 * std::max(1, p.sc.xcd_items), B) : dim3(p.sc.sk_g);
     if (d == 128) {
       if (list) {
         if (small) attn_bf16_kernel<128, true, 4><<<grid, 256, 0, s>>>(p);

@@ -191,6 +191,14 @@ struct AttnSchedule {
   int32_t xcd_items;                     // most items on one XCD
   // heads with n_split > 1 (their query tiles merge the splits at the end)
   int32_t n_chead;
+  // Stream-K schedule of the page walk (8 waves): items (one 256-query tile
+  // of one head) are numbered b, h, query tile; each has max(1, list_len[h])
+  // x tiles-per-page 64-key tiles, head h's first one at sk_head_off[h]
+  // within a batch entry (sk_head_off[H]: tiles per entry). The launch's
+  // tiles are cut into sk_g ranges, one per workgroup: ranges [0, sk_rm) of
+  // sk_q + 1 tiles, then ranges of sk_q.
+  int32_t sk_g, sk_q, sk_rm;
+  int32_t sk_head_off[HSA_MAX_HEADS + 1];
 };
 
 struct AttnParams {
@@ -232,15 +240,17 @@ struct AttnParams {
 static_assert(sizeof(AttnParams) <= 3584, "AttnParams must leave room in the 4 KB argument segment");
 static_assert(HSA_MAX_LIST <= 32767 && 4 * HSA_MAX_HEADS <= 32767, "per-head schedule fields are int16");
 
-// Chooses the split of each head's page list and the item order for
-// list_len[h] pages per head (H heads, head dim d, n_q queries, page size P);
-// at most max_part partial slots. split = false keeps every head whole.
-// waves: 8 (256-query workgroups, one per CU) for the page walk, 4 (128
-// queries, two per CU) for tile lists. Fills p.sc and returns true; false
-// if no schedule fits the chunk table (p.sc is then not written). The last
-// few schedules are cached (thread-safe), so a call with the inputs of a
-// recent one costs a table lookup.
-bool plan_attention(AttnParams& p, int H, int d, int n_q, int P, const int* list_len,
+// Work schedule of a bf16 attention launch over B batch entries, H heads of
+// head dim d, n_q queries, page size P and list_len[h] pages per head, with
+// at most max_part partial slots per batch entry. waves = 8: the page walk's
+// stream-K ranges (256-query workgroups, one per CU; split = false keeps
+// every item in one range). waves = 4: the tile-list walk (128 queries, two
+// workgroups per CU): the split of each head's list and the item order,
+// split = false keeping every head whole. Fills p.sc and returns true; false
+// if no schedule fits (p.sc is then not written). The last few schedules are
+// cached (thread-safe), so a call with the inputs of a recent one costs a
+// table lookup.
+bool plan_attention(AttnParams& p, int B, int H, int d, int n_q, int P, const int* list_len,
                     int max_part, bool split, int waves);
 // Workspace of split key lists for n_part partial slots (any workgroup
 // width): partial outputs, then partial LSEs, then the arrival counters.

@@ -367,12 +367,149 @@ def test_attention_planner_fits_its_chunk_table():
                     assert 1 <= n_chunks.value <= 256, (H_, n_q, n_chunks.value)
                     waves = 4 if adaptive else 8
                     assert n_items.value >= H_ * -(-n_q // (32 * waves))
-                    assert 1 <= widest.value <= max(lens)
+                    # tile lists split a head's pages; the page walk's ranges
+                    # cut an item (its list's 64-key tiles) into pieces
+                    most = max(lens) * (1 if adaptive else -(-1560 // 64))
+                    assert 1 <= widest.value <= most
                     checked += 1
     assert checked > 500
     cfg = P.config(1, 4, 128, 1560, "bf16")
     bad = (ctypes.c_int32 * 4)(3, 0, 3, 3)
     assert lib.hsa_attention_plan(ctypes.byref(cfg), 100, bad, 0, None, None, None) == 1
+
+
+def _stream_k_segments(B, H, n_q, P, lens, G):
+    """The page walk's segments as its kernel derives them: the launch's
+    tiles (items b, h, 256-query tile; max(1, lens[h]) x ceil(P / 64) tiles
+    each) cut into G ranges (the first T % G of them one tile longer); yields
+    (range, item, first tile, end tile, rotation, item start)."""
+    nqt, tpp = -(-n_q // 256), -(-P // 64)
+    off = [0]
+    for h in range(H):
+        off.append(off[-1] + nqt * max(1, lens[h]) * tpp)
+    per_b = off[H]
+    T = B * per_b
+    q, rm = divmod(T, G)
+    start = lambda i: i * q + min(i, rm)
+    range_of = lambda t: t // (q + 1) if t < rm * (q + 1) else rm + (t - rm * (q + 1)) // q
+    for r in range(G):
+        t, t_end = start(r), start(r + 1)
+        while t < t_end:
+            b = t // per_b
+            tb = t - b * per_b
+            h = 0
+            while h + 1 < H and off[h + 1] <= tb:
+                h += 1
+            n = max(1, lens[h]) * tpp
+            qt, a = divmod(tb - off[h], n)
+            item0 = t - a
+            e = min(n, t_end - item0)
+            # rotation: the larger of the first two pieces (or the one piece)
+            # runs in step with its range
+            r0 = range_of(item0)
+            s1 = start(r0 + 1)
+            rs = s1
+            if item0 + n <= s1 or (item0 + n <= start(r0 + 2) and s1 - item0 >= item0 + n - s1):
+                rs = start(r0)
+            yield r, (b, h, qt), a, e, (item0 - rs) % n, item0
+            t = item0 + e
+
+
+def _walked_keys(a, e, sigma, n, n_real):
+    """Key tiles the kernel walks for the segment [a, e) of an item of n
+    tiles rotated by sigma, with n_real real tiles: its count and start as the
+    kernel computes them, then the tiles, wrapping at n_real."""
+    length = e - a
+    S = a + sigma if a + sigma < n else a + sigma - n
+    c1 = max(0, min(S + length, n_real) - S)
+    c2 = min(S + length - n, n_real) if S + length > n else 0
+    k = S if c1 > 0 else 0
+    keys = []
+    for _ in range(c1 + c2):
+        keys.append(k)
+        k = k + 1 if k + 1 < n_real else 0
+    return keys
+
+
+def test_stream_k_ranges_cover_every_tile_once():
+    # The page walk cuts the launch's tiles into the planner's ranges (one
+    # workgroup each). Every tile must be walked exactly once; an item cut
+    # into pieces must sit in consecutive ranges, only as a range's first or
+    # last segment (its partial slot 0 or 1), with no two pieces sharing a
+    # slot; the planner's widest cut must be the largest piece count. Each
+    # item's rotated, wrapping walk must visit every key tile of its real
+    # list (which may be shorter than the planned one) exactly once, and a
+    # piece that is in step with its range must walk key tile = time.
+    lib = P.lib()
+    n_items, n_chunks, widest = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    rng = __import__("numpy").random.default_rng(9)
+    cases = [(1, 12, 4680, 1560, None), (2, 64, 600, 64, None), (3, 5, 300, 96, None),
+             (1, 17, 2560, 64, None), (4, 12, 4680, 1560, None), (1, 1, 1, 64, (1,)),
+             (1, 3, 257, 64, (1, 1, 1)), (2, 7, 20000, 40, None), (1, 12, 4680, 1560, (7,) * 12),
+             (1, 12, 4680, 1560, (4, 19, 11, 5, 5, 19, 5, 11, 11, 11, 7, 11))]
+    for B, H_, n_q, page, lens in cases:
+        lens = lens or tuple(int(x) for x in rng.integers(1, 120, H_))
+        cfg = P.config(B, H_, 128, page, "bf16")
+        arr = (ctypes.c_int32 * H_)(*lens)
+        assert lib.hsa_attention_plan(ctypes.byref(cfg), n_q, arr, 0, ctypes.byref(n_items),
+                                      ctypes.byref(n_chunks), ctypes.byref(widest)) == 0
+        G = n_chunks.value
+        assert 1 <= G <= 256, G
+        if len(set(max(1, x) for x in lens)) == 1 and 224 <= B * n_items.value <= 256:
+            assert G == B * n_items.value and widest.value == 1  # whole items, none cut
+        # workgroup w runs on XCD w % 8: each XCD's ranges are contiguous and
+        # every range has one workgroup
+        xcd_ranges = {}
+        for w in range(G):
+            x = w % 8
+            xcd_ranges.setdefault(x, []).append(x * (G // 8) + min(x, G % 8) + w // 8)
+        flat = [r for x in sorted(xcd_ranges) for r in xcd_ranges[x]]
+        assert flat == list(range(G))
+        segs = list(_stream_k_segments(B, H_, n_q, page, lens, G))
+        tpp = -(-page // 64)
+        # real lists: the planned length, or fewer pages for some heads
+        real = [max(0, x - int(rng.integers(0, 3))) if h % 2 else x for h, x in enumerate(lens)]
+        range_start = {}
+        for r, _, a, _, _, item0 in segs:
+            range_start.setdefault(r, item0 + a)
+        pieces, walked, keys, in_step = {}, 0, {}, set()
+        for r, item, a, e, sigma, item0 in segs:
+            assert 0 <= a < e
+            walked += e - a
+            pieces.setdefault(item, []).append((r, a, e))
+            n = max(1, lens[item[1]]) * tpp
+            ks = _walked_keys(a, e, sigma, n, real[item[1]] * tpp)
+            keys.setdefault(item, []).extend(ks)
+            if (a + sigma) % n == (item0 + a - range_start[r]) % n:
+                in_step.add(item)
+                if real[item[1]] == lens[item[1]]:
+                    assert ks == [(item0 + v - range_start[r]) % n for v in range(a, e)]
+        assert in_step == set(pieces)  # every item has a piece in step
+        assert walked == B * n_items.value // H_ * sum(max(1, x) * tpp for x in lens)
+        assert len(pieces) == B * n_items.value
+        for item, ks in keys.items():
+            assert sorted(ks) == list(range(real[item[1]] * tpp)), item
+        first = {}
+        last = {}
+        for r, item, a, e, _, _ in segs:
+            first.setdefault(r, item)
+            last[r] = item
+        slots = set()
+        most = 1
+        for item, ps in pieces.items():
+            n = max(1, lens[item[1]]) * tpp
+            assert ps[0][1] == 0 and ps[-1][2] == n
+            assert all(x[2] == y[1] for x, y in zip(ps, ps[1:]))  # contiguous tiles
+            assert [x[0] for x in ps] == list(range(ps[0][0], ps[0][0] + len(ps)))
+            most = max(most, len(ps))
+            if len(ps) == 1:
+                continue
+            for k, (r, a, e) in enumerate(ps):
+                slot = 1 if k == 0 and a == 0 and first[r] != item else 0
+                assert (first[r] == item) if slot == 0 else (last[r] == item)
+                assert (r, slot) not in slots
+                slots.add((r, slot))
+        assert most == widest.value, (B, H_, n_q, page, most, widest.value)
 
 
 def test_noalloc_rejects_calls_beyond_its_static_workspace():
