@@ -127,8 +127,9 @@ size_t hsa_adaptive_workspace_size(const hsa_config_t* cfg, int32_t n_q,
  * (adaptive = 1) use, for cfg->batch batch entries. Page walk: writes the
  * work items of one batch entry (256-query tiles x heads), the workgroups
  * of the launch (each walks one of that many equal ranges of the launch's
- * 64-key tiles, at most HSA_PLAN_MAX_CHUNKS) and the most pieces the ranges
- * cut an item into. Tile-list walk: the work items (128-query tile x key
+ * 64-key tiles, at most HSA_PLAN_MAX_CHUNKS; launches of at least
+ * 4 x HSA_PLAN_MAX_CHUNKS items take one workgroup per whole item) and the
+ * most pieces the ranges cut an item into. Tile-list walk: the work items (128-query tile x key
  * split), the chunks of the launch's schedule table (at most
  * HSA_PLAN_MAX_CHUNKS) and the largest key split of a head. Each output
  * pointer is nullable. Errors: INVALID_ARG, UNSUPPORTED (no schedule fits;

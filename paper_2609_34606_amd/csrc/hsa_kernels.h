@@ -196,8 +196,9 @@ struct AttnSchedule {
   // x tiles-per-page 64-key tiles, head h's first one at sk_head_off[h]
   // within a batch entry (sk_head_off[H]: tiles per entry). The launch's
   // tiles are cut into sk_g ranges, one per workgroup: ranges [0, sk_rm) of
-  // sk_q + 1 tiles, then ranges of sk_q.
-  int32_t sk_g, sk_q, sk_rm;
+  // sk_q + 1 tiles, then ranges of sk_q. sk_whole = 1: range i is item i
+  // whole instead (sk_g = items; sk_q, sk_rm unused).
+  int32_t sk_g, sk_q, sk_rm, sk_whole;
   int32_t sk_head_off[HSA_MAX_HEADS + 1];
 };
 

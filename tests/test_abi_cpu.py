@@ -364,7 +364,11 @@ def test_attention_planner_fits_its_chunk_table():
                                                 ctypes.byref(n_items), ctypes.byref(n_chunks),
                                                 ctypes.byref(widest))
                     assert st == 0, (H_, n_q, lens[:3], adaptive, st)
-                    assert 1 <= n_chunks.value <= 256, (H_, n_q, n_chunks.value)
+                    if adaptive == 0 and n_items.value >= 1024:
+                        # many items: one workgroup per whole item
+                        assert n_chunks.value == n_items.value and widest.value == 1
+                    else:
+                        assert 1 <= n_chunks.value <= 256, (H_, n_q, n_chunks.value)
                     waves = 4 if adaptive else 8
                     assert n_items.value >= H_ * -(-n_q // (32 * waves))
                     # tile lists split a head's pages; the page walk's ranges
@@ -378,17 +382,26 @@ def test_attention_planner_fits_its_chunk_table():
     assert lib.hsa_attention_plan(ctypes.byref(cfg), 100, bad, 0, None, None, None) == 1
 
 
-def _stream_k_segments(B, H, n_q, P, lens, G):
+def _stream_k_segments(B, H, n_q, P, lens, G, whole=False):
     """The page walk's segments as its kernel derives them: the launch's
     tiles (items b, h, 256-query tile; max(1, lens[h]) x ceil(P / 64) tiles
-    each) cut into G ranges (the first T % G of them one tile longer); yields
-    (range, item, first tile, end tile, rotation, item start)."""
+    each) cut into G ranges (the first T % G of them one tile longer), or
+    with whole, range i = item i; yields (range, item, first tile, end tile,
+    rotation, item start)."""
     nqt, tpp = -(-n_q // 256), -(-P // 64)
     off = [0]
     for h in range(H):
         off.append(off[-1] + nqt * max(1, lens[h]) * tpp)
     per_b = off[H]
     T = B * per_b
+    if whole:
+        for i in range(B * H * nqt):
+            b, rest = divmod(i, H * nqt)
+            h, qt = divmod(rest, nqt)
+            n = max(1, lens[h]) * tpp
+            t0 = b * per_b + off[h] + qt * n
+            yield i, (b, h, qt), 0, n, 0, t0
+        return
     q, rm = divmod(T, G)
     start = lambda i: i * q + min(i, rm)
     range_of = lambda t: t // (q + 1) if t < rm * (q + 1) else rm + (t - rm * (q + 1)) // q
@@ -446,7 +459,8 @@ def test_stream_k_ranges_cover_every_tile_once():
     cases = [(1, 12, 4680, 1560, None), (2, 64, 600, 64, None), (3, 5, 300, 96, None),
              (1, 17, 2560, 64, None), (4, 12, 4680, 1560, None), (1, 1, 1, 64, (1,)),
              (1, 3, 257, 64, (1, 1, 1)), (2, 7, 20000, 40, None), (1, 12, 4680, 1560, (7,) * 12),
-             (1, 12, 4680, 1560, (4, 19, 11, 5, 5, 19, 5, 11, 11, 11, 7, 11))]
+             (1, 12, 4680, 1560, (4, 19, 11, 5, 5, 19, 5, 11, 11, 11, 7, 11)),
+             (30, 12, 4680, 1560, (11,) * 12), (5, 12, 4680, 1560, None), (4, 12, 4680, 1560, (9,) * 12)]
     for B, H_, n_q, page, lens in cases:
         lens = lens or tuple(int(x) for x in rng.integers(1, 120, H_))
         cfg = P.config(B, H_, 128, page, "bf16")
@@ -454,7 +468,11 @@ def test_stream_k_ranges_cover_every_tile_once():
         assert lib.hsa_attention_plan(ctypes.byref(cfg), n_q, arr, 0, ctypes.byref(n_items),
                                       ctypes.byref(n_chunks), ctypes.byref(widest)) == 0
         G = n_chunks.value
-        assert 1 <= G <= 256, G
+        whole = B * n_items.value >= 1024
+        if whole:  # one workgroup per whole item
+            assert G == B * n_items.value and widest.value == 1
+        else:
+            assert 1 <= G <= 256, G
         if len(set(max(1, x) for x in lens)) == 1 and 224 <= B * n_items.value <= 256:
             assert G == B * n_items.value and widest.value == 1  # whole items, none cut
         # workgroup w runs on XCD w % 8: each XCD's ranges are contiguous and
@@ -465,7 +483,7 @@ def test_stream_k_ranges_cover_every_tile_once():
             xcd_ranges.setdefault(x, []).append(x * (G // 8) + min(x, G % 8) + w // 8)
         flat = [r for x in sorted(xcd_ranges) for r in xcd_ranges[x]]
         assert flat == list(range(G))
-        segs = list(_stream_k_segments(B, H_, n_q, page, lens, G))
+        segs = list(_stream_k_segments(B, H_, n_q, page, lens, G, whole))
         tpp = -(-page // 64)
         # real lists: the planned length, or fewer pages for some heads
         real = [max(0, x - int(rng.integers(0, 3))) if h % 2 else x for h, x in enumerate(lens)]

@@ -137,6 +137,25 @@ def test_many_heads_split_schedule(B, H, n_q, P, long_k, short_k):
     _run_small(wl)
 
 
+def test_whole_item_schedule_many_items():
+    # A launch of at least 4 x 256 items (two batch entries, 64 heads, nine
+    # query tiles each) takes one workgroup per whole item; lists of unequal
+    # length (every third head long). Every output element is compared.
+    import ctypes
+    from paper_2609_34606_amd import config, lib
+    B, H, n_q, P = 2, 64, 2100, 64
+    k_h = tuple(24 if h % 3 == 0 else 2 for h in range(H))
+    wl = SMALL.replace(batch=B, heads=H, n_q=n_q, page_size=P, n_cand=28, n_cur=2, k_h=k_h, seed=77)
+    lens = (ctypes.c_int32 * H)(*[k + 2 for k in k_h])
+    items, chunks, widest = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    cfg = config(B, H, wl.head_dim, P, "bf16")
+    assert lib().hsa_attention_plan(ctypes.byref(cfg), n_q, lens, 0, ctypes.byref(items),
+                                    ctypes.byref(chunks), ctypes.byref(widest)) == 0
+    say(f"[case] whole items: {B * items.value} items, {chunks.value} workgroups")
+    assert chunks.value == B * items.value >= 1024 and widest.value == 1
+    _run_small(wl)
+
+
 def _full_size(name, rows_k=None, gate_cases=True):
     """A full-size workload through the library and the oracle. rows_k None
     compares every query row; otherwise a sample of rows_k rows plus the
