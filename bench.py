@@ -3,8 +3,11 @@
 
 A step is one pass of the whole path over one chunk of synthetic input with
 everything resident in HBM: hsa_state_update over every page of the layer
-(cold build of the linear state and page index) followed by hsa_forward
-(query summary, page selection, sparse branch, linear branch, gated merge).
+(cold build of the linear state and page index), hsa_page_select (query
+summary, page scores, top-k_h) and hsa_forward_selected (sparse branch,
+linear branch, gated merge) -- the two halves of hsa_forward, the same
+kernels, called apart so that an event between them times the attention
+launch inside every timed step.
 Default workload (``--config c3``): one layer, 12 heads x d128, 4680
 queries, 120 history pages of 1560 tokens (187,200 keys) plus the 3 current
 pages, head-adaptive budgets k_h drawn from {2, 4, 8, 16}. The other
@@ -17,8 +20,8 @@ stream the library launches on; ``value`` is the median step time over
 
 Prints one JSON line. ``value`` is milliseconds per chunk (lower is better);
 the line also carries effective TFLOP/s, per-phase times, the roofline of the
-dominant kernel (the attention launch inside hsa_forward) and the fp64 oracle
-timed on this host's cores.
+dominant kernel (the attention launch, timed inside the steps) and the fp64
+oracle timed on this host's cores.
 """
 from __future__ import annotations
 
@@ -173,9 +176,9 @@ def cpu_baseline(wl, dev, k_h, heads):
 
 
 def bench_core(args, wl, dev=None):
-    """One workload: the step (cold fold + hsa_forward) timed per step, its
-    phases, and the attention launch with its roofline. Returns (result,
-    layer, inputs, selection)."""
+    """One workload: the step (cold fold, page selection, attention) timed
+    per step and per part, the parts again back to back, and the attention
+    launch with its roofline. Returns (result, layer, inputs, selection)."""
     import torch
     from paper_2609_34606_amd import HsaLayer, hsa_page_select
     from synth_inputs import make_case_torch
@@ -191,18 +194,31 @@ def bench_core(args, wl, dev=None):
     out = torch.empty_like(q)
     sel = torch.empty((wl.batch, wl.heads, k_max), dtype=torch.int32, device=q.device)
 
-    # one event between the fold and the forward of each step, so that the
-    # step's two parts are also timed where they run (the fold right after
-    # the previous step's attention launch)
-    mids = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    # events between the fold, the page selection and the attention launch of
+    # each step, so that the step's parts are timed where they run (the fold
+    # right after the previous step's attention launch, the attention right
+    # after the selection)
+    mids = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in range(args.steps)]
     k_step = [0]
+    ws = layer.workspace("sel", 1 << 24)
+
+    def select():
+        hsa_page_select(layer.cfg, q, n_q, layer.page_kmean, layer.max_pages, wl.n_cand, k_h, k_max,
+                        sel, ws=ws)
+
+    def attend():
+        layer.forward_selected(q, sel, wl.n_cand, wl.n_cur, k_h, k_max=k_max, out=out)
 
     def step(mark=False):
         layer.fold(0, n_pages)
         if mark:
-            mids[k_step[0]].record()
+            mids[k_step[0]][0].record()
+        select()
+        if mark:
+            mids[k_step[0]][1].record()
             k_step[0] += 1
-        layer.forward(q, wl.n_cand, wl.n_cur, k_h, k_max=k_max, out=out)
+        attend()
 
     for _ in range(args.warmup):
         step()
@@ -212,21 +228,19 @@ def bench_core(args, wl, dev=None):
     t0 = time.perf_counter()
     t_step, step_evs = time_each(lambda: step(True), args.steps, torch, keep=True)
     wall_ms = (time.perf_counter() - t0) * 1e3
-    t_fold_in = np.array([a.elapsed_time(m) for (a, _), m in zip(step_evs, mids)])
-    t_fwd_in = np.array([m.elapsed_time(b) for (_, b), m in zip(step_evs, mids)])
+    t_fold_in = np.array([a.elapsed_time(m1) for (a, _), (m1, _) in zip(step_evs, mids)])
+    t_sel_in = np.array([m1.elapsed_time(m2) for (m1, m2) in mids])
+    t_attn_in = np.array([m2.elapsed_time(b) for (_, b), (_, m2) in zip(step_evs, mids)])
     log(f"{wl.name}: step median {np.median(t_step):.4f} ms")
     n = args.steps
+    # each part again, back to back (other cache and clock conditions than in
+    # the step: the attention re-reads the pages it has just read)
     t_state = time_each(lambda: layer.fold(0, n_pages), n, torch)
     t_warm = time_each(lambda: layer.fold(wl.n_cand, wl.n_cur), n, torch)
-    ws = layer.workspace("sel", 1 << 24)
-    t_sel = time_each(lambda: hsa_page_select(layer.cfg, q, n_q, layer.page_kmean, layer.max_pages,
-                                              wl.n_cand, k_h, k_max, sel, ws=ws), n, torch)
+    t_sel = time_each(select, n, torch)
     t_fwd = time_each(lambda: layer.forward(q, wl.n_cand, wl.n_cur, k_h, k_max=k_max, out=out),
                       n, torch)
-    # the attention launch alone: sparse branch + linear branch + merge for the
-    # selection just computed
-    t_attn = time_each(lambda: layer.forward_selected(q, sel, wl.n_cand, wl.n_cur, k_h, k_max=k_max,
-                                                      out=out), n, torch)
+    t_attn = time_each(attend, n, torch)
     k_eff = [min(k, wl.n_cand) for k in k_h]
     fa = attn_flops(wl, k_eff, n_q)
     fl = linear_flops(wl, n_q)
@@ -234,7 +248,7 @@ def bench_core(args, wl, dev=None):
     total = fa + fl + fs
     peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
     ms = float(np.median(t_step))
-    ms_attn_mean = float(np.mean(t_attn))
+    ms_attn_mean = float(np.mean(t_attn_in))
     achieved = fa / (ms_attn_mean * 1e-3) / 1e12
     ms_state = float(np.median(t_state))
     res = {
@@ -246,8 +260,9 @@ def bench_core(args, wl, dev=None):
                    "head_dim": wl.head_dim, "n_q": n_q, "page_size": wl.page_size,
                    "history_pages": wl.n_cand, "current_pages": wl.n_cur, "k_h": k_h,
                    "state": "cold (all pages folded every step)", "parallelism": "single GPU"},
-        "step_parts_ms": {"state_update_cold": stats(t_fold_in), "forward": stats(t_fwd_in),
-                          "note": "the two parts of the timed steps (an event between them); "
+        "step_parts_ms": {"state_update_cold": stats(t_fold_in), "page_select": stats(t_sel_in),
+                          "attention_launch": stats(t_attn_in),
+                          "note": "the three parts of the timed steps (events between them); "
                                   "phases_ms times each part alone, back to back"},
         "phases_ms": {"state_update_cold": stats(t_state),
                       "state_update_warm_current_pages": stats(t_warm),
@@ -260,10 +275,11 @@ def bench_core(args, wl, dev=None):
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
                      "traffic": measured_traffic(wl.name),
-                     "kernel": "attention launch of hsa_forward_selected (mean of per-launch "
-                               "HIP event times)",
+                     "kernel": "attention launch (hsa_forward_selected) inside the timed steps "
+                               "(mean of per-step HIP event times)",
                      "flops_per_launch": fa,
-                     "frac_at_median_launch": round(fa / (float(np.median(t_attn)) * 1e-3) / 1e12 / peak, 4)},
+                     "frac_at_median_launch": round(fa / (float(np.median(t_attn_in)) * 1e-3) / 1e12 / peak, 4),
+                     "frac_back_to_back": round(fa / (float(np.mean(t_attn)) * 1e-3) / 1e12 / peak, 4)},
     }
     return res, layer, dev, sel
 
