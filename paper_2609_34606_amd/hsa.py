@@ -175,6 +175,18 @@ def _ptr(t) -> Optional[int]:
     return int(t)
 
 
+def _out(t, n: int, dtype: str, what: str) -> Optional[int]:
+    """Pointer of an optional output of at least n elements of dtype
+    ('int32' or 'float64'), or None."""
+    if t is None:
+        return None
+    if hasattr(t, "dtype") and str(t.dtype) != f"torch.{dtype}":
+        raise ValueError(f"{what}: expected {dtype}, got {t.dtype}")
+    if hasattr(t, "numel") and t.numel() < n:
+        raise ValueError(f"{what}: {t.numel()} elements, need {n}")
+    return _ptr(t)
+
+
 def _gate(cfg, g, n_q: int) -> Optional[int]:
     """Pointer of a gate-logit tensor after checking that it holds what the
     kernels read: fp32, [B, n_q, H] or, with cfg.gate_dims = d, [B, n_q, H, d]."""
@@ -421,6 +433,7 @@ def hsa_forward_noalloc(cfg, q, n_q, pool, n_cand, n_cur_pages, k_h, k_max, kv_s
 
 # Paper's setting of the coverage thresholds (tau_max, tau_min) = (1.00, 0.35).
 TAU_MIN, TAU_MAX = 0.35, 1.00
+BLOCK_Q = 64  # queries per query block (HSA_BLOCK_Q)
 
 
 def hsa_block_select(cfg, q, n_q, pool, sel, k_max, cur_first_page, n_cur_pages,
@@ -429,11 +442,16 @@ def hsa_block_select(cfg, q, n_q, pool, sel, k_max, cur_first_page, n_cur_pages,
                      check=True) -> int:
     if ws is None:
         ws = _workspace(hsa_adaptive_workspace_size(cfg, n_q, k_max, n_cur_pages), q.device)
+    bh = cfg.batch * cfg.num_heads
+    n_qb = -(-n_q // BLOCK_Q)
     st = lib().hsa_block_select(ctypes.byref(cfg), _rows(cfg, q, n_q, "q"), n_q, ctypes.byref(pool), _ptr(sel),
                                 k_max, cur_first_page, n_cur_pages, float(tau_min),
-                                float(tau_max), _ptr(gini), _ptr(tau), _ptr(n_kept), _ptr(kept),
-                                _ptr(pooled), kept_len, _ptr(ws),
-                                0 if ws is None else ws.numel(), _stream(stream))
+                                float(tau_max), _out(gini, bh, "float64", "gini"),
+                                _out(tau, bh, "float64", "tau"),
+                                _out(n_kept, bh * n_qb, "int32", "n_kept"),
+                                _out(kept, bh * n_qb * kept_len, "int32", "kept"),
+                                _out(pooled, bh * n_qb * kept_len, "float64", "pooled"), kept_len,
+                                _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream))
     if check:
         _check("hsa_block_select", st)
     return st

@@ -325,6 +325,18 @@ def test_query_and_output_tensors_are_checked_against_the_config():
         H._rows(cfg, torch.zeros((2, 5, 3, 64), dtype=bf), 5, "o_sp", fp32=True)
 
 
+def test_block_select_outputs_are_checked_for_size_and_type():
+    import torch
+    from paper_2609_34606_amd import hsa as H
+    assert H._out(None, 10, "int32", "x") is None
+    assert H._out(torch.zeros(10, dtype=torch.int32), 10, "int32", "x") is not None
+    assert H._out(torch.zeros(12, dtype=torch.float64), 10, "float64", "x") is not None
+    for t, dt in ((torch.zeros(9, dtype=torch.int32), "int32"), (torch.zeros(10), "float64"),
+                  (torch.zeros(10, dtype=torch.int64), "int32")):
+        with pytest.raises(ValueError):
+            H._out(t, 10, dt, "x")
+
+
 def test_pool_tensors_are_checked_against_the_config():
     import torch
     from paper_2609_34606_amd import hsa as H
