@@ -119,7 +119,22 @@ def measured_traffic(workload: str, key: str = "hbm_bytes_per_launch"):
     hbm_bytes_per_launch_tile_list: the block-sparse one) from the committed
     counter summary of this workload, if it was taken on the current kernel
     sources, else None."""
-    path = os.path.join(ROOT, "profiles", f"attn_{workload}_hbm_traffic.txt")
+    v = profile_value(f"attn_{workload}_hbm_traffic.txt", key)
+    return None if v is None else int(v) or None
+
+
+def measured_mfma_busy(workload: str):
+    """Fraction of the SIMD cycles of the page walk's launch in which the MFMA
+    pipe is busy (rocprofv3 SQ_VALU_MFMA_BUSY_CYCLES over 1024 SIMDs x the
+    launch's shader cycles), from the committed counter summary of this
+    workload, if it was taken on the current kernel sources, else None."""
+    return profile_value(f"attn_pp_kernel_{workload}_counters.txt", "mfma_busy_fraction")
+
+
+def profile_value(name: str, key: str):
+    """A key: value figure of a committed summary under profiles/, if the
+    summary was taken on the current kernel sources, else None."""
+    path = os.path.join(ROOT, "profiles", name)
     if not os.path.exists(path):
         return None
     kv = {}
@@ -131,7 +146,7 @@ def measured_traffic(workload: str, key: str = "hbm_bytes_per_launch"):
     if kv.get("kernel_source_sha256_16") != kernel_source_hash():
         return None
     try:
-        return int(float(kv[key])) or None
+        return float(kv[key])
     except (KeyError, ValueError):
         return None
 
@@ -279,7 +294,11 @@ def bench_core(args, wl, dev=None):
                                "(mean of per-step HIP event times)",
                      "flops_per_launch": fa,
                      "frac_at_median_launch": round(fa / (float(np.median(t_attn_in)) * 1e-3) / 1e12 / peak, 4),
-                     "frac_back_to_back": round(fa / (float(np.mean(t_attn)) * 1e-3) / 1e12 / peak, 4)},
+                     "frac_back_to_back": round(fa / (float(np.mean(t_attn)) * 1e-3) / 1e12 / peak, 4),
+                     "mfma_busy_frac_counters": measured_mfma_busy(wl.name),
+                     "mfma_busy_note": "share of SIMD cycles with the MFMA pipe busy (rocprof counters, "
+                                       "committed summary); frac above is against the nominal peak, "
+                                       "which assumes the 2.4 GHz clock"},
     }
     return res, layer, dev, sel
 
