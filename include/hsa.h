@@ -128,8 +128,10 @@ size_t hsa_adaptive_workspace_size(const hsa_config_t* cfg, int32_t n_q,
  * work items of one batch entry (256-query tiles x heads), the workgroups
  * of the launch (each walks one of that many equal ranges of the launch's
  * 64-key tiles, at most HSA_PLAN_MAX_CHUNKS; launches of at least
- * 4 x HSA_PLAN_MAX_CHUNKS items take one workgroup per whole item) and the
- * most pieces the ranges cut an item into. Tile-list walk: the work items (128-query tile x key
+ * 4 x HSA_PLAN_MAX_CHUNKS items, and launches of at most HSA_PLAN_MAX_CHUNKS
+ * items whose longest item exceeds a range by at most four tiles, take one
+ * workgroup per whole item) and the most pieces the ranges cut an item
+ * into. Tile-list walk: the work items (128-query tile x key
  * split), the chunks of the launch's schedule table (at most
  * HSA_PLAN_MAX_CHUNKS) and the largest key split of a head. Each output
  * pointer is nullable. Errors: INVALID_ARG, UNSUPPORTED (no schedule fits;

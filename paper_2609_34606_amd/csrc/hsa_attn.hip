@@ -1303,7 +1303,9 @@ namespace {
 // length that fill at least 7/8 of the CUs whole (one or more per range)
 // are not cut: the partial outputs, merges and second prologues of cut
 // items cost more there than the idle CUs. Launches of at least 4 x 256
-// items take one whole item per workgroup (sk_whole): with many items per
+// items, and launches of at most 256 items whose longest item is at most
+// kCutTiles longer than a range, take one whole item per workgroup
+// (sk_whole): with many items per
 // range, the 32 ranges running on an XCD would each walk a different head
 // and share no page in its L2 (30 batched layers of the streaming workload:
 // 17.4 against 14.7 ms per chunk), while the dispatcher's own balancing
@@ -1311,7 +1313,7 @@ namespace {
 // kernel does not read the schedule) takes one range.
 bool plan_stream_k(AttnParams& p, int B, int H, int n_q, int P, const int* list_len, int max_part,
                    bool split) {
-  constexpr int kMaxRanges = 256, kMinTiles = 16, kWholeItems = 4 * kMaxRanges;
+  constexpr int kMaxRanges = 256, kMinTiles = 16, kWholeItems = 4 * kMaxRanges, kCutTiles = 4;
   const int nqt = (n_q + 255) / 256, tpp = (P + kBN - 1) / kBN;
   int64_t per_b = 0;
   for (int h = 0; h < H; ++h) {
@@ -1327,7 +1329,14 @@ bool plan_stream_k(AttnParams& p, int B, int H, int n_q, int P, const int* list_
     const int64_t k = (items + kMaxRanges - 1) / kMaxRanges;  // items per range
     if (items % k == 0 && 8 * (items / k) >= 7 * kMaxRanges) G = items / k;
   }
-  const bool whole = split && items >= kWholeItems && items <= INT32_MAX;
+  // whole items also when the launch holds at most one item per CU and its
+  // longest item is at most a few tiles longer than a range: cutting then
+  // saves less than the second prologue and the merge of a cut item cost
+  // (the Linformer branch over compressed pages: items of 5-19 tiles)
+  int max_len = 1;
+  for (int h = 0; h < H; ++h) max_len = std::max(max_len, std::max(1, list_len[h]) * tpp);
+  const bool whole = split && items <= INT32_MAX &&
+                     (items >= kWholeItems || (items <= kMaxRanges && max_len <= T / G + kCutTiles));
   if (whole) G = items;
   if (!split) G = 1;
   // ranges [0, rm) hold q + 1 tiles, the others q

@@ -472,7 +472,8 @@ def test_stream_k_ranges_cover_every_tile_once():
              (1, 17, 2560, 64, None), (4, 12, 4680, 1560, None), (1, 1, 1, 64, (1,)),
              (1, 3, 257, 64, (1, 1, 1)), (2, 7, 20000, 40, None), (1, 12, 4680, 1560, (7,) * 12),
              (1, 12, 4680, 1560, (4, 19, 11, 5, 5, 19, 5, 11, 11, 11, 7, 11)),
-             (30, 12, 4680, 1560, (11,) * 12), (5, 12, 4680, 1560, None), (4, 12, 4680, 1560, (9,) * 12)]
+             (30, 12, 4680, 1560, (11,) * 12), (5, 12, 4680, 1560, None), (4, 12, 4680, 1560, (9,) * 12),
+             (1, 12, 4680, 64, (5, 7, 11, 19, 5, 19, 5, 11, 11, 11, 7, 11)), (1, 3, 600, 64, (2, 9, 30))]
     for B, H_, n_q, page, lens in cases:
         lens = lens or tuple(int(x) for x in rng.integers(1, 120, H_))
         cfg = P.config(B, H_, 128, page, "bf16")
@@ -480,8 +481,18 @@ def test_stream_k_ranges_cover_every_tile_once():
         assert lib.hsa_attention_plan(ctypes.byref(cfg), n_q, arr, 0, ctypes.byref(n_items),
                                       ctypes.byref(n_chunks), ctypes.byref(widest)) == 0
         G = n_chunks.value
-        whole = B * n_items.value >= 1024
-        if whole:  # one workgroup per whole item
+        items = B * n_items.value
+        tpp = -(-page // 64)
+        T = items // H_ * sum(max(1, x) * tpp for x in lens)
+        g_sk = max(1, min(256, T // 16, 2 * items))
+        if len(set(max(1, x) for x in lens)) == 1:
+            k = -(-items // 256)
+            if items % k == 0 and 8 * (items // k) >= 7 * 256:
+                g_sk = items // k
+        max_len = max(max(1, x) for x in lens) * tpp
+        # one workgroup per whole item: many items, or few short ones
+        whole = items >= 1024 or (items <= 256 and max_len <= T // g_sk + 4)
+        if whole:
             assert G == B * n_items.value and widest.value == 1
         else:
             assert 1 <= G <= 256, G
