@@ -114,19 +114,21 @@ def _rows(n_q, k=192, seed=0):
     return np.unique(np.concatenate([r, [t for t in tail if 0 <= t < n_q]]))
 
 
-@pytest.mark.parametrize("B,H,n_q,P,long_k,short_k", [(1, 17, 2560, 64, 48, 4), (1, 32, 1200, 128, 40, 4),
-                                                     (2, 64, 600, 64, 24, 2)])
-def test_many_heads_split_schedule(B, H, n_q, P, long_k, short_k):
+@pytest.mark.parametrize("B,H,n_q,P,long_k,short_k,d", [(1, 17, 2560, 64, 48, 4, 128), (1, 32, 1200, 128, 40, 4, 128),
+                                                       (2, 64, 600, 64, 24, 2, 128), (3, 5, 700, 96, 30, 2, 64)])
+def test_many_heads_split_schedule(B, H, n_q, P, long_k, short_k, d):
     # More heads than the workloads have (up to the 64 the library takes,
-    # with two batch entries), every third with a long list: the planner
-    # splits those lists (and deals more chunks than there are heads), so the
-    # schedule table, the split merge and the per-head schedule fields are
-    # exercised beyond H = 12. Every output element is compared.
+    # with two batch entries), every third with a long list: the stream-K
+    # ranges cut those items into pieces (more workgroups than heads), so the
+    # piece merge and the per-head schedule fields are exercised beyond
+    # H = 12; three batch entries at d = 64 with pages that straddle tiles
+    # put range boundaries across batch entries. Every output element is
+    # compared.
     import ctypes
     from paper_2609_34606_amd import config, lib
     k_h = tuple(long_k if h % 3 == 0 else short_k for h in range(H))
-    wl = SMALL.replace(batch=B, heads=H, n_q=n_q, page_size=P, n_cand=long_k + 4, n_cur=2, k_h=k_h,
-                       seed=61 + H)
+    wl = SMALL.replace(batch=B, heads=H, head_dim=d, n_q=n_q, page_size=P, n_cand=long_k + 4, n_cur=2,
+                       k_h=k_h, seed=61 + H)
     lens = (ctypes.c_int32 * H)(*[k + 2 for k in k_h])
     items, chunks, widest = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
     cfg = config(B, H, wl.head_dim, P, "bf16")
