@@ -504,12 +504,17 @@ __global__ __launch_bounds__(64 * kW, 8 / kW) void attn_bf16_kernel(AttnParams p
     issue_k_at(1, ev);
     ek = entry(u0 + 2);
     // the query fragments have landed once the three tile copies alone may
-    // be outstanding; pinned, they keep the compiler (which does not see the
-    // copies) from waiting for its own loads inside the walk
+    // be outstanding
     wait_vmcnt<2 * L::kInstK + L::kInstV>();
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) asm volatile("" : "+v"(qf[kk]));
   }
+  // Pinned here, on every path into the walk, the query fragments count as
+  // loaded for the compiler (which does not see the tile copies). Pinned
+  // inside the branch above, the path that skips the walk would leave their
+  // loads pending at the join, and the compiler would then wait for every
+  // outstanding load, the ring's tile copies included, inside each tile's
+  // score products.
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) asm volatile("" : "+v"(qf[kk]));
   // ring slots: kbuf / vbuf of the tile being computed, and of the tiles
   // issued in this iteration (tile + SK - 1 and tile + SV - 1)
   int kbuf = 0, vbuf = 0;
