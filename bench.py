@@ -131,6 +131,15 @@ def measured_mfma_busy(workload: str):
     return profile_value(f"attn_pp_kernel_{workload}_counters.txt", "mfma_busy_fraction")
 
 
+def measured_shader_clock(workload: str):
+    """Shader clock (GHz) of the page walk's launch: its per-shader-engine
+    busy cycles (rocprofv3 SQ_BUSY_CYCLES / 32) over each dispatch's duration
+    from the kernel trace of the same run, from the committed counter
+    summary of this workload, if it was taken on the current kernel sources,
+    else None."""
+    return profile_value(f"attn_pp_kernel_{workload}_counters.txt", "shader_clock_ghz")
+
+
 def profile_value(name: str, key: str):
     """A key: value figure of a committed summary under profiles/, if the
     summary was taken on the current kernel sources, else None."""
@@ -308,6 +317,7 @@ def bench_core(args, wl, dev=None):
                      "frac_at_median_launch": round(fa / (float(np.median(t_attn_in)) * 1e-3) / 1e12 / peak, 4),
                      "frac_back_to_back": round(fa / (float(np.mean(t_attn)) * 1e-3) / 1e12 / peak, 4),
                      "mfma_busy_frac_counters": measured_mfma_busy(wl.name),
+                     "shader_clock_ghz_counters": measured_shader_clock(wl.name),
                      "mfma_busy_note": "share of SIMD cycles with the MFMA pipe busy (rocprof counters, "
                                        "committed summary); frac above is against the nominal peak, "
                                        "which assumes the 2.4 GHz clock"},
