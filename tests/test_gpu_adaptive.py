@@ -230,3 +230,11 @@ def test_c3_long_history_adaptive_full_size():
 
 def test_c4_prompt_switch_adaptive_full_size():
     _full_size("c4", qb_k=4)
+
+
+def test_c3_zero_threshold_full_size():
+    """tau = 0 keeps one key block (one or two 64-key tiles) per query block,
+    while the planner splits the heads' lists by their page counts: many
+    splits of a query block then walk no tile at all, and the merge has to
+    weigh their empty partials out."""
+    _full_size("c3", qb_k=4, tau=(0.0, 0.0))
