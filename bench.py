@@ -449,7 +449,11 @@ def bench_adaptive(args, wl, layer, q, k_h, k_max, sel):
                      "frac": round(achieved / peak, 4),
                      "traffic": measured_traffic(wl.name, "hbm_bytes_per_launch_tile_list"),
                      "kernel": "attn_bf16_kernel, tile-list mode (sparse-branch launch)",
-                     "flops_per_launch": fa},
+                     "flops_per_launch": fa,
+                     "mfma_busy_frac_counters": profile_value(
+                         f"attn_bf16_kernel_tile_list_{wl.name}_counters.txt", "mfma_busy_fraction"),
+                     "shader_clock_ghz_counters": profile_value(
+                         f"attn_bf16_kernel_tile_list_{wl.name}_counters.txt", "shader_clock_ghz")},
     }
 
 
