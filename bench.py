@@ -790,6 +790,40 @@ def bench_sub(args, name):
     return r
 
 
+def measured_ceilings():
+    """Reference ceilings of this GPU, measured with library kernels beside
+    the path's own (none of them is part of the path): the HBM rate of a
+    device copy of 1.2 GB (read + written bytes) and of a fill of the same
+    size (written bytes), and the bf16 matrix rate of a library GEMM of
+    8192 x 8192 x 8192. Medians over 10 runs after 3 warmups. (A library
+    reduction reads far below the copy's rate, so it is no read ceiling.)"""
+    import torch
+    n = 1200 << 20
+    a = torch.ones(n // 2, dtype=torch.bfloat16, device="cuda:0")
+    b = torch.empty_like(a)
+    copy_ms = time_after_warmup(lambda: b.copy_(a), torch)
+    fill_ms = time_after_warmup(lambda: b.fill_(1.0), torch)
+    del a, b
+    m = 8192
+    x = torch.randn((m, m), dtype=torch.bfloat16, device="cuda:0")
+    y = torch.randn((m, m), dtype=torch.bfloat16, device="cuda:0")
+    z = torch.empty((m, m), dtype=torch.bfloat16, device="cuda:0")
+    gemm_ms = time_after_warmup(lambda: torch.matmul(x, y, out=z), torch)
+    del x, y, z
+    torch.cuda.empty_cache()
+    return {"device_copy_tb_s": round(2 * n / (copy_ms * 1e-3) / 1e12, 3),
+            "device_fill_tb_s": round(n / (fill_ms * 1e-3) / 1e12, 3),
+            "gemm_bf16_8192_tflop_s": round(2 * m ** 3 / (gemm_ms * 1e-3) / 1e12, 1),
+            "peaks": {"hbm_tb_s": PEAK_HBM_GBS / 1e3, "bf16_tflop_s": PEAK_BF16_TFLOPS},
+            "note": "library kernels (torch copy and fill, hipBLASLt GEMM), not the path's own"}
+
+
+def time_after_warmup(fn, torch, warmup=3, iters=10):
+    for _ in range(warmup):
+        fn()
+    return time_med(fn, iters, torch)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -804,6 +838,9 @@ def main():
                          "measurements")
     ap.add_argument("--layers", type=int, default=0, help="c5 only: override the layer count")
     ap.add_argument("--chunks", type=int, default=0, help="c5 only: override the chunk count")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip the reference ceilings (a device copy, a fill and a library "
+                         "bf16 GEMM) measured after the workloads")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the run, copy a MIB-sized device buffer 3 times (a plain copy of "
                          "known size, to scale HBM byte counters)")
@@ -826,6 +863,9 @@ def main():
         for name in subs:
             log(f"sub-workload {name} ...")
             res["sub_configs"][name] = bench_sub(args, name)
+    if not args.no_ceilings:
+        log("measured ceilings ...")
+        res["ceilings_measured"] = measured_ceilings()
     if args.copy_calibration:
         import torch
         n = args.copy_calibration << 20
